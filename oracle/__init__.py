@@ -1,0 +1,119 @@
+"""ctypes wrapper of the plain C oracle (liboracle.so).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
+CPU-baseline leg are the only callers. The product path never imports this
+package. Inputs and outputs are numpy arrays on the host.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liboracle.so")
+NB = 32
+
+# Proposed defaults (the paper prints no values for these thresholds).
+XR_DEFAULTS = dict(min_ranks=3, c_min_pair=8, min_kernels=8, k_mad_pm=5189, ratio_pm=1250, alpha_pm=1500,
+                   tau_rank_pm=20)
+L1_DEFAULTS = dict(W=5, theta_pm=1500, beta_pm=1200, rho_pm=1300, cmax_pm=100, min_seg=2)
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        V, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        L.orc_bin.argtypes = [ctypes.c_uint64]
+        L.orc_bin.restype = ctypes.c_int
+        L.orc_summarize.argtypes = [I64, I32, I32, I64] + [V] * 5 + [V] * 5 + [V] * 8
+        L.orc_summarize.restype = I64
+        L.orc_cross_rank.argtypes = [I32, I32, I32, V, V] + [I32] * 7 + [V] * 8 + [V] * 3 + [V] * 4
+        L.orc_cross_rank.restype = ctypes.c_int
+        L.orc_iter_windows.argtypes = [I32, I32, V] + [I32] * 6 + [V] * 5
+        L.orc_iter_windows.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a: np.ndarray) -> int:
+    assert a.flags["C_CONTIGUOUS"], "oracle inputs must be contiguous"
+    return a.ctypes.data
+
+
+def bin_of(d: int) -> int:
+    return lib().orc_bin(d)
+
+
+def summarize(ev: dict, n_kernels: int, n_streams: int, n_events: int | None = None) -> dict:
+    """Exact per-(segment, kernel) group-by. ev: kernel_id, stream, start_ns,
+    end_ns, seg_off (numpy). Returns dict of numpy outputs; 'bad_segments'
+    counts malformed segments."""
+    kid = np.ascontiguousarray(ev["kernel_id"], dtype=np.int32)
+    st = np.ascontiguousarray(ev["stream"], dtype=np.int32)
+    t0 = np.ascontiguousarray(ev["start_ns"], dtype=np.int64)
+    t1 = np.ascontiguousarray(ev["end_ns"], dtype=np.int64)
+    off = np.ascontiguousarray(ev["seg_off"], dtype=np.int64)
+    G = len(off) - 1
+    K, NS = n_kernels, n_streams
+    n = len(kid) if n_events is None else n_events
+    out = {
+        "count": np.empty(G * K, np.uint32), "sum_ns": np.empty(G * K, np.int64),
+        "min_ns": np.empty(G * K, np.int64), "max_ns": np.empty(G * K, np.int64),
+        "hist": np.empty(G * K * NB, np.uint32),
+        "n_valid": np.empty(G, np.uint32), "n_invalid": np.empty(G, np.uint32),
+        "t_first": np.empty(G, np.int64), "t_last": np.empty(G, np.int64), "step_ns": np.empty(G, np.int64),
+        "busy_ns": np.empty(G, np.int64), "stream_busy_ns": np.empty(G * NS, np.int64),
+        "wire_bytes": np.empty(G, np.int64),
+    }
+    bad = lib().orc_summarize(G, K, NS, n, _p(kid), _p(st), _p(t0), _p(t1), _p(off),
+                              *[_p(out[k]) for k in ("count", "sum_ns", "min_ns", "max_ns", "hist", "n_valid",
+                                                     "n_invalid", "t_first", "t_last", "step_ns", "busy_ns",
+                                                     "stream_busy_ns", "wire_bytes")])
+    out["hist"] = out["hist"].reshape(G * K, NB)
+    out["stream_busy_ns"] = out["stream_busy_ns"].reshape(G, NS)
+    out["bad_segments"] = int(bad)
+    return out
+
+
+def cross_rank(count: np.ndarray, sum_ns: np.ndarray, R: int, S: int, K: int, **params) -> dict:
+    p = dict(XR_DEFAULTS, **params)
+    count = np.ascontiguousarray(count, dtype=np.uint32).reshape(-1)
+    sum_ns = np.ascontiguousarray(sum_ns, dtype=np.int64).reshape(-1)
+    assert count.size == R * S * K and sum_ns.size == R * S * K
+    SK, C, RS = S * K, R * S * K, R * S
+    out = {
+        "n_present": np.empty(SK, np.uint32), "med_ns": np.empty(SK, np.int64), "mad_ns": np.empty(SK, np.int64),
+        "q1_ns": np.empty(SK, np.int64), "q3_ns": np.empty(SK, np.int64), "xmean_ns": np.empty(SK, np.float32),
+        "n_flag": np.empty(SK, np.uint32), "n_degraded": np.empty(SK, np.uint32),
+        "z": np.empty(C, np.float32), "mean_ns": np.empty(C, np.float32), "flags": np.empty(C, np.uint8),
+        "score_pm": np.empty(RS, np.int32), "n_eval": np.empty(RS, np.uint32), "n_flag_rank": np.empty(RS, np.uint32),
+        "straggler": np.empty(RS, np.uint8),
+    }
+    rc = lib().orc_cross_rank(R, S, K, _p(count), _p(sum_ns), p["min_ranks"], p["c_min_pair"], p["min_kernels"],
+                              p["k_mad_pm"], p["ratio_pm"], p["alpha_pm"], p["tau_rank_pm"],
+                              *[_p(out[k]) for k in ("n_present", "med_ns", "mad_ns", "q1_ns", "q3_ns", "xmean_ns",
+                                                     "n_flag", "n_degraded", "z", "mean_ns", "flags", "score_pm",
+                                                     "n_eval", "n_flag_rank", "straggler")])
+    if rc != 0:
+        raise RuntimeError(f"orc_cross_rank failed: {rc}")
+    return out
+
+
+def iter_windows(step_ns: np.ndarray, R: int, S: int, **params) -> dict:
+    p = dict(L1_DEFAULTS, **params)
+    y = np.ascontiguousarray(step_ns, dtype=np.int64).reshape(-1)
+    assert y.size == R * S
+    out = {"flags": np.empty(R * S, np.uint8), "cls": np.empty(R, np.uint8), "eff_width": np.empty(R, np.int32),
+           "cp": np.empty(R, np.int32), "cp_ratio": np.empty(R, np.float32)}
+    rc = lib().orc_iter_windows(R, S, _p(y), p["W"], p["theta_pm"], p["beta_pm"], p["rho_pm"], p["cmax_pm"],
+                                p["min_seg"], *[_p(out[k]) for k in ("flags", "cls", "eff_width", "cp", "cp_ratio")])
+    if rc != 0:
+        raise RuntimeError(f"orc_iter_windows failed: {rc}")
+    return out
