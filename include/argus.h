@@ -1,0 +1,234 @@
+/*
+ * libargus: MI355X (gfx950) kernels for the data-parallel hot path of ARGUS
+ * ("ARGUS: Production-Scale Tracing and Performance Diagnosis for over
+ * 10,000-GPU Clusters", arXiv 2606.20374).
+ *
+ *   argus_summarize     raw per-rank kernel-event arrays -> per (rank, step,
+ *                       kernel id) count, sum, min, max and octave histogram
+ *                       of durations, plus per (rank, step) aggregates
+ *                       (section 4.3 record fields; section 5.2 grouping per
+ *                       kernel and rank in each window, log-duration grid).
+ *   argus_cross_rank    summaries -> per (step, kernel) robust cross-rank
+ *                       statistics (lower median, quartiles, MAD), per-cell
+ *                       robust z, outlier / IQR-fence / degraded-pair flags
+ *                       and per (rank, step) straggler decisions (section
+ *                       6.2 and Eq. 4; z-score of Appendix B).
+ *   argus_iter_windows  per-rank step times -> L1 jitter windows, effective
+ *                       width, change point and class (section 6.1,
+ *                       Appendix B).
+ *
+ * Conventions for every entry point:
+ *   - All array pointers are DEVICE pointers owned by the caller. The library
+ *     never allocates or frees device memory; calls that need scratch take a
+ *     caller workspace whose size the matching *_workspace query reports.
+ *   - Calls are asynchronous on the caller's stream (a hipStream_t passed as
+ *     void*; NULL is the default stream). Results are visible after the
+ *     caller synchronises that stream.
+ *   - The return value is a status checked on the host before any launch
+ *     (ARGUS_E*); nothing is launched when it is not ARGUS_OK. Conditions
+ *     that only the device can see (malformed segment offsets, out-of-range
+ *     step times) are OR-ed as ARGUS_DEV_* bits into the optional device
+ *     word *dev_status, which the call first resets to 0.
+ *   - The library writes every element of every non-NULL output, including
+ *     identity values for empty cells, so outputs need no pre-clearing.
+ *   - Calls keep no mutable global state and are safe from several host
+ *     threads on different streams.
+ *   - Integer outputs are exact and deterministic; float outputs are
+ *     computed in double and rounded once to float.
+ */
+#ifndef ARGUS_H
+#define ARGUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ARGUS_ABI_VERSION 1
+#define ARGUS_NBINS 32          /* octave bins per cell */
+#define ARGUS_MAX_KERNELS 65536 /* n_kernels limit */
+#define ARGUS_MAX_STREAMS 64    /* n_streams limit */
+#define ARGUS_MAX_XR_RANKS 16384 /* argus_cross_rank: n_ranks limit */
+#define ARGUS_MAX_XR_KERNELS 16384 /* argus_cross_rank: n_kernels limit */
+#define ARGUS_MAX_L1_STEPS 4096  /* argus_iter_windows: n_steps limit */
+
+enum {
+  ARGUS_OK = 0,
+  ARGUS_EINVAL = -1,      /* NULL pointer, bad dimension, bad parameter, workspace too small */
+  ARGUS_EUNSUPPORTED = -2, /* current device is not gfx950 */
+  ARGUS_EHIP = -3,        /* a HIP launch failed */
+  ARGUS_EDEVICE = -4      /* not returned by calls; names the dev_status channel */
+};
+
+/* device-detected condition bits OR-ed into *dev_status */
+enum {
+  ARGUS_DEV_BAD_SEGMENT = 1, /* some seg_off range was malformed; that segment was summarized as empty */
+  ARGUS_DEV_L1_DOMAIN = 2    /* some rank had a step time outside [0, 2^40) ns; that rank got class 0x80 */
+};
+
+int argus_abi_version(void);
+const char* argus_status_string(int status);
+
+/* ---------------------------------------------------------------- summarize
+ *
+ * Events are structure-of-arrays, grouped into n_ranks * n_steps segments:
+ * segment g = r * n_steps + s covers events [seg_off[g], seg_off[g+1]).
+ * Order within a segment is arbitrary. Total events may exceed 2^31.
+ *
+ * An event is valid iff 0 <= kernel_id < n_kernels, 0 <= stream < n_streams,
+ * start_ns >= 0 and end_ns >= start_ns. Invalid events are only counted in
+ * n_invalid (the paper's collectors drop under backpressure rather than mix
+ * bad records in: Appendix A). For a valid event d = end_ns - start_ns and its
+ * octave bin is 0 for d < 2, else min(floor(log2 d), 31).
+ *
+ * A segment is malformed unless 0 <= seg_off[g] <= seg_off[g+1] <= n_events
+ * and its length is below 2^32; a malformed segment is summarized as empty
+ * and ARGUS_DEV_BAD_SEGMENT is raised. Sums wrap modulo 2^64.
+ */
+typedef struct argus_events {
+  const int32_t* kernel_id; /* [n_events] */
+  const int32_t* stream;    /* [n_events] */
+  const int64_t* start_ns;  /* [n_events] */
+  const int64_t* end_ns;    /* [n_events] */
+  const int64_t* seg_off;   /* [n_ranks * n_steps + 1] */
+  int64_t n_events;         /* length of the four event arrays */
+  int32_t n_ranks, n_steps, n_kernels, n_streams;
+} argus_events_t;
+
+typedef struct argus_summary {
+  /* per cell, [n_ranks][n_steps][n_kernels] (hist: [..][ARGUS_NBINS]) */
+  uint32_t* count;  /* valid events of the kernel */
+  int64_t* sum_ns;  /* sum of d */
+  int64_t* min_ns;  /* min d, INT64_MAX when count == 0 */
+  int64_t* max_ns;  /* max d, INT64_MIN when count == 0 */
+  uint32_t* hist;   /* octave histogram of d */
+  /* per segment, [n_ranks][n_steps] */
+  uint32_t* n_valid;
+  uint32_t* n_invalid;
+  int64_t* t_first;        /* min start of valid events, INT64_MAX when none */
+  int64_t* t_last;         /* max end of valid events, INT64_MIN when none */
+  int64_t* step_ns;        /* t_last - t_first, 0 when no valid event */
+  int64_t* busy_ns;        /* sum of d over valid events */
+  int64_t* stream_busy_ns; /* [n_ranks][n_steps][n_streams] sum of d per stream */
+  int64_t* wire_bytes;     /* optional (may be NULL): bytes of the uploaded summary records:
+                              sum over cells with count > 0 of 33 + 5 * (nonzero bins) */
+  int32_t* dev_status;     /* optional (may be NULL) */
+} argus_summary_t;
+
+size_t argus_summarize_workspace(const argus_events_t* ev);
+
+/* Every output pointer except wire_bytes and dev_status is required. */
+int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* workspace, size_t workspace_bytes,
+                    void* stream);
+
+/* --------------------------------------------------------------- cross-rank
+ *
+ * For each step s and kernel k, over the ranks r where count > 0 ("present"):
+ *   x_r = min(floor((uint64)sum / count), INT64_MAX)    exact integer mean
+ *   n   = number of present ranks
+ * If n < min_ranks the kernel is not evaluated: med = mad = q1 = q3 = -1,
+ * xmean = 0, and its cells get z = 0, flags = 0. Otherwise, with v = sorted x:
+ *   med = v[(n-1)/2], q1 = v[(n-1)/4], q3 = v[3(n-1)/4]   (lower nearest-rank)
+ *   mad = lower median of |x_r - med|,  madf = max(mad, 1)
+ *   xmean = (float)((double)(exact sum of x) / n)
+ * Per present cell of an evaluated kernel (flags bit2 = 1):
+ *   z     = (float)((double)(x - med) / (1.4826 * madf))
+ *   bit0  = count >= c_min_pair && 1000 (x - med) > k_mad_pm * madf && 1000 x >= ratio_pm * med
+ *   bit1  = 1000 (x - q3) > alpha_pm * max(q3 - q1, 1)              (Eq. 4 upper fence)
+ * Per (rank, step), over E = evaluated present kernels with med >= 1:
+ *   score_pm = lower median of min(floor(1000 x / med), INT32_MAX), -1 if E empty
+ *   n_eval = |E|, n_flag_rank = #{k in E with bit0}
+ *   straggler = n_eval >= min_kernels && score_pm >= 1000 + tau_rank_pm
+ * bit3 (degraded pair) = bit0 && !straggler(rank, step).
+ * n_flag / n_degraded per (s, k) count bit0 / bit3 over ranks.
+ * mean_ns of a present cell = (float)((double)sum / count) (0 when absent).
+ */
+typedef struct argus_xr_params {
+  int32_t min_ranks;   /* >= 1, default 3 */
+  int32_t c_min_pair;  /* >= 0, default 8 */
+  int32_t min_kernels; /* >= 0, default 8 */
+  int32_t k_mad_pm;    /* >= 0, default 5189 (modified z 3.5 = 3.5 / 0.6745 MADs) */
+  int32_t ratio_pm;    /* >= 0, default 1250 */
+  int32_t alpha_pm;    /* >= 0, default 1500 (Tukey) */
+  int32_t tau_rank_pm; /* >= -1000, default 20 */
+} argus_xr_params_t;
+
+void argus_xr_default(argus_xr_params_t* p);
+
+typedef struct argus_xr_out {
+  /* per (step, kernel), [n_steps][n_kernels] */
+  uint32_t* n_present;
+  int64_t* med_ns;
+  int64_t* mad_ns;
+  int64_t* q1_ns;
+  int64_t* q3_ns;
+  float* xmean_ns;
+  uint32_t* n_flag;
+  uint32_t* n_degraded;
+  /* per cell, [n_ranks][n_steps][n_kernels] */
+  float* z;
+  float* mean_ns; /* optional (may be NULL) */
+  uint8_t* flags;
+  /* per (rank, step), [n_ranks][n_steps] */
+  int32_t* score_pm;
+  uint32_t* n_eval;
+  uint32_t* n_flag_rank;
+  uint8_t* straggler;
+  int32_t* dev_status; /* optional (may be NULL) */
+} argus_xr_out_t;
+
+size_t argus_cross_rank_workspace(int32_t n_ranks, int32_t n_steps, int32_t n_kernels);
+
+/* count and sum_ns are argus_summary_t outputs ([n_ranks][n_steps][n_kernels]). */
+int argus_cross_rank(const uint32_t* count, const int64_t* sum_ns, int32_t n_ranks, int32_t n_steps,
+                     int32_t n_kernels, const argus_xr_params_t* params, const argus_xr_out_t* out, void* workspace,
+                     size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------- iter windows
+ *
+ * Per rank r over y = step_ns[r][0..n_steps) (valid domain 0 <= y < 2^40):
+ *  1. window width w = min(W, n_steps); window t covers [t, t+w-1]; it is a
+ *     candidate iff 1000 max > theta_pm min.
+ *  2. candidate windows that overlap or touch merge into intervals [a, b];
+ *     their points get flags bit0.
+ *  3. per interval: baseline = lower median of the points outside [a, b]
+ *     (of all points when none lie outside); points with 1000 y > beta_pm *
+ *     baseline get bit1; the interval's width is its longest run of such
+ *     points; eff_width = the largest interval width (0 if none).
+ *  4. change point: split t (left [0, t), right [t, S)), both at least
+ *     min_seg long, is valid iff sum_left > 0, mean_R / mean_L >= rho_pm /
+ *     1000 and both sides have sample (n-1) relative std <= cmax_pm / 1000,
+ *     all tested exactly in integers. The valid split with the largest
+ *     ratio wins (earliest on ties): cp = t, cp_ratio = (float) ratio, and
+ *     steps >= t get bit2; otherwise cp = -1, cp_ratio = 0.
+ *  5. cls = (eff_width > 0) | (cp >= 0) << 1: stable 0, jitter 1,
+ *     regression 2, both 3. A rank with any y outside the domain gets
+ *     cls = 0x80, eff_width 0, cp -1, no flags, and raises ARGUS_DEV_L1_DOMAIN.
+ */
+typedef struct argus_l1_params {
+  int32_t W;        /* >= 1, default 5 */
+  int32_t theta_pm; /* >= 0, default 1500 */
+  int32_t beta_pm;  /* >= 0, default 1200 */
+  int32_t rho_pm;   /* >= 0, default 1300 */
+  int32_t cmax_pm;  /* >= 0, default 100 */
+  int32_t min_seg;  /* >= 1, default 2 */
+} argus_l1_params_t;
+
+void argus_l1_default(argus_l1_params_t* p);
+
+size_t argus_iter_windows_workspace(int32_t n_ranks, int32_t n_steps);
+
+/* cp_ratio and dev_status may be NULL; the other outputs are required. */
+int argus_iter_windows(const int64_t* step_ns, int32_t n_ranks, int32_t n_steps, const argus_l1_params_t* params,
+                       uint8_t* flags /* [n_ranks][n_steps] */, uint8_t* cls /* [n_ranks] */,
+                       int32_t* eff_width /* [n_ranks] */, int32_t* cp /* [n_ranks] */,
+                       float* cp_ratio /* [n_ranks] */, int32_t* dev_status, void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ARGUS_H */

@@ -1,0 +1,206 @@
+"""Thin Python binding of libargus (include/argus.h).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+libargus.so. PyTorch supplies device memory (torch.empty on the GPU) and the
+current stream. There is no CPU fallback: if the library is missing or the
+device is not gfx950 the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libargus.so")
+NBINS = 32
+
+OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
+DEV_BAD_SEGMENT, DEV_L1_DOMAIN = 1, 2
+
+V, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+
+
+class Events(ctypes.Structure):
+    _fields_ = [("kernel_id", V), ("stream", V), ("start_ns", V), ("end_ns", V), ("seg_off", V),
+                ("n_events", I64), ("n_ranks", I32), ("n_steps", I32), ("n_kernels", I32), ("n_streams", I32)]
+
+
+SUMMARY_FIELDS = ["count", "sum_ns", "min_ns", "max_ns", "hist", "n_valid", "n_invalid", "t_first", "t_last",
+                  "step_ns", "busy_ns", "stream_busy_ns", "wire_bytes", "dev_status"]
+
+
+class Summary(ctypes.Structure):
+    _fields_ = [(f, V) for f in SUMMARY_FIELDS]
+
+
+class XrParams(ctypes.Structure):
+    _fields_ = [(f, I32) for f in ("min_ranks", "c_min_pair", "min_kernels", "k_mad_pm", "ratio_pm", "alpha_pm",
+                                   "tau_rank_pm")]
+
+
+XR_FIELDS = ["n_present", "med_ns", "mad_ns", "q1_ns", "q3_ns", "xmean_ns", "n_flag", "n_degraded", "z", "mean_ns",
+             "flags", "score_pm", "n_eval", "n_flag_rank", "straggler", "dev_status"]
+
+
+class XrOut(ctypes.Structure):
+    _fields_ = [(f, V) for f in XR_FIELDS]
+
+
+class L1Params(ctypes.Structure):
+    _fields_ = [(f, I32) for f in ("W", "theta_pm", "beta_pm", "rho_pm", "cmax_pm", "min_seg")]
+
+
+class ArgusError(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def lib():
+    """Load libargus.so; raises if it is not built (no fallback path exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ArgusError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.argus_abi_version.restype = ctypes.c_int
+        L.argus_status_string.argtypes = [ctypes.c_int]
+        L.argus_status_string.restype = ctypes.c_char_p
+        L.argus_summarize_workspace.argtypes = [P(Events)]
+        L.argus_summarize_workspace.restype = ctypes.c_size_t
+        L.argus_summarize.argtypes = [P(Events), P(Summary), V, ctypes.c_size_t, V]
+        L.argus_summarize.restype = ctypes.c_int
+        L.argus_xr_default.argtypes = [P(XrParams)]
+        L.argus_cross_rank_workspace.argtypes = [I32, I32, I32]
+        L.argus_cross_rank_workspace.restype = ctypes.c_size_t
+        L.argus_cross_rank.argtypes = [V, V, I32, I32, I32, P(XrParams), P(XrOut), V, ctypes.c_size_t, V]
+        L.argus_cross_rank.restype = ctypes.c_int
+        L.argus_l1_default.argtypes = [P(L1Params)]
+        L.argus_iter_windows_workspace.argtypes = [I32, I32]
+        L.argus_iter_windows_workspace.restype = ctypes.c_size_t
+        L.argus_iter_windows.argtypes = [V, I32, I32, P(L1Params), V, V, V, V, V, V, V, ctypes.c_size_t, V]
+        L.argus_iter_windows.restype = ctypes.c_int
+        if L.argus_abi_version() != 1:
+            raise ArgusError("libargus ABI version mismatch")
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise ArgusError(f"{what}: {lib().argus_status_string(rc).decode()} ({rc})")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    assert t.is_cuda and t.is_contiguous(), "libargus takes contiguous device tensors"
+    return t.data_ptr()
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def xr_defaults() -> dict:
+    p = XrParams()
+    lib().argus_xr_default(ctypes.byref(p))
+    return {f: getattr(p, f) for f, _ in XrParams._fields_}
+
+
+def l1_defaults() -> dict:
+    p = L1Params()
+    lib().argus_l1_default(ctypes.byref(p))
+    return {f: getattr(p, f) for f, _ in L1Params._fields_}
+
+
+# ------------------------------------------------------------------ summarize
+def alloc_summary(n_ranks: int, n_steps: int, n_kernels: int, n_streams: int, device="cuda") -> dict:
+    G, C = n_ranks * n_steps, n_ranks * n_steps * n_kernels
+    e = lambda n, dt: torch.empty(n, dtype=dt, device=device)  # noqa: E731
+    return {
+        "count": e(C, torch.int32), "sum_ns": e(C, torch.int64), "min_ns": e(C, torch.int64),
+        "max_ns": e(C, torch.int64), "hist": e(C * NBINS, torch.int32),
+        "n_valid": e(G, torch.int32), "n_invalid": e(G, torch.int32), "t_first": e(G, torch.int64),
+        "t_last": e(G, torch.int64), "step_ns": e(G, torch.int64), "busy_ns": e(G, torch.int64),
+        "stream_busy_ns": e(G * n_streams, torch.int64), "wire_bytes": e(G, torch.int64),
+        "dev_status": e(1, torch.int32),
+    }
+
+
+def summarize(ev: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: int,
+              out: Optional[dict] = None) -> dict:
+    """argus_summarize over SoA device tensors ev = {kernel_id, stream,
+    start_ns, end_ns, seg_off}. Unsigned outputs are returned in signed
+    torch dtypes of the same width (reinterpret with .view on the host)."""
+    dev = ev["kernel_id"].device
+    if out is None:
+        out = alloc_summary(n_ranks, n_steps, n_kernels, n_streams, dev)
+    e = Events(_ptr(ev["kernel_id"]), _ptr(ev["stream"]), _ptr(ev["start_ns"]), _ptr(ev["end_ns"]),
+               _ptr(ev["seg_off"]), ev["kernel_id"].numel(), n_ranks, n_steps, n_kernels, n_streams)
+    s = Summary(*[_ptr(out.get(f)) for f in SUMMARY_FIELDS])
+    ws = lib().argus_summarize_workspace(ctypes.byref(e))
+    assert ws == 0
+    _check(lib().argus_summarize(ctypes.byref(e), ctypes.byref(s), None, 0, _stream(dev)), "argus_summarize")
+    return out
+
+
+# ----------------------------------------------------------------- cross-rank
+def alloc_cross_rank(n_ranks: int, n_steps: int, n_kernels: int, device="cuda") -> dict:
+    SK, C, RS = n_steps * n_kernels, n_ranks * n_steps * n_kernels, n_ranks * n_steps
+    e = lambda n, dt: torch.empty(n, dtype=dt, device=device)  # noqa: E731
+    ws = lib().argus_cross_rank_workspace(n_ranks, n_steps, n_kernels)
+    return {
+        "n_present": e(SK, torch.int32), "med_ns": e(SK, torch.int64), "mad_ns": e(SK, torch.int64),
+        "q1_ns": e(SK, torch.int64), "q3_ns": e(SK, torch.int64), "xmean_ns": e(SK, torch.float32),
+        "n_flag": e(SK, torch.int32), "n_degraded": e(SK, torch.int32),
+        "z": e(C, torch.float32), "mean_ns": e(C, torch.float32), "flags": e(C, torch.uint8),
+        "score_pm": e(RS, torch.int32), "n_eval": e(RS, torch.int32), "n_flag_rank": e(RS, torch.int32),
+        "straggler": e(RS, torch.uint8), "dev_status": e(1, torch.int32),
+        "_workspace": e(max(ws, 1), torch.uint8),
+    }
+
+
+def cross_rank(count: torch.Tensor, sum_ns: torch.Tensor, n_ranks: int, n_steps: int, n_kernels: int,
+               out: Optional[dict] = None, **params) -> dict:
+    dev = count.device
+    if out is None:
+        out = alloc_cross_rank(n_ranks, n_steps, n_kernels, dev)
+    p = XrParams()
+    lib().argus_xr_default(ctypes.byref(p))
+    for k, v in params.items():
+        setattr(p, k, v)
+    o = XrOut(*[_ptr(out.get(f)) for f in XR_FIELDS])
+    ws = out["_workspace"]
+    _check(lib().argus_cross_rank(_ptr(count), _ptr(sum_ns), n_ranks, n_steps, n_kernels, ctypes.byref(p),
+                                  ctypes.byref(o), _ptr(ws), ws.numel(), _stream(dev)), "argus_cross_rank")
+    return out
+
+
+# --------------------------------------------------------------- iter windows
+def alloc_iter_windows(n_ranks: int, n_steps: int, device="cuda") -> dict:
+    e = lambda n, dt: torch.empty(n, dtype=dt, device=device)  # noqa: E731
+    return {"flags": e(max(n_ranks * n_steps, 1), torch.uint8), "cls": e(max(n_ranks, 1), torch.uint8),
+            "eff_width": e(max(n_ranks, 1), torch.int32), "cp": e(max(n_ranks, 1), torch.int32),
+            "cp_ratio": e(max(n_ranks, 1), torch.float32), "dev_status": e(1, torch.int32)}
+
+
+def iter_windows(step_ns: torch.Tensor, n_ranks: int, n_steps: int, out: Optional[dict] = None, **params) -> dict:
+    dev = step_ns.device
+    if out is None:
+        out = alloc_iter_windows(n_ranks, n_steps, dev)
+    p = L1Params()
+    lib().argus_l1_default(ctypes.byref(p))
+    for k, v in params.items():
+        setattr(p, k, v)
+    _check(lib().argus_iter_windows(_ptr(step_ns), n_ranks, n_steps, ctypes.byref(p), _ptr(out["flags"]),
+                                    _ptr(out["cls"]), _ptr(out["eff_width"]), _ptr(out["cp"]),
+                                    _ptr(out["cp_ratio"]), _ptr(out["dev_status"]), None, 0, _stream(dev)),
+           "argus_iter_windows")
+    return out

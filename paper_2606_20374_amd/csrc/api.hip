@@ -1,0 +1,170 @@
+// C-ABI host wrapper of libargus: argument checks, workspace sizing and
+// launches on the caller's stream. See include/argus.h for the contract.
+#include <atomic>
+#include <cstring>
+
+#include "argus_internal.h"
+
+namespace argus {
+namespace {
+
+__global__ void clear_status_kernel(int32_t* s) { *s = 0; }
+
+// Per-device cache of "is gfx950": 0 unknown, 1 yes, 2 no.
+std::atomic<int> g_arch_ok[64];
+
+int check_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ARGUS_EHIP;
+  if (dev < 0 || dev >= 64) return ARGUS_EUNSUPPORTED;
+  int v = g_arch_ok[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return ARGUS_EHIP;
+    v = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+    g_arch_ok[dev].store(v, std::memory_order_relaxed);
+  }
+  return v == 1 ? ARGUS_OK : ARGUS_EUNSUPPORTED;
+}
+
+int status_of(hipError_t e) { return e == hipSuccess ? ARGUS_OK : ARGUS_EHIP; }
+
+}  // namespace
+
+hipError_t launch_clear_status(int32_t* dev_status, hipStream_t st) {
+  if (!dev_status) return hipSuccess;
+  hipLaunchKernelGGL(clear_status_kernel, dim3(1), dim3(1), 0, st, dev_status);
+  return hipGetLastError();
+}
+
+}  // namespace argus
+
+using namespace argus;
+
+extern "C" {
+
+int argus_abi_version(void) { return ARGUS_ABI_VERSION; }
+
+const char* argus_status_string(int status) {
+  switch (status) {
+    case ARGUS_OK: return "ok";
+    case ARGUS_EINVAL: return "invalid argument";
+    case ARGUS_EUNSUPPORTED: return "unsupported device (gfx950 required)";
+    case ARGUS_EHIP: return "HIP launch failed";
+    case ARGUS_EDEVICE: return "device-detected condition (see dev_status)";
+    default: return "unknown status";
+  }
+}
+
+size_t argus_summarize_workspace(const argus_events_t* ev) {
+  (void)ev;
+  return 0;
+}
+
+int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* workspace, size_t workspace_bytes,
+                    void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (!ev || !out) return ARGUS_EINVAL;
+  if (ev->n_ranks < 0 || ev->n_steps < 0 || ev->n_events < 0) return ARGUS_EINVAL;
+  if (ev->n_kernels < 1 || ev->n_kernels > ARGUS_MAX_KERNELS) return ARGUS_EINVAL;
+  if (ev->n_streams < 1 || ev->n_streams > ARGUS_MAX_STREAMS) return ARGUS_EINVAL;
+  const int64_t n_seg = (int64_t)ev->n_ranks * ev->n_steps;
+  if (n_seg > INT32_MAX) return ARGUS_EINVAL;
+  if (!ev->seg_off) return ARGUS_EINVAL;
+  if (ev->n_events > 0 && (!ev->kernel_id || !ev->stream || !ev->start_ns || !ev->end_ns)) return ARGUS_EINVAL;
+  if (!out->count || !out->sum_ns || !out->min_ns || !out->max_ns || !out->hist || !out->n_valid ||
+      !out->n_invalid || !out->t_first || !out->t_last || !out->step_ns || !out->busy_ns || !out->stream_busy_ns)
+    return ARGUS_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(out->hist) & 15u) != 0) return ARGUS_EINVAL;  // 16-byte histogram stores
+  int rc = check_device();
+  if (rc != ARGUS_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  rc = status_of(launch_clear_status(out->dev_status, st));
+  if (rc != ARGUS_OK) return rc;
+  SummarizeLaunch l{ev->kernel_id, ev->stream, ev->start_ns, ev->end_ns, ev->seg_off, ev->n_events, (int32_t)n_seg,
+                    ev->n_kernels, ev->n_streams, out->count, out->sum_ns, out->min_ns, out->max_ns, out->hist,
+                    out->n_valid, out->n_invalid, out->t_first, out->t_last, out->step_ns, out->busy_ns,
+                    out->stream_busy_ns, out->wire_bytes, out->dev_status};
+  return status_of(launch_summarize(l, st));
+}
+
+void argus_xr_default(argus_xr_params_t* p) {
+  if (!p) return;
+  p->min_ranks = 3;
+  p->c_min_pair = 8;
+  p->min_kernels = 8;
+  p->k_mad_pm = 5189;
+  p->ratio_pm = 1250;
+  p->alpha_pm = 1500;
+  p->tau_rank_pm = 20;
+}
+
+size_t argus_cross_rank_workspace(int32_t n_ranks, int32_t n_steps, int32_t n_kernels) {
+  if (n_ranks < 0 || n_steps < 0 || n_kernels < 0) return 0;
+  return (size_t)n_ranks * (size_t)n_steps * (size_t)n_kernels * sizeof(int64_t);
+}
+
+int argus_cross_rank(const uint32_t* count, const int64_t* sum_ns, int32_t n_ranks, int32_t n_steps,
+                     int32_t n_kernels, const argus_xr_params_t* params, const argus_xr_out_t* out, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  if (!count || !sum_ns || !params || !out) return ARGUS_EINVAL;
+  if (n_ranks < 1 || n_ranks > ARGUS_MAX_XR_RANKS || n_steps < 1 || n_steps > 65535 || n_kernels < 1 ||
+      n_kernels > ARGUS_MAX_XR_KERNELS)
+    return ARGUS_EINVAL;
+  if ((int64_t)n_ranks * n_steps > INT32_MAX || (int64_t)n_steps * n_kernels > INT32_MAX) return ARGUS_EINVAL;
+  const argus_xr_params_t& p = *params;
+  if (p.min_ranks < 1 || p.c_min_pair < 0 || p.min_kernels < 0 || p.k_mad_pm < 0 || p.ratio_pm < 0 ||
+      p.alpha_pm < 0 || p.tau_rank_pm < -1000)
+    return ARGUS_EINVAL;
+  const argus_xr_out_t& o = *out;
+  if (!o.n_present || !o.med_ns || !o.mad_ns || !o.q1_ns || !o.q3_ns || !o.xmean_ns || !o.n_flag ||
+      !o.n_degraded || !o.z || !o.flags || !o.score_pm || !o.n_eval || !o.n_flag_rank || !o.straggler)
+    return ARGUS_EINVAL;
+  if (!workspace || workspace_bytes < argus_cross_rank_workspace(n_ranks, n_steps, n_kernels)) return ARGUS_EINVAL;
+  int rc = check_device();
+  if (rc != ARGUS_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  rc = status_of(launch_clear_status(o.dev_status, st));
+  if (rc != ARGUS_OK) return rc;
+  CrossRankLaunch l{count, sum_ns, n_ranks, n_steps, n_kernels, p, o, static_cast<int64_t*>(workspace)};
+  return status_of(launch_cross_rank(l, st));
+}
+
+void argus_l1_default(argus_l1_params_t* p) {
+  if (!p) return;
+  p->W = 5;
+  p->theta_pm = 1500;
+  p->beta_pm = 1200;
+  p->rho_pm = 1300;
+  p->cmax_pm = 100;
+  p->min_seg = 2;
+}
+
+size_t argus_iter_windows_workspace(int32_t n_ranks, int32_t n_steps) {
+  (void)n_ranks;
+  (void)n_steps;
+  return 0;
+}
+
+int argus_iter_windows(const int64_t* step_ns, int32_t n_ranks, int32_t n_steps, const argus_l1_params_t* params,
+                       uint8_t* flags, uint8_t* cls, int32_t* eff_width, int32_t* cp, float* cp_ratio,
+                       int32_t* dev_status, void* workspace, size_t workspace_bytes, void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  if (!params || !cls || !eff_width || !cp) return ARGUS_EINVAL;
+  if (n_ranks < 0 || n_steps < 0 || n_steps > ARGUS_MAX_L1_STEPS) return ARGUS_EINVAL;
+  if (n_steps > 0 && n_ranks > 0 && (!step_ns || !flags)) return ARGUS_EINVAL;
+  const argus_l1_params_t& p = *params;
+  if (p.W < 1 || p.theta_pm < 0 || p.beta_pm < 0 || p.rho_pm < 0 || p.cmax_pm < 0 || p.min_seg < 1)
+    return ARGUS_EINVAL;
+  int rc = check_device();
+  if (rc != ARGUS_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  rc = status_of(launch_clear_status(dev_status, st));
+  if (rc != ARGUS_OK) return rc;
+  IterWindowsLaunch l{step_ns, n_ranks, n_steps, p, flags, cls, eff_width, cp, cp_ratio, dev_status};
+  return status_of(launch_iter_windows(l, st));
+}
+
+}  // extern "C"

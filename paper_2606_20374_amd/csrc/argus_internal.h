@@ -1,0 +1,101 @@
+// Internal helpers shared by the libargus kernels and host wrapper.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/argus.h"
+
+namespace argus {
+
+constexpr int NB = ARGUS_NBINS;
+
+// Octave bin of a duration: 0 for d < 2, else floor(log2 d) saturated at 31.
+__device__ __forceinline__ int octave_bin(uint64_t d) {
+  if (d < 2) return 0;
+  int b = 63 - __builtin_clzll(d);
+  return b < NB - 1 ? b : NB - 1;
+}
+
+template <typename T>
+__device__ __forceinline__ T lds_load(T* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+template <typename T>
+__device__ __forceinline__ void lds_store(T* p, T v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// 64-lane wavefront reductions (gfx950 runs wave64 only).
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ long long wave_min_i64(long long v) {
+  for (int o = 32; o > 0; o >>= 1) {
+    long long w = __shfl_xor(v, o, 64);
+    v = w < v ? w : v;
+  }
+  return v;
+}
+__device__ __forceinline__ long long wave_max_i64(long long v) {
+  for (int o = 32; o > 0; o >>= 1) {
+    long long w = __shfl_xor(v, o, 64);
+    v = w > v ? w : v;
+  }
+  return v;
+}
+
+// Launch-side entry points of each kernel file (host code).
+struct SummarizeLaunch {
+  const int32_t* kernel_id;
+  const int32_t* stream;
+  const int64_t* start_ns;
+  const int64_t* end_ns;
+  const int64_t* seg_off;
+  int64_t n_events;
+  int32_t n_seg, n_kernels, n_streams;
+  uint32_t* count;
+  int64_t* sum_ns;
+  int64_t* min_ns;
+  int64_t* max_ns;
+  uint32_t* hist;
+  uint32_t* n_valid;
+  uint32_t* n_invalid;
+  int64_t* t_first;
+  int64_t* t_last;
+  int64_t* step_ns;
+  int64_t* busy_ns;
+  int64_t* stream_busy_ns;
+  int64_t* wire_bytes;
+  int32_t* dev_status;
+};
+hipError_t launch_summarize(const SummarizeLaunch& a, hipStream_t st);
+
+struct CrossRankLaunch {
+  const uint32_t* count;
+  const int64_t* sum_ns;
+  int32_t R, S, K;
+  argus_xr_params_t p;
+  argus_xr_out_t o;
+  int64_t* xT;  // workspace [S][K][R]
+};
+hipError_t launch_cross_rank(const CrossRankLaunch& a, hipStream_t st);
+
+struct IterWindowsLaunch {
+  const int64_t* step_ns;
+  int32_t R, S;
+  argus_l1_params_t p;
+  uint8_t* flags;
+  uint8_t* cls;
+  int32_t* eff_width;
+  int32_t* cp;
+  float* cp_ratio;
+  int32_t* dev_status;
+};
+hipError_t launch_iter_windows(const IterWindowsLaunch& a, hipStream_t st);
+
+hipError_t launch_clear_status(int32_t* dev_status, hipStream_t st);
+
+}  // namespace argus

@@ -1,0 +1,91 @@
+"""Helpers for GPU-vs-oracle parity tests.
+
+Expected values always come from the CPU oracle run on host-generated
+events; the GPU side runs on device-generated events of the same trace
+(byte-identical by construction and checked by checksum).
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+import oracle
+
+NB = 32
+SUM_INT_FIELDS = ["count", "sum_ns", "min_ns", "max_ns", "hist", "n_valid", "n_invalid", "t_first", "t_last",
+                  "step_ns", "busy_ns", "stream_busy_ns", "wire_bytes"]
+XR_INT_FIELDS = ["n_present", "med_ns", "mad_ns", "q1_ns", "q3_ns", "n_flag", "n_degraded", "flags", "score_pm",
+                 "n_eval", "n_flag_rank", "straggler"]
+XR_FLOAT_FIELDS = ["xmean_ns", "z", "mean_ns"]
+L1_INT_FIELDS = ["flags", "cls", "eff_width", "cp"]
+RTOL = 1e-5  # float32 outputs: relative tolerance
+
+
+def host_threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def to_np(t, like=None):
+    a = t.detach().cpu().numpy().reshape(-1)
+    if like is not None and a.dtype != like.dtype and a.dtype.itemsize == like.dtype.itemsize:
+        a = a.view(like.dtype)
+    return a
+
+
+def assert_int_equal(gpu: dict, ref: dict, fields, what=""):
+    for f in fields:
+        r = np.asarray(ref[f]).reshape(-1)
+        g = to_np(gpu[f], r)
+        assert g.shape == r.shape, (what, f, g.shape, r.shape)
+        if not np.array_equal(g, r):
+            bad = np.nonzero(g != r)[0]
+            raise AssertionError(f"{what} {f}: {len(bad)} mismatches, first at {bad[:5]}: gpu {g[bad[:5]]} "
+                                 f"oracle {r[bad[:5]]}")
+
+
+def assert_float_close(gpu: dict, ref: dict, fields, what=""):
+    for f in fields:
+        r = np.asarray(ref[f]).reshape(-1)
+        g = to_np(gpu[f], r)
+        ok = np.abs(g.astype(np.float64) - r.astype(np.float64)) <= RTOL * np.abs(r.astype(np.float64))
+        if not ok.all():
+            bad = np.nonzero(~ok)[0]
+            raise AssertionError(f"{what} {f}: {len(bad)} beyond rtol {RTOL}, first {bad[:5]}: gpu {g[bad[:5]]} "
+                                 f"oracle {r[bad[:5]]}")
+
+
+def oracle_summary_sharded(trace, g_begin=0, g_end=None, chunk=32, n_threads=None) -> dict:
+    """Oracle summaries of segments [g_begin, g_end), regenerated on the host
+    chunk by chunk and summarized by the unmodified single-threaded oracle on
+    disjoint chunks in parallel (segments are independent)."""
+    cfg = trace.cfg
+    K, NS = cfg.n_kernels, cfg.n_streams
+    g_end = cfg.n_segments if g_end is None else g_end
+    G = g_end - g_begin
+    n_threads = n_threads or host_threads()
+    out = {
+        "count": np.empty(G * K, np.uint32), "sum_ns": np.empty(G * K, np.int64),
+        "min_ns": np.empty(G * K, np.int64), "max_ns": np.empty(G * K, np.int64),
+        "hist": np.empty((G * K, NB), np.uint32),
+        "n_valid": np.empty(G, np.uint32), "n_invalid": np.empty(G, np.uint32),
+        "t_first": np.empty(G, np.int64), "t_last": np.empty(G, np.int64), "step_ns": np.empty(G, np.int64),
+        "busy_ns": np.empty(G, np.int64), "stream_busy_ns": np.empty((G, NS), np.int64),
+        "wire_bytes": np.empty(G, np.int64),
+    }
+
+    def work(g0):
+        g1 = min(g_end, g0 + chunk)
+        ev = trace.fill_host(g0, g1, n_threads=1)
+        o = oracle.summarize(ev, K, NS)
+        a, b = g0 - g_begin, g1 - g_begin
+        for f in ("count", "sum_ns", "min_ns", "max_ns", "hist"):
+            out[f][a * K:b * K] = o[f]
+        for f in ("n_valid", "n_invalid", "t_first", "t_last", "step_ns", "busy_ns", "stream_busy_ns",
+                  "wire_bytes"):
+            out[f][a:b] = o[f]
+
+    with ThreadPoolExecutor(n_threads) as ex:
+        list(ex.map(work, range(g_begin, g_end, chunk)))
+    return out

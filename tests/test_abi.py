@@ -1,0 +1,80 @@
+"""The C-ABI library loads and exports every symbol the headers declare;
+host-side argument checks reject bad calls before any launch (no GPU needed)."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+import paper_2606_20374_amd as pa
+from paper_2606_20374_amd import argus as A
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for m in re.finditer(r"^\s*(?:const\s+)?[\w\s\*]+?\b(argus_\w+)\s*\(", text, flags=re.M):
+            names.add(m.group(1))
+    return names
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_functions()
+    assert {"argus_summarize", "argus_cross_rank", "argus_iter_windows", "argus_abi_version"} <= names
+    L = ctypes.CDLL(A.LIB_PATH)
+    for n in sorted(names):
+        assert hasattr(L, n), n
+
+
+def test_version_and_defaults():
+    assert pa.lib().argus_abi_version() == 1
+    assert pa.xr_defaults() == dict(min_ranks=3, c_min_pair=8, min_kernels=8, k_mad_pm=5189, ratio_pm=1250,
+                                     alpha_pm=1500, tau_rank_pm=20)
+    assert pa.l1_defaults() == dict(W=5, theta_pm=1500, beta_pm=1200, rho_pm=1300, cmax_pm=100, min_seg=2)
+    assert pa.lib().argus_status_string(-1) == b"invalid argument"
+
+
+def test_workspace_sizes():
+    assert pa.lib().argus_cross_rank_workspace(10240, 1, 2048) == 10240 * 2048 * 8
+    assert pa.lib().argus_iter_windows_workspace(10, 10) == 0
+
+
+@pytest.mark.parametrize("mutate", [
+    lambda e, s: setattr(e, "n_kernels", 0),
+    lambda e, s: setattr(e, "n_kernels", 65537),
+    lambda e, s: setattr(e, "n_streams", 65),
+    lambda e, s: setattr(e, "n_ranks", -1),
+    lambda e, s: setattr(e, "seg_off", None),
+    lambda e, s: setattr(s, "hist", None),
+    lambda e, s: setattr(s, "hist", 0x1008),  # misaligned histogram
+])
+def test_summarize_rejects_bad_arguments(mutate):
+    e = A.Events(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 10, 2, 2, 4, 2)
+    s = A.Summary(*([0x1000] * 12 + [None, None]))
+    mutate(e, s)
+    assert pa.lib().argus_summarize(ctypes.byref(e), ctypes.byref(s), None, 0, None) == A.EINVAL
+
+
+def test_cross_rank_and_l1_reject_bad_arguments():
+    p = A.XrParams()
+    pa.lib().argus_xr_default(ctypes.byref(p))
+    o = A.XrOut(*([0x1000] * 16))
+    L = pa.lib()
+    assert L.argus_cross_rank(0x1000, 0x1000, 16385, 1, 4, ctypes.byref(p), ctypes.byref(o), 0x1000, 1 << 40,
+                              None) == A.EINVAL
+    assert L.argus_cross_rank(0x1000, 0x1000, 8, 1, 4, ctypes.byref(p), ctypes.byref(o), 0x1000, 8, None) == A.EINVAL
+    p.min_ranks = 0
+    assert L.argus_cross_rank(0x1000, 0x1000, 8, 1, 4, ctypes.byref(p), ctypes.byref(o), 0x1000, 1 << 20,
+                              None) == A.EINVAL
+    q = A.L1Params()
+    L.argus_l1_default(ctypes.byref(q))
+    assert L.argus_iter_windows(0x1000, 4, 4097, ctypes.byref(q), 0x1000, 0x1000, 0x1000, 0x1000, None, None, None,
+                                0, None) == A.EINVAL
+    q.W = 0
+    assert L.argus_iter_windows(0x1000, 4, 8, ctypes.byref(q), 0x1000, 0x1000, 0x1000, 0x1000, None, None, None, 0,
+                                None) == A.EINVAL
