@@ -80,35 +80,48 @@ struct Args {
   int32_t* dev_status;
 };
 
+// Count bin b of a kernel outside its inline window in a full pool record,
+// claiming one for the kernel on first need. Several lanes of one wavefront
+// may race for the same claim; the loser waits until the winner publishes.
+// The loop only exits when no active lane of the wavefront is still pending,
+// so the winner's publish always executes inside the loop body, before any
+// waiting lane of its own wavefront re-reads the state (a per-lane early
+// exit would let the compiler move the publish past the loop, where a
+// waiting lane of the same wavefront could never observe it).
 template <int NSLOT>
 __device__ __forceinline__ void pool_add(Smem<NSLOT>& sm, int slot, uint32_t m, int b) {
+  bool pending = true;
   while (true) {
-    const uint32_t st = (m >> 8) & 0xFFu;
-    if (st == kStPoison) return;
-    if (st != kStNone && st != kStBusy) {
-      atomicAdd(&sm.pool[st - 1][b], 1u);
-      return;
-    }
-    if (st == kStNone) {
-      const uint32_t claim = (m & ~0xFF00u) | (kStBusy << 8);
-      const uint32_t old = atomicCAS(&sm.meta[slot], m, claim);
-      if (old == m) {
-        const uint32_t idx = atomicAdd(&sm.npool, 1u);
-        uint32_t fin;
-        if (idx < (uint32_t)kPool) {
-          atomicAdd(&sm.pool[idx][b], 1u);
-          fin = (m & ~0xFF00u) | ((idx + 1u) << 8);
+    if (pending) {
+      const uint32_t st = (m >> 8) & 0xFFu;
+      if (st == kStPoison) {
+        pending = false;
+      } else if (st != kStNone && st != kStBusy) {
+        atomicAdd(&sm.pool[st - 1][b], 1u);
+        pending = false;
+      } else if (st == kStNone) {
+        const uint32_t claim = (m & ~0xFF00u) | (kStBusy << 8);
+        const uint32_t old = atomicCAS(&sm.meta[slot], m, claim);
+        if (old == m) {
+          const uint32_t idx = atomicAdd(&sm.npool, 1u);
+          uint32_t fin;
+          if (idx < (uint32_t)kPool) {
+            atomicAdd(&sm.pool[idx][b], 1u);
+            fin = (m & ~0xFF00u) | ((idx + 1u) << 8);
+          } else {
+            fin = (m & ~0xFF00u) | (kStPoison << 8);
+            lds_store(&sm.poison, 1u);
+          }
+          atomicExch(&sm.meta[slot], fin);
+          pending = false;
         } else {
-          fin = (m & ~0xFF00u) | (kStPoison << 8);
-          lds_store(&sm.poison, 1u);
+          m = old;
         }
-        atomicExch(&sm.meta[slot], fin);
-        return;
+      } else {
+        m = lds_load(&sm.meta[slot]);
       }
-      m = old;
-    } else {
-      m = lds_load(&sm.meta[slot]);
     }
+    if (!__any(pending)) break;
   }
 }
 
