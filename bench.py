@@ -91,7 +91,9 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="cluster", choices=sorted(WORKLOADS))
-    ap.add_argument("--cpu-sample-ranks", type=int, default=768)
+    ap.add_argument("--cpu-sample-ranks", type=int, default=2560)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES bytes (counter calibration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -106,6 +108,17 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        # a plain copy of known size: reads and writes exactly BYTES each,
+        # the reference for scaling FETCH_SIZE / WRITE_SIZE counters
+        n = args.copy_calibration // 8
+        src = torch.ones(n, dtype=torch.int64, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n * 8}))
+        return
     trace = tracegen.make(args.config)
     cfg = trace.cfg
     R, S, K, NS = cfg.n_ranks, cfg.n_steps, cfg.n_kernels, cfg.n_streams
