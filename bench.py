@@ -45,6 +45,24 @@ def algorithmic_summarize_bytes(n_events: int, present_cells: int, n_seg: int, n
     return 24 * n_events + 156 * present_cells + (48 + 8 * n_streams) * n_seg
 
 
+def measured_traffic(config: str):
+    """HBM bytes per summarize launch from the committed rocprofv3 counter
+    summary, or None when the kernel source changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"summarize_{config}.md")
+    src = os.path.join(ROOT, "paper_2606_20374_amd", "csrc", "summarize.hip")
+    if not os.path.exists(path):
+        return None
+    sha, traffic = None, None
+    for line in open(path):
+        if line.startswith("kernel-source:"):
+            sha = line.split()[-1]
+        elif line.startswith("traffic_bytes_per_launch:"):
+            traffic = int(line.split()[-1])
+    cur = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    return traffic if sha == cur else None
+
+
 def cpu_baseline(trace, sample_ranks: int, gpu_sum: dict) -> dict:
     """Oracle (single-threaded, as it stands) on the first sample_ranks ranks
     of the same workload; also checks the GPU summaries of those ranks."""
@@ -197,7 +215,7 @@ def main():
         "cross_rank_ms_per_step": float(np.mean(xr_ms)) / S,
         "iter_windows_ms": float(np.mean(l1_ms)),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config),
                      "kernel": "summarize_kernel", "algorithmic_bytes_per_launch": alg_bytes},
         "detection": {"stragglers_recovered": strag_ok, "pairs_recovered": pairs_ok,
                       "n_flagged_ranks": int(strag.sum())},
