@@ -8,17 +8,20 @@
 //
 // Design (gfx950):
 // * One 1024-thread workgroup owns one rank-step segment and streams its
-//   structure-of-arrays events from HBM once, with coalesced non-temporal
-//   loads, four events per thread in flight per iteration.
-// * Per-kernel state is privatised in LDS: 64-bit sum, min and max, and an
-//   8-bin window of the octave histogram anchored at the first duration seen
-//   for that kernel (lognormal kernels span two or three octaves). Bins
+//   structure-of-arrays events from HBM exactly once: 16-byte non-temporal
+//   loads of four consecutive events per thread, software pipelined so the
+//   next group is in flight while the current one is processed.
+// * Per-kernel state is privatised in LDS: 64-bit sum, min and max, and a
+//   WIN-bin window of the octave histogram anchored at the first duration
+//   seen for that kernel (lognormal kernels span two or three octaves). Bins
 //   outside the window go to a small pool of full 32-bin records that a
-//   kernel claims on first need. If the pool runs dry the kernel is marked
-//   and redone exactly in another pass over the segment, so the result is
-//   exact for every input; typical traces need one pass.
-// * Up to 2048 kernel ids are held per pass; larger id spaces are covered in
-//   id ranges, one pass each.
+//   kernel claims on first need.
+// * Kernel ids map to LDS slots directly when the id space fits (dense), or
+//   through an LDS id->slot map that hands out slots on first sight
+//   (mapped), so a large, sparse id space still takes one pass.
+// * Whenever the pool or the slots run out, the kernels concerned are
+//   marked and redone exactly in another pass over the segment: the result
+//   is exact for every input; typical traces need one pass.
 // * Per-segment aggregates (valid/invalid counts, first start, last end,
 //   busy time) are kept in registers and reduced once per segment; per-stream
 //   busy time uses LDS atomics.
@@ -29,31 +32,39 @@
 namespace argus {
 namespace {
 
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef long long v2l __attribute__((ext_vector_type(2)));
+
 constexpr int kThreads = 1024;
-constexpr int kUnroll = 4;
-constexpr int kWin = 8;        // histogram bins held inline per kernel
-constexpr int kPool = 32;      // full 32-bin records per pass
+constexpr int kPool = 32;  // full 32-bin records per pass
 constexpr uint32_t kBaseUnset = 0xFFu;
 constexpr uint32_t kStNone = 0, kStBusy = 0xFE, kStPoison = 0xFF;
 constexpr uint32_t kDone = 1u << 16;
+constexpr int kMapIds = 16384;  // ids per pass in mapped mode
+constexpr uint32_t kMapEmpty = 0xFFFF, kMapBusy = 0xFFFE, kMapDefer = 0xFFFD, kMapDone = 0xFFFC;
 
 // meta word of a slot: bits 0-7 window base bin (0xFF unset), bits 8-15
 // full-record state (0 none, 1..kPool record index + 1, 0xFE being claimed,
 // 0xFF pool exhausted: redo in another pass), bit 16 already written.
+//
+// map entry (mapped mode, 16 bits, two per 32-bit word): a slot index, or
+// empty / being claimed / deferred to another pass / already written.
 
-template <int NSLOT>
+template <int NSLOT, int WIN, bool MAPPED>
 struct Smem {
   unsigned long long sum[NSLOT];
   long long mn[NSLOT];
   long long mx[NSLOT];
-  uint32_t win[NSLOT][kWin];
+  uint32_t win[NSLOT][WIN];
   uint32_t meta[NSLOT];
   uint32_t pool[kPool][NB];
   unsigned long long stream_busy[ARGUS_MAX_STREAMS];
+  uint32_t map[MAPPED ? kMapIds / 2 : 1];
+  uint16_t slot_kid[MAPPED ? NSLOT : 1];
   unsigned long long red_busy, red_wire;
   long long red_first, red_last;
   uint32_t red_valid, red_invalid;
-  uint32_t npool, poison;
+  uint32_t npool, poison, nslots;
 };
 
 struct Args {
@@ -64,6 +75,7 @@ struct Args {
   const int64_t* seg_off;
   int64_t n_events;
   int32_t n_kernels, n_streams;
+  int32_t vec_ok;  // event arrays 16-byte aligned: vector loads allowed
   uint32_t* count;
   int64_t* sum_ns;
   int64_t* min_ns;
@@ -80,86 +92,183 @@ struct Args {
   int32_t* dev_status;
 };
 
-// Count bin b of a kernel outside its inline window in a full pool record,
-// claiming one for the kernel on first need. Several lanes of one wavefront
-// may race for the same claim; the loser waits until the winner publishes.
-// The loop only exits when no active lane of the wavefront is still pending,
-// so the winner's publish always executes inside the loop body, before any
-// waiting lane of its own wavefront re-reads the state (a per-lane early
-// exit would let the compiler move the publish past the loop, where a
-// waiting lane of the same wavefront could never observe it).
-template <int NSLOT>
-__device__ __forceinline__ void pool_add(Smem<NSLOT>& sm, int slot, uint32_t m, int b) {
-  bool pending = true;
-  while (true) {
-    if (pending) {
-      const uint32_t st = (m >> 8) & 0xFFu;
-      if (st == kStPoison) {
-        pending = false;
-      } else if (st != kStNone && st != kStBusy) {
-        atomicAdd(&sm.pool[st - 1][b], 1u);
-        pending = false;
-      } else if (st == kStNone) {
-        const uint32_t claim = (m & ~0xFF00u) | (kStBusy << 8);
-        const uint32_t old = atomicCAS(&sm.meta[slot], m, claim);
-        if (old == m) {
-          const uint32_t idx = atomicAdd(&sm.npool, 1u);
-          uint32_t fin;
-          if (idx < (uint32_t)kPool) {
-            atomicAdd(&sm.pool[idx][b], 1u);
-            fin = (m & ~0xFF00u) | ((idx + 1u) << 8);
-          } else {
-            fin = (m & ~0xFF00u) | (kStPoison << 8);
-            lds_store(&sm.poison, 1u);
+template <int NSLOT, int WIN, bool MAPPED>
+struct Seg {
+  using S = Smem<NSLOT, WIN, MAPPED>;
+  S& sm;
+
+  __device__ __forceinline__ uint16_t map_get(int lk) const {
+    return reinterpret_cast<const uint16_t*>(sm.map)[lk];
+  }
+  __device__ __forceinline__ void map_set(int lk, uint16_t v) { reinterpret_cast<uint16_t*>(sm.map)[lk] = v; }
+
+  // Slot of local id lk, claiming one on first sight (mapped mode); -1 when
+  // the id is already written or deferred to another pass. Lanes of one
+  // wavefront may race for the same claim; the loop exits only when no
+  // active lane is still pending, so a winner's publish executes inside the
+  // loop, before a waiting lane of its own wavefront re-reads the entry.
+  __device__ int map_claim(int lk, uint32_t e) {
+    uint32_t* w = &sm.map[lk >> 1];
+    const int sh = (lk & 1) * 16;
+    int res = -2;
+    while (true) {
+      if (res == -2) {
+        if (e < (uint32_t)NSLOT) {
+          res = (int)e;
+        } else if (e == kMapDone || e == kMapDefer) {
+          res = -1;
+        } else if (e == kMapEmpty) {
+          const uint32_t word = lds_load(w);
+          if (((word >> sh) & 0xFFFFu) == kMapEmpty) {
+            const uint32_t want = (word & ~(0xFFFFu << sh)) | (kMapBusy << sh);
+            if (atomicCAS(w, word, want) == word) {
+              const uint32_t s = atomicAdd(&sm.nslots, 1u);
+              uint32_t fin;
+              if (s < (uint32_t)NSLOT) {
+                sm.slot_kid[s] = (uint16_t)lk;
+                fin = s;
+                res = (int)s;
+              } else {
+                fin = kMapDefer;
+                lds_store(&sm.poison, 1u);
+                res = -1;
+              }
+              // our half is BUSY and only we change it: flip it to fin
+              atomicXor(w, (kMapBusy ^ fin) << sh);
+            }
           }
-          atomicExch(&sm.meta[slot], fin);
-          pending = false;
-        } else {
-          m = old;
+          if (res == -2) e = (lds_load(w) >> sh) & 0xFFFFu;
+        } else {  // being claimed by another lane
+          e = (lds_load(w) >> sh) & 0xFFFFu;
         }
+      }
+      if (!__any(res == -2)) break;
+    }
+    return res;
+  }
+
+  // Count bin b outside the inline window in a full pool record, claiming
+  // one for the slot on first need (same exit discipline as map_claim).
+  __device__ void pool_add(int slot, uint32_t m, int b) {
+    bool pending = true;
+    while (true) {
+      if (pending) {
+        const uint32_t st = (m >> 8) & 0xFFu;
+        if (st == kStPoison) {
+          pending = false;
+        } else if (st != kStNone && st != kStBusy) {
+          atomicAdd(&sm.pool[st - 1][b], 1u);
+          pending = false;
+        } else if (st == kStNone) {
+          const uint32_t claim = (m & ~0xFF00u) | (kStBusy << 8);
+          const uint32_t old = atomicCAS(&sm.meta[slot], m, claim);
+          if (old == m) {
+            const uint32_t idx = atomicAdd(&sm.npool, 1u);
+            uint32_t fin;
+            if (idx < (uint32_t)kPool) {
+              atomicAdd(&sm.pool[idx][b], 1u);
+              fin = (m & ~0xFF00u) | ((idx + 1u) << 8);
+            } else {
+              fin = (m & ~0xFF00u) | (kStPoison << 8);
+              lds_store(&sm.poison, 1u);
+            }
+            atomicExch(&sm.meta[slot], fin);
+            pending = false;
+          } else {
+            m = old;
+          }
+        } else {
+          m = lds_load(&sm.meta[slot]);
+        }
+      }
+      if (!__any(pending)) break;
+    }
+  }
+
+  __device__ __forceinline__ void slot_add(int slot, uint32_t m, uint64_t d) {
+    if (m & kDone) return;
+    const int b = octave_bin(d);
+    if ((m & 0xFFu) == kBaseUnset) {
+      int base = b - WIN / 2 + 1;
+      base = base < 0 ? 0 : (base > NB - WIN ? NB - WIN : base);
+      const uint32_t want = (m & ~0xFFu) | (uint32_t)base;
+      const uint32_t old = atomicCAS(&sm.meta[slot], m, want);
+      m = (old == m) ? want : old;
+    }
+    const int off = b - (int)(m & 0xFFu);
+    if ((unsigned)off < (unsigned)WIN)
+      atomicAdd(&sm.win[slot][off], 1u);
+    else
+      pool_add(slot, m, b);
+    atomicAdd(&sm.sum[slot], (unsigned long long)d);
+    atomicMin(&sm.mn[slot], (long long)d);
+    atomicMax(&sm.mx[slot], (long long)d);
+  }
+
+  __device__ __forceinline__ void slot_reset(int s) {
+    sm.sum[s] = 0;
+    sm.mn[s] = INT64_MAX;
+    sm.mx[s] = INT64_MIN;
+#pragma unroll
+    for (int w = 0; w < WIN; ++w) sm.win[s][w] = 0;
+    sm.meta[s] = kBaseUnset;
+  }
+};
+
+// Four events of one thread: validity, per-segment aggregates, then the
+// per-kernel updates with the LDS lookups of all four issued up front.
+template <int NSLOT, int WIN, bool MAPPED>
+__device__ __forceinline__ void process4(Seg<NSLOT, WIN, MAPPED>& sg, const Args& a, const int32_t (&kid)[4],
+                                         const int32_t (&st)[4], const int64_t (&t0)[4], const int64_t (&t1)[4],
+                                         int n, bool first_scan, int kb, int nk, uint32_t& nv, uint32_t& ni,
+                                         unsigned long long& busy, long long& tf, long long& tl) {
+  uint64_t d[4];
+  int lk[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const bool valid =
+        j < n && kid[j] >= 0 && kid[j] < a.n_kernels && st[j] >= 0 && st[j] < a.n_streams && t0[j] >= 0 && t1[j] >= t0[j];
+    d[j] = (uint64_t)t1[j] - (uint64_t)t0[j];
+    if (first_scan && j < n) {
+      if (valid) {
+        nv++;
+        busy += d[j];
+        tf = t0[j] < tf ? t0[j] : tf;
+        tl = t1[j] > tl ? t1[j] : tl;
+        atomicAdd(&sg.sm.stream_busy[st[j]], (unsigned long long)d[j]);
       } else {
-        m = lds_load(&sm.meta[slot]);
+        ni++;
       }
     }
-    if (!__any(pending)) break;
+    lk[j] = valid && (unsigned)(kid[j] - kb) < (unsigned)nk ? kid[j] - kb : -1;
   }
-}
-
-template <int NSLOT>
-__device__ __forceinline__ void slot_add(Smem<NSLOT>& sm, int slot, uint64_t d) {
-  uint32_t m = lds_load(&sm.meta[slot]);
-  if (m & kDone) return;
-  const int b = octave_bin(d);
-  if ((m & 0xFFu) == kBaseUnset) {
-    int base = b - 3;
-    base = base < 0 ? 0 : (base > NB - kWin ? NB - kWin : base);
-    const uint32_t want = (m & ~0xFFu) | (uint32_t)base;
-    const uint32_t old = atomicCAS(&sm.meta[slot], m, want);
-    m = (old == m) ? want : old;
-  }
-  const int off = b - (int)(m & 0xFFu);
-  if ((unsigned)off < (unsigned)kWin)
-    atomicAdd(&sm.win[slot][off], 1u);
-  else
-    pool_add(sm, slot, m, b);
-  atomicAdd(&sm.sum[slot], (unsigned long long)d);
-  atomicMin(&sm.mn[slot], (long long)d);
-  atomicMax(&sm.mx[slot], (long long)d);
-}
-
-template <int NSLOT>
-__device__ __forceinline__ void slot_reset(Smem<NSLOT>& sm, int slot) {
-  sm.sum[slot] = 0;
-  sm.mn[slot] = INT64_MAX;
-  sm.mx[slot] = INT64_MIN;
+  int slot[4];
+  if (MAPPED) {
+    uint32_t e[4];
 #pragma unroll
-  for (int w = 0; w < kWin; ++w) sm.win[slot][w] = 0;
-  sm.meta[slot] = kBaseUnset;
+    for (int j = 0; j < 4; ++j) e[j] = lk[j] >= 0 ? sg.map_get(lk[j]) : kMapDone;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) slot[j] = e[j] < (uint32_t)NSLOT ? (int)e[j] : -1;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (lk[j] >= 0 && e[j] >= (uint32_t)NSLOT && e[j] != kMapDone && e[j] != kMapDefer)
+        slot[j] = sg.map_claim(lk[j], e[j]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) slot[j] = lk[j];
+  }
+  uint32_t m[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) m[j] = slot[j] >= 0 ? sg.sm.meta[slot[j]] : 0u;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    if (slot[j] >= 0) sg.slot_add(slot[j], m[j], d[j]);
 }
 
-template <int NSLOT>
+template <int NSLOT, int WIN, bool MAPPED>
 __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
-  __shared__ Smem<NSLOT> sm;
+  __shared__ Smem<NSLOT, WIN, MAPPED> sm;
+  Seg<NSLOT, WIN, MAPPED> sg{sm};
   const int tid = threadIdx.x;
   const int64_t g = blockIdx.x;
   const int32_t K = a.n_kernels, NS = a.n_streams;
@@ -180,68 +289,127 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
     sm.red_invalid = 0;
   }
 
+  // aligned part [a4, b4) in 4-event groups; head [lo, a4) and tail [b4, hi)
+  int64_t a4 = lo, b4 = lo;
+  if (a.vec_ok) {
+    const int64_t up = (lo + 3) & ~(int64_t)3, dn = hi & ~(int64_t)3;
+    a4 = up < hi ? up : hi;
+    b4 = dn > a4 ? dn : a4;
+  }
+  const int64_t qa = a4 >> 2, qb = b4 >> 2;
+  const v4i* K4 = reinterpret_cast<const v4i*>(a.kernel_id);
+  const v4i* S4 = reinterpret_cast<const v4i*>(a.stream);
+  const v2l* T0 = reinterpret_cast<const v2l*>(a.start_ns);
+  const v2l* T1 = reinterpret_cast<const v2l*>(a.end_ns);
+
   uint32_t nv = 0, ni = 0;
   unsigned long long busy = 0, wire = 0;
   long long tf = INT64_MAX, tl = INT64_MIN;
   bool first_scan = true;
+  constexpr int kRange = MAPPED ? kMapIds : NSLOT;
 
-  for (int32_t kb = 0; kb < K; kb += NSLOT) {
-    const int nk = K - kb < NSLOT ? K - kb : NSLOT;
-    for (int s = tid; s < nk; s += kThreads) slot_reset(sm, s);
+  for (int32_t kb = 0; kb < K; kb += kRange) {
+    const int nk = K - kb < kRange ? K - kb : kRange;
+    if (MAPPED)
+      for (int i = tid; i < kMapIds / 2; i += kThreads) sm.map[i] = 0xFFFFFFFFu;
+    else
+      for (int s = tid; s < nk; s += kThreads) sg.slot_reset(s);
     while (true) {
+      // mapped mode hands out slots afresh in every pass
+      if (MAPPED)
+        for (int s = tid; s < NSLOT; s += kThreads) sg.slot_reset(s);
       for (int i = tid; i < kPool * NB; i += kThreads) (&sm.pool[0][0])[i] = 0;
       if (tid == 0) {
         sm.npool = 0;
         sm.poison = 0;
+        sm.nslots = 0;
       }
       __syncthreads();
 
-      for (int64_t i0 = lo; i0 < hi; i0 += (int64_t)kUnroll * kThreads) {
-        int32_t kid[kUnroll], st[kUnroll];
-        int64_t t0[kUnroll], t1[kUnroll];
-        bool in[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-          const int64_t i = i0 + (int64_t)u * kThreads + tid;
-          in[u] = i < hi;
-          if (in[u]) {
-            kid[u] = __builtin_nontemporal_load(a.kernel_id + i);
-            st[u] = __builtin_nontemporal_load(a.stream + i);
-            t0[u] = __builtin_nontemporal_load(a.start_ns + i);
-            t1[u] = __builtin_nontemporal_load(a.end_ns + i);
-          }
+      // unaligned head and tail: at most 3 events each, on the first threads
+      if (a.vec_ok) {
+        int32_t kid[4], st[4];
+        int64_t t0[4], t1[4];
+        int n = 0;
+        const int64_t h = a4 - lo, t = hi - b4;
+        const int64_t i = tid < h ? lo + tid : (tid - h < t ? b4 + (tid - h) : -1);
+        if (i >= 0) {
+          kid[0] = a.kernel_id[i];
+          st[0] = a.stream[i];
+          t0[0] = a.start_ns[i];
+          t1[0] = a.end_ns[i];
+          n = 1;
         }
+        for (int j = n; j < 4; ++j) {
+          kid[j] = -1;
+          st[j] = 0;
+          t0[j] = t1[j] = 0;
+        }
+        if (n) process4(sg, a, kid, st, t0, t1, n, first_scan, kb, nk, nv, ni, busy, tf, tl);
+      }
+      if (!a.vec_ok) {
+        // scalar fallback for unaligned arrays: four strided events per thread
+        for (int64_t i0 = lo + tid; i0 < hi; i0 += 4ll * kThreads) {
+          int32_t kid[4], st[4];
+          int64_t t0[4], t1[4];
+          int n = 0;
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-          if (!in[u]) continue;
-          const bool valid = kid[u] >= 0 && kid[u] < K && st[u] >= 0 && st[u] < NS && t0[u] >= 0 && t1[u] >= t0[u];
-          const uint64_t d = (uint64_t)t1[u] - (uint64_t)t0[u];
-          if (first_scan) {
-            if (valid) {
-              nv++;
-              busy += d;
-              tf = t0[u] < tf ? t0[u] : tf;
-              tl = t1[u] > tl ? t1[u] : tl;
-              atomicAdd(&sm.stream_busy[st[u]], (unsigned long long)d);
-            } else {
-              ni++;
-            }
+          for (int j = 0; j < 4; ++j) {
+            const int64_t i = i0 + (int64_t)j * kThreads;  // in range for a prefix of j
+            const bool in = i < hi;
+            kid[j] = in ? a.kernel_id[i] : -1;
+            st[j] = in ? a.stream[i] : 0;
+            t0[j] = in ? a.start_ns[i] : 0;
+            t1[j] = in ? a.end_ns[i] : 0;
+            n += in;
           }
-          const int slot = kid[u] - kb;
-          if (valid && (unsigned)slot < (unsigned)nk) slot_add(sm, slot, d);
+          process4(sg, a, kid, st, t0, t1, n, first_scan, kb, nk, nv, ni, busy, tf, tl);
+        }
+      }
+      // aligned body: group q holds events 4q..4q+3; the next group's loads
+      // are issued before the current group is processed
+      {
+        int64_t q = qa + tid;
+        v4i nk4 = 0, ns4 = 0;
+        v2l na0 = 0, na1 = 0, nb0 = 0, nb1 = 0;
+        if (q < qb) {
+          nk4 = __builtin_nontemporal_load(K4 + q);
+          ns4 = __builtin_nontemporal_load(S4 + q);
+          na0 = __builtin_nontemporal_load(T0 + 2 * q);
+          na1 = __builtin_nontemporal_load(T0 + 2 * q + 1);
+          nb0 = __builtin_nontemporal_load(T1 + 2 * q);
+          nb1 = __builtin_nontemporal_load(T1 + 2 * q + 1);
+        }
+        while (q < qb) {
+          const int32_t kid[4] = {nk4.x, nk4.y, nk4.z, nk4.w};
+          const int32_t st[4] = {ns4.x, ns4.y, ns4.z, ns4.w};
+          const int64_t t0[4] = {na0.x, na0.y, na1.x, na1.y};
+          const int64_t t1[4] = {nb0.x, nb0.y, nb1.x, nb1.y};
+          const int64_t qn = q + kThreads;
+          if (qn < qb) {
+            nk4 = __builtin_nontemporal_load(K4 + qn);
+            ns4 = __builtin_nontemporal_load(S4 + qn);
+            na0 = __builtin_nontemporal_load(T0 + 2 * qn);
+            na1 = __builtin_nontemporal_load(T0 + 2 * qn + 1);
+            nb0 = __builtin_nontemporal_load(T1 + 2 * qn);
+            nb1 = __builtin_nontemporal_load(T1 + 2 * qn + 1);
+          }
+          process4(sg, a, kid, st, t0, t1, 4, first_scan, kb, nk, nv, ni, busy, tf, tl);
+          q = qn;
         }
       }
       first_scan = false;
       __syncthreads();
 
       // flush: per-kernel scalars and wire size
-      for (int s = tid; s < nk; s += kThreads) {
+      const int nslot = MAPPED ? (int)(sm.nslots < (uint32_t)NSLOT ? sm.nslots : NSLOT) : nk;
+      for (int s = tid; s < nslot; s += kThreads) {
         const uint32_t m = sm.meta[s];
         const uint32_t pst = (m >> 8) & 0xFFu;
         if ((m & kDone) || pst == kStPoison) continue;
         uint32_t cnt = 0, nnz = 0;
 #pragma unroll
-        for (int w = 0; w < kWin; ++w) {
+        for (int w = 0; w < WIN; ++w) {
           cnt += sm.win[s][w];
           nnz += sm.win[s][w] != 0;
         }
@@ -251,15 +419,15 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
             nnz += sm.pool[pst - 1][b] != 0;
           }
         }
-        const int64_t c = g * K + kb + s;
+        const int64_t c = g * K + kb + (MAPPED ? (int)sm.slot_kid[s] : s);
         a.count[c] = cnt;
         a.sum_ns[c] = (int64_t)sm.sum[s];
         a.min_ns[c] = sm.mn[s];
         a.max_ns[c] = sm.mx[s];
         if (cnt) wire += 33u + 5u * nnz;
       }
-      // flush: histograms, four bins per thread, coalesced 16-byte stores
-      for (int it = tid; it < nk * (NB / 4); it += kThreads) {
+      // flush: histograms, four bins per thread, 16-byte stores
+      for (int it = tid; it < nslot * (NB / 4); it += kThreads) {
         const int s = it >> 3, q = it & 7;
         const uint32_t m = sm.meta[s];
         const uint32_t pst = (m >> 8) & 0xFFu;
@@ -270,25 +438,49 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         for (int j = 0; j < 4; ++j) {
           const int b = 4 * q + j;
           const int off = b - base;
-          v[j] = (base != (int)kBaseUnset && (unsigned)off < (unsigned)kWin) ? sm.win[s][off] : 0u;
+          v[j] = (base != (int)kBaseUnset && (unsigned)off < (unsigned)WIN) ? sm.win[s][off] : 0u;
           if (pst != kStNone) v[j] += sm.pool[pst - 1][b];
         }
-        const int64_t c = g * K + kb + s;
+        const int64_t c = g * K + kb + (MAPPED ? (int)sm.slot_kid[s] : s);
         *reinterpret_cast<uint4*>(a.hist + c * NB + 4 * q) = make_uint4(v[0], v[1], v[2], v[3]);
       }
       __syncthreads();
       const bool again = sm.poison != 0;
-      // mark written kernels done; kernels that found the pool empty start over
-      for (int s = tid; s < nk; s += kThreads) {
+      // mark what was written; kernels that ran out of room start over
+      for (int s = tid; s < nslot; s += kThreads) {
         const uint32_t m = sm.meta[s];
         if (m & kDone) continue;
-        if (((m >> 8) & 0xFFu) == kStPoison)
-          slot_reset(sm, s);
-        else
+        const bool redo = ((m >> 8) & 0xFFu) == kStPoison;
+        if (MAPPED) {
+          sg.map_set(sm.slot_kid[s], redo ? (uint16_t)kMapEmpty : (uint16_t)kMapDone);
+        } else if (redo) {
+          sg.slot_reset(s);
+        } else {
           sm.meta[s] = m | kDone;
+        }
       }
+      if (MAPPED)
+        for (int i = tid; i < nk; i += kThreads)
+          if (sg.map_get(i) == kMapDefer) sg.map_set(i, (uint16_t)kMapEmpty);
       __syncthreads();
       if (!again) break;
+    }
+    if (MAPPED) {
+      // identity values for the ids of this range that never occurred
+      for (int i = tid; i < nk; i += kThreads) {
+        if (sg.map_get(i) != kMapEmpty) continue;
+        const int64_t c = g * K + kb + i;
+        a.count[c] = 0;
+        a.sum_ns[c] = 0;
+        a.min_ns[c] = INT64_MAX;
+        a.max_ns[c] = INT64_MIN;
+      }
+      for (int it = tid; it < nk * (NB / 4); it += kThreads) {
+        if (sg.map_get(it >> 3) != kMapEmpty) continue;
+        const int64_t c = g * K + kb + (it >> 3);
+        *reinterpret_cast<uint4*>(a.hist + c * NB + 4 * (it & 7)) = make_uint4(0u, 0u, 0u, 0u);
+      }
+      __syncthreads();
     }
   }
 
@@ -317,22 +509,27 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
   if (tid < NS) a.stream_busy_ns[g * NS + tid] = (int64_t)sm.stream_busy[tid];
 }
 
-template <int NSLOT>
+template <int NSLOT, int WIN, bool MAPPED>
 hipError_t launch_t(const Args& args, int32_t n_seg, hipStream_t st) {
-  hipLaunchKernelGGL(summarize_kernel<NSLOT>, dim3(n_seg), dim3(kThreads), 0, st, args);
+  hipLaunchKernelGGL((summarize_kernel<NSLOT, WIN, MAPPED>), dim3(n_seg), dim3(kThreads), 0, st, args);
   return hipGetLastError();
 }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 }  // namespace
 
 hipError_t launch_summarize(const SummarizeLaunch& l, hipStream_t st) {
-  Args a{l.kernel_id, l.stream, l.start_ns, l.end_ns, l.seg_off, l.n_events, l.n_kernels, l.n_streams,
+  const int32_t vec_ok =
+      aligned16(l.kernel_id) && aligned16(l.stream) && aligned16(l.start_ns) && aligned16(l.end_ns) ? 1 : 0;
+  Args a{l.kernel_id, l.stream, l.start_ns, l.end_ns, l.seg_off, l.n_events, l.n_kernels, l.n_streams, vec_ok,
          l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist, l.n_valid, l.n_invalid, l.t_first, l.t_last,
          l.step_ns, l.busy_ns, l.stream_busy_ns, l.wire_bytes, l.dev_status};
   if (l.n_seg == 0) return hipSuccess;
-  if (l.n_kernels <= 64) return launch_t<64>(a, l.n_seg, st);
-  if (l.n_kernels <= 512) return launch_t<512>(a, l.n_seg, st);
-  return launch_t<2048>(a, l.n_seg, st);
+  if (l.n_kernels <= 64) return launch_t<64, 8, false>(a, l.n_seg, st);
+  if (l.n_kernels <= 512) return launch_t<512, 8, false>(a, l.n_seg, st);
+  if (l.n_kernels <= 2048) return launch_t<2048, 8, false>(a, l.n_seg, st);
+  return launch_t<2048, 6, true>(a, l.n_seg, st);
 }
 
 }  // namespace argus

@@ -59,7 +59,8 @@ def assert_float_close(gpu: dict, ref: dict, fields, what=""):
 def oracle_summary_sharded(trace, g_begin=0, g_end=None, chunk=32, n_threads=None) -> dict:
     """Oracle summaries of segments [g_begin, g_end), regenerated on the host
     chunk by chunk and summarized by the unmodified single-threaded oracle on
-    disjoint chunks in parallel (segments are independent)."""
+    disjoint chunks in parallel (segments are independent). Also returns the
+    generator's per-segment checksums of the host events ("checksum")."""
     cfg = trace.cfg
     K, NS = cfg.n_kernels, cfg.n_streams
     g_end = cfg.n_segments if g_end is None else g_end
@@ -72,12 +73,13 @@ def oracle_summary_sharded(trace, g_begin=0, g_end=None, chunk=32, n_threads=Non
         "n_valid": np.empty(G, np.uint32), "n_invalid": np.empty(G, np.uint32),
         "t_first": np.empty(G, np.int64), "t_last": np.empty(G, np.int64), "step_ns": np.empty(G, np.int64),
         "busy_ns": np.empty(G, np.int64), "stream_busy_ns": np.empty((G, NS), np.int64),
-        "wire_bytes": np.empty(G, np.int64),
+        "wire_bytes": np.empty(G, np.int64), "checksum": np.empty(G, np.uint64),
     }
 
     def work(g0):
         g1 = min(g_end, g0 + chunk)
         ev = trace.fill_host(g0, g1, n_threads=1)
+        out["checksum"][g0 - g_begin:g1 - g_begin] = trace.checksum_host(ev, g0, g1)
         o = oracle.summarize(ev, K, NS)
         a, b = g0 - g_begin, g1 - g_begin
         for f in ("count", "sum_ns", "min_ns", "max_ns", "hist"):

@@ -1,0 +1,99 @@
+"""GPU parity at the full workload sizes, in the launch configuration that
+bench.py times (one summarize, cross-rank and iteration-window call over
+every rank-step of the workload).
+
+The oracle regenerates every segment on the host and summarizes it with the
+unmodified single-threaded code on disjoint chunks in parallel; its
+summaries (never the GPU's) feed the oracle's cross-rank and L1 steps.
+Everything is compared element by element; float32 fields within 1e-5
+relative. Planted faults must be recovered exactly.
+"""
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_20374_amd as pa
+import tracegen
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _gpu_chunks(t: torch.Tensor, per_seg: int, g0: int, g1: int):
+    return t[g0 * per_seg:g1 * per_seg].cpu().numpy()
+
+
+def _full_parity(name: str, chunk_segments: int = 512):
+    print(f"\n[gpu-case] full-size {name}", flush=True)
+    trace = tracegen.make(name)
+    cfg = trace.cfg
+    R, S, K, NS = cfg.n_ranks, cfg.n_steps, cfg.n_kernels, cfg.n_streams
+    G = R * S
+    ev = trace.fill_device(device=DEV)
+    s, x, w = pa.run_step(ev, R, S, K, NS)
+    torch.cuda.synchronize()
+    assert int(s["dev_status"].item()) == 0
+    dev_sums = trace.checksum_device(ev)
+    del ev
+    gc.collect()
+    torch.cuda.empty_cache()
+    print(f"[gpu-case] {name}: GPU step done, oracle over {G} segments", flush=True)
+
+    so = P.oracle_summary_sharded(trace)
+    # device and host generators produced the same events in every segment
+    assert np.array_equal(dev_sums, so.pop("checksum"))
+    # summaries, compared chunk by chunk to bound host memory
+    for g0 in range(0, G, chunk_segments):
+        g1 = min(G, g0 + chunk_segments)
+        for f, per in (("count", K), ("sum_ns", K), ("min_ns", K), ("max_ns", K), ("hist", K * P.NB)):
+            ref = so[f].reshape(-1)[g0 * per:g1 * per]
+            got = _gpu_chunks(s[f], per, g0, g1).view(ref.dtype)
+            if not np.array_equal(got, ref):
+                bad = np.nonzero(got != ref)[0]
+                raise AssertionError(f"{name} {f} segments {g0}-{g1}: {len(bad)} mismatches at {bad[:5]}")
+    P.assert_int_equal(s, so, ["n_valid", "n_invalid", "t_first", "t_last", "step_ns", "busy_ns",
+                               "stream_busy_ns", "wire_bytes"], name)
+    hist = so.pop("hist")
+    del hist
+    xo = oracle.cross_rank(so["count"], so["sum_ns"], R, S, K)
+    P.assert_int_equal(x, xo, P.XR_INT_FIELDS, name)
+    P.assert_float_close(x, xo, P.XR_FLOAT_FIELDS, name)
+    wo = oracle.iter_windows(so["step_ns"], R, S)
+    P.assert_int_equal(w, wo, P.L1_INT_FIELDS, name)
+    P.assert_float_close(w, wo, ["cp_ratio"], name)
+
+    truth = trace.truth()
+    strag = x["straggler"].cpu().numpy().reshape(R, S)
+    flags = x["flags"].cpu().numpy().reshape(R, S, K)
+    for t in range(S):
+        assert set(np.nonzero(strag[:, t])[0].tolist()) == truth["stragglers"]
+        assert {(int(r), int(k)) for r, k in zip(*np.nonzero(flags[:, t, :] & 8))} == truth["pairs"]
+    l1 = w["flags"].cpu().numpy().reshape(R, S)
+    assert {(int(r), int(t)) for r, t in zip(*np.nonzero(l1 & 2))} == truth["anomalous"]
+    del s, x, w
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_full_medium():
+    _full_parity("medium")
+
+
+@pytest.mark.timeout(900)
+def test_full_production():
+    _full_parity("production")
+
+
+@pytest.mark.timeout(1200)
+def test_full_cluster():
+    _full_parity("cluster")
+
+
+@pytest.mark.timeout(1200)
+def test_full_skew():
+    _full_parity("skew")
