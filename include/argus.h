@@ -117,9 +117,13 @@ typedef struct argus_summary {
   int32_t* dev_status;     /* optional (may be NULL) */
 } argus_summary_t;
 
+/* Bytes of caller workspace argus_summarize needs (a small, fixed amount:
+ * the work-queue counter of its persistent workgroups). The workspace must be
+ * device memory, 4-byte aligned, and not shared by calls that may overlap. */
 size_t argus_summarize_workspace(const argus_events_t* ev);
 
-/* Every output pointer except wire_bytes and dev_status is required. */
+/* Every output pointer except wire_bytes and dev_status is required; hist
+ * must be 16-byte aligned. workspace: see argus_summarize_workspace. */
 int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* workspace, size_t workspace_bytes,
                     void* stream);
 

@@ -130,7 +130,7 @@ def alloc_summary(n_ranks: int, n_steps: int, n_kernels: int, n_streams: int, de
         "n_valid": e(G, torch.int32), "n_invalid": e(G, torch.int32), "t_first": e(G, torch.int64),
         "t_last": e(G, torch.int64), "step_ns": e(G, torch.int64), "busy_ns": e(G, torch.int64),
         "stream_busy_ns": e(G * n_streams, torch.int64), "wire_bytes": e(G, torch.int64),
-        "dev_status": e(1, torch.int32),
+        "dev_status": e(1, torch.int32), "_workspace": e(256, torch.uint8),
     }
 
 
@@ -145,9 +145,10 @@ def summarize(ev: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: i
     e = Events(_ptr(ev["kernel_id"]), _ptr(ev["stream"]), _ptr(ev["start_ns"]), _ptr(ev["end_ns"]),
                _ptr(ev["seg_off"]), ev["kernel_id"].numel(), n_ranks, n_steps, n_kernels, n_streams)
     s = Summary(*[_ptr(out.get(f)) for f in SUMMARY_FIELDS])
-    ws = lib().argus_summarize_workspace(ctypes.byref(e))
-    assert ws == 0
-    _check(lib().argus_summarize(ctypes.byref(e), ctypes.byref(s), None, 0, _stream(dev)), "argus_summarize")
+    ws = out["_workspace"]
+    assert ws.numel() >= lib().argus_summarize_workspace(ctypes.byref(e))
+    _check(lib().argus_summarize(ctypes.byref(e), ctypes.byref(s), _ptr(ws), ws.numel(), _stream(dev)),
+           "argus_summarize")
     return out
 
 

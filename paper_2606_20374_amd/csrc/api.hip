@@ -8,7 +8,10 @@
 namespace argus {
 namespace {
 
-__global__ void clear_status_kernel(int32_t* s) { *s = 0; }
+__global__ void clear_kernel(int32_t* status, uint32_t* queue) {
+  if (status) *status = 0;
+  if (queue) *queue = 0;
+}
 
 // Per-device cache of "is gfx950": 0 unknown, 1 yes, 2 no.
 std::atomic<int> g_arch_ok[64];
@@ -31,9 +34,9 @@ int status_of(hipError_t e) { return e == hipSuccess ? ARGUS_OK : ARGUS_EHIP; }
 
 }  // namespace
 
-hipError_t launch_clear_status(int32_t* dev_status, hipStream_t st) {
-  if (!dev_status) return hipSuccess;
-  hipLaunchKernelGGL(clear_status_kernel, dim3(1), dim3(1), 0, st, dev_status);
+hipError_t launch_clear(int32_t* dev_status, uint32_t* queue, hipStream_t st) {
+  if (!dev_status && !queue) return hipSuccess;
+  hipLaunchKernelGGL(clear_kernel, dim3(1), dim3(1), 0, st, dev_status, queue);
   return hipGetLastError();
 }
 
@@ -58,14 +61,14 @@ const char* argus_status_string(int status) {
 
 size_t argus_summarize_workspace(const argus_events_t* ev) {
   (void)ev;
-  return 0;
+  return kSummarizeWorkspace;
 }
 
 int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* workspace, size_t workspace_bytes,
                     void* stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   if (!ev || !out) return ARGUS_EINVAL;
+  if (!workspace || workspace_bytes < kSummarizeWorkspace) return ARGUS_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 3u) != 0) return ARGUS_EINVAL;
   if (ev->n_ranks < 0 || ev->n_steps < 0 || ev->n_events < 0) return ARGUS_EINVAL;
   if (ev->n_kernels < 1 || ev->n_kernels > ARGUS_MAX_KERNELS) return ARGUS_EINVAL;
   if (ev->n_streams < 1 || ev->n_streams > ARGUS_MAX_STREAMS) return ARGUS_EINVAL;
@@ -80,12 +83,13 @@ int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* 
   int rc = check_device();
   if (rc != ARGUS_OK) return rc;
   hipStream_t st = (hipStream_t)stream;
-  rc = status_of(launch_clear_status(out->dev_status, st));
+  uint32_t* queue = static_cast<uint32_t*>(workspace);
+  rc = status_of(launch_clear(out->dev_status, queue, st));
   if (rc != ARGUS_OK) return rc;
   SummarizeLaunch l{ev->kernel_id, ev->stream, ev->start_ns, ev->end_ns, ev->seg_off, ev->n_events, (int32_t)n_seg,
                     ev->n_kernels, ev->n_streams, out->count, out->sum_ns, out->min_ns, out->max_ns, out->hist,
                     out->n_valid, out->n_invalid, out->t_first, out->t_last, out->step_ns, out->busy_ns,
-                    out->stream_busy_ns, out->wire_bytes, out->dev_status};
+                    out->stream_busy_ns, out->wire_bytes, out->dev_status, queue};
   return status_of(launch_summarize(l, st));
 }
 
@@ -125,7 +129,7 @@ int argus_cross_rank(const uint32_t* count, const int64_t* sum_ns, int32_t n_ran
   int rc = check_device();
   if (rc != ARGUS_OK) return rc;
   hipStream_t st = (hipStream_t)stream;
-  rc = status_of(launch_clear_status(o.dev_status, st));
+  rc = status_of(launch_clear(o.dev_status, nullptr, st));
   if (rc != ARGUS_OK) return rc;
   CrossRankLaunch l{count, sum_ns, n_ranks, n_steps, n_kernels, p, o, static_cast<int64_t*>(workspace)};
   return status_of(launch_cross_rank(l, st));
@@ -161,7 +165,7 @@ int argus_iter_windows(const int64_t* step_ns, int32_t n_ranks, int32_t n_steps,
   int rc = check_device();
   if (rc != ARGUS_OK) return rc;
   hipStream_t st = (hipStream_t)stream;
-  rc = status_of(launch_clear_status(dev_status, st));
+  rc = status_of(launch_clear(dev_status, nullptr, st));
   if (rc != ARGUS_OK) return rc;
   IterWindowsLaunch l{step_ns, n_ranks, n_steps, p, flags, cls, eff_width, cp, cp_ratio, dev_status};
   return status_of(launch_iter_windows(l, st));

@@ -70,6 +70,7 @@ struct SummarizeLaunch {
   int64_t* stream_busy_ns;
   int64_t* wire_bytes;
   int32_t* dev_status;
+  uint32_t* queue;  // workspace word, zeroed by launch_clear before the kernel
 };
 hipError_t launch_summarize(const SummarizeLaunch& a, hipStream_t st);
 
@@ -96,6 +97,9 @@ struct IterWindowsLaunch {
 };
 hipError_t launch_iter_windows(const IterWindowsLaunch& a, hipStream_t st);
 
-hipError_t launch_clear_status(int32_t* dev_status, hipStream_t st);
+// Zero the optional device status word and the optional queue counter.
+hipError_t launch_clear(int32_t* dev_status, uint32_t* queue, hipStream_t st);
+
+constexpr size_t kSummarizeWorkspace = 256;
 
 }  // namespace argus

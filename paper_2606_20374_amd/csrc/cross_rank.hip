@@ -12,12 +12,17 @@
 // Three launches per call:
 //   1. transpose: [R][S][K] (count, sum) -> x in a [S][K][R] workspace,
 //      64x64 tiles through LDS so both the read and the write are coalesced;
-//   2. per (step, kernel): load the kernel's row of x into LDS, then an
-//      MSD radix select (8-bit digits over x - min) for q1, median, q3 and,
-//      on |x - median|, the MAD; exact 128-bit sum for the mean;
-//   3. per (rank, step): per-cell z, mean and flags, then a radix select of
-//      the rank's typical per-kernel ratio to the median, the straggler
-//      decision, and the degraded-pair bit on the rank's outlier cells.
+//   2. per (step, kernel): one 1024-thread workgroup holds the kernel's x of
+//      every rank in registers (up to 16 per thread) and runs an MSD radix
+//      select over x - min, 8-bit digits, for q1, median and q3 together,
+//      then once more on |x - median| for the MAD; exact 128-bit sum for the
+//      mean;
+//   3. per (rank, step): per-cell z, mean and flags, a radix select of the
+//      rank's typical per-kernel ratio to the median, the straggler decision
+//      and the degraded-pair bit.
+// Digit histograms live in LDS; lanes of a wavefront that hit the same bin
+// are counted by one atomic (values of one kernel cluster tightly around
+// the median, so most lanes share a bin in the leading digits).
 #include "argus_internal.h"
 
 namespace argus {
@@ -26,64 +31,123 @@ namespace {
 typedef unsigned __int128 u128;
 typedef __int128 i128;
 
-constexpr int kSelThreads = 256;
-
-// Inclusive scan of one value per thread over a 256-thread block.
-__device__ __forceinline__ uint32_t block_scan_256(uint32_t v, uint32_t* wave_tot) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t n = __shfl_up(v, o, 64);
-    if (lane >= o) v += n;
-  }
-  if (lane == 63) wave_tot[wave] = v;
-  __syncthreads();
-  uint32_t add = 0;
-  for (int w = 0; w < wave; ++w) add += wave_tot[w];
-  __syncthreads();
-  return v + add;
-}
-
-struct SelShared {
-  uint32_t hist[256];
-  uint32_t wave_tot[4];
-  uint32_t digit, before;
-};
-
-// k-th smallest (0-based) of keys[0..n), all keys <= range. Block-wide; all
-// threads of the 256-thread block must call it.
-template <typename KeyT>
-__device__ uint64_t block_select(const KeyT* keys, int n, uint32_t k, uint64_t range, SelShared& sh) {
-  if (range == 0) return 0;
-  const int nbits = 64 - __builtin_clzll(range);
-  const int passes = (nbits + 7) >> 3;
-  uint64_t prefix = 0;
-  for (int p = passes - 1; p >= 0; --p) {
-    const int shift = p * 8;
-    sh.hist[threadIdx.x] = 0;
-    __syncthreads();
-    for (int i = threadIdx.x; i < n; i += kSelThreads) {
-      const uint64_t key = keys[i];
-      if (p == passes - 1 || (key >> (shift + 8)) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    const uint32_t h = sh.hist[threadIdx.x];
-    const uint32_t incl = block_scan_256(h, sh.wave_tot);
-    const uint32_t excl = incl - h;
-    if (excl <= k && k < incl) {
-      sh.digit = threadIdx.x;
-      sh.before = excl;
-    }
-    __syncthreads();
-    prefix = (prefix << 8) | sh.digit;
-    k -= sh.before;
-    __syncthreads();
-  }
-  return prefix;
-}
+constexpr int kStatThreads = 1024;
+constexpr int kRankThreads = 512;
 
 __device__ __forceinline__ int64_t cell_x(uint32_t count, int64_t sum) {
   const uint64_t x = (uint64_t)sum / count;
   return x > (uint64_t)INT64_MAX ? INT64_MAX : (int64_t)x;
+}
+
+// hist[bin] += 1 for every active lane. Two rounds count all active lanes
+// sharing the first remaining lane's bin with one atomic (the bin is read
+// with readlane, no LDS round trip); the rest add individually. Must be
+// reached by every lane of the wavefront.
+__device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool active) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const unsigned long long act = __ballot(active);
+    if (act == 0) return;
+    const int leader = __ffsll((long long)act) - 1;
+    const uint32_t lb = __builtin_amdgcn_readlane(bin, leader);
+    const bool mine = active && bin == lb;
+    const unsigned long long same = __ballot(mine);
+    if (lane == leader) atomicAdd(&hist[lb], (uint32_t)__popcll(same));
+    if (mine) active = false;
+  }
+  if (active) atomicAdd(&hist[bin], 1u);
+}
+
+template <int T>
+struct SelShared {
+  uint32_t hist[T][256];
+  uint32_t wave_tot[T * 4];
+  uint32_t digit[T], before[T];
+};
+
+// MSD radix select of the ranks k[0..T) among the valid register keys of
+// the whole block (bit j of vm: key[j] valid), all keys <= range. Every
+// thread of the block must call it; T * 256 <= blockDim.
+template <int V, int T, typename KeyT>
+__device__ void select_ranks(const KeyT (&key)[V], uint32_t vm, uint64_t range, const uint32_t (&k)[T],
+                             uint64_t (&out)[T], SelShared<T>& sh) {
+  uint64_t prefix[T];
+  uint32_t kk[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    prefix[t] = 0;
+    kk[t] = k[t];
+  }
+  if (range != 0) {
+    const int nbits = 64 - __builtin_clzll(range);
+    const int passes = (nbits + 7) >> 3;
+    const int tid = threadIdx.x;
+    for (int p = passes - 1; p >= 0; --p) {
+      const int shift = p * 8;
+      const bool top = p == passes - 1;
+      if (tid < T * 256) (&sh.hist[0][0])[tid] = 0;
+      __syncthreads();
+      // targets with equal prefixes share one histogram: rep[t] is the first
+      int rep[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        rep[t] = t;
+#pragma unroll
+        for (int q = T - 1; q >= 0; --q)
+          if (q < t && prefix[q] == prefix[t]) rep[t] = q;
+      }
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const uint64_t kj = (uint64_t)key[j];
+        const bool ok = (vm >> j) & 1u;
+        const uint32_t digit = (uint32_t)(kj >> shift) & 255u;
+        const uint64_t hi = top ? 0 : kj >> (shift + 8);
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+          if (rep[t] == t) hist_add(sh.hist[t], digit, ok && (top || hi == prefix[t]));
+      }
+      __syncthreads();
+      // per-target inclusive scan over its 256 bins (four wavefronts each)
+      const int t = tid >> 8, b = tid & 255, lane = tid & 63, w = tid >> 6;
+      uint32_t h = 0, v = 0;
+      if (tid < T * 256) {
+        int rt = 0;
+#pragma unroll
+        for (int q = 0; q < T; ++q)
+          if (q == t) rt = rep[q];
+        h = sh.hist[rt][b];
+        v = h;
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint32_t n = __shfl_up(v, o, 64);
+          if (lane >= o) v += n;
+        }
+        if (lane == 63) sh.wave_tot[w] = v;
+      }
+      __syncthreads();
+      if (tid < T * 256) {
+        for (int ww = t * 4; ww < w; ++ww) v += sh.wave_tot[ww];
+        const uint32_t excl = v - h;
+        uint32_t target = 0;
+#pragma unroll
+        for (int q = 0; q < T; ++q)
+          if (q == t) target = kk[q];
+        if (excl <= target && target < v) {
+          sh.digit[t] = (uint32_t)b;
+          sh.before[t] = excl;
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < T; ++q) {
+        prefix[q] = (prefix[q] << 8) | sh.digit[q];
+        kk[q] -= sh.before[q];
+      }
+      __syncthreads();
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < T; ++t) out[t] = prefix[t];
 }
 
 // ---------------------------------------------------------------- transpose
@@ -120,42 +184,50 @@ struct StatsArgs {
   uint32_t *n_flag, *n_degraded;
 };
 
-template <int RCAP>
-__global__ __launch_bounds__(kSelThreads) void xr_kernel_stats(StatsArgs a) {
-  __shared__ uint64_t vals[RCAP];
-  __shared__ SelShared sh;
+template <int V>
+__global__ __launch_bounds__(kStatThreads) void xr_kernel_stats(StatsArgs a) {
+  __shared__ SelShared<3> sh3;
+  __shared__ SelShared<1> sh1;
   __shared__ uint32_t n_sh;
   __shared__ unsigned long long red_min, red_max, red_lo, red_hi;
+  const int tid = threadIdx.x;
   const int64_t sk = blockIdx.x;
   const int64_t* row = a.xT + sk * a.R;
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     n_sh = 0;
     red_min = ~0ull;
     red_max = 0;
     red_lo = 0;
     red_hi = 0;
   }
-  __syncthreads();
+  uint64_t key[V];
+  uint32_t vm = 0, cnt = 0;
   unsigned long long mn = ~0ull, mx = 0;
   u128 acc = 0;
-  for (int r = threadIdx.x; r < a.R; r += kSelThreads) {
-    const int64_t x = row[r];
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int r = tid + j * kStatThreads;
+    const int64_t x = r < a.R ? row[r] : -1;
+    key[j] = x >= 0 ? (uint64_t)x : 0;
     if (x >= 0) {
-      const uint32_t i = atomicAdd(&n_sh, 1u);
-      vals[i] = (uint64_t)x;
+      vm |= 1u << j;
+      ++cnt;
       mn = (uint64_t)x < mn ? (uint64_t)x : mn;
       mx = (uint64_t)x > mx ? (uint64_t)x : mx;
       acc += (uint64_t)x;
     }
   }
+  __syncthreads();
   for (int o = 32; o > 0; o >>= 1) {
     const unsigned long long mo = __shfl_xor(mn, o, 64), xo = __shfl_xor(mx, o, 64);
     mn = mo < mn ? mo : mn;
     mx = xo > mx ? xo : mx;
+    cnt += __shfl_xor(cnt, o, 64);
   }
-  if ((threadIdx.x & 63) == 0) {
+  if ((tid & 63) == 0) {
     atomicMin(&red_min, mn);
     atomicMax(&red_max, mx);
+    atomicAdd(&n_sh, cnt);
   }
   // exact 128-bit sum of x: low words added with explicit carry detection
   if (acc != 0) {
@@ -165,40 +237,37 @@ __global__ __launch_bounds__(kSelThreads) void xr_kernel_stats(StatsArgs a) {
   }
   __syncthreads();
   const int n = (int)n_sh;
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     a.n_present[sk] = (uint32_t)n;
     a.n_flag[sk] = 0;
     a.n_degraded[sk] = 0;
   }
   if (n < a.min_ranks || n == 0) {
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
       a.med[sk] = a.mad[sk] = a.q1[sk] = a.q3[sk] = -1;
       a.xmean[sk] = 0.0f;
     }
     return;
   }
   const uint64_t vmin = red_min, vmax = red_max;
-  for (int i = threadIdx.x; i < n; i += kSelThreads) vals[i] -= vmin;
-  __syncthreads();
-  const uint64_t range = vmax - vmin;
+#pragma unroll
+  for (int j = 0; j < V; ++j) key[j] -= (vm >> j) & 1u ? vmin : 0;
   const uint32_t nm1 = (uint32_t)(n - 1);
-  const int64_t q1 = (int64_t)(vmin + block_select(vals, n, nm1 / 4, range, sh));
-  const int64_t med = (int64_t)(vmin + block_select(vals, n, nm1 / 2, range, sh));
-  const int64_t q3 = (int64_t)(vmin + block_select(vals, n, (uint32_t)((3ull * nm1) / 4), range, sh));
-  // absolute deviations from the median, in place
-  const uint64_t dmed = (uint64_t)med - vmin;
-  for (int i = threadIdx.x; i < n; i += kSelThreads) {
-    const uint64_t v = vals[i];
-    vals[i] = v >= dmed ? v - dmed : dmed - v;
-  }
-  __syncthreads();
-  const uint64_t drange = (vmax - (uint64_t)med) > dmed ? (vmax - (uint64_t)med) : dmed;
-  const int64_t mad = (int64_t)block_select(vals, n, nm1 / 2, drange, sh);
-  if (threadIdx.x == 0) {
-    a.med[sk] = med;
-    a.mad[sk] = mad;
-    a.q1[sk] = q1;
-    a.q3[sk] = q3;
+  const uint32_t ranks[3] = {nm1 / 4, nm1 / 2, (uint32_t)((3ull * nm1) / 4)};
+  uint64_t qs[3];
+  select_ranks<V, 3>(key, vm, vmax - vmin, ranks, qs, sh3);
+  const uint64_t dmed = qs[1];  // median - vmin
+#pragma unroll
+  for (int j = 0; j < V; ++j) key[j] = key[j] >= dmed ? key[j] - dmed : dmed - key[j];
+  const uint64_t top = vmax - vmin - dmed;
+  const uint32_t r1[1] = {nm1 / 2};
+  uint64_t md[1];
+  select_ranks<V, 1>(key, vm, top > dmed ? top : dmed, r1, md, sh1);
+  if (tid == 0) {
+    a.q1[sk] = (int64_t)(vmin + qs[0]);
+    a.med[sk] = (int64_t)(vmin + qs[1]);
+    a.q3[sk] = (int64_t)(vmin + qs[2]);
+    a.mad[sk] = (int64_t)md[0];
     const u128 total = ((u128)red_hi << 64) | (u128)red_lo;
     a.xmean[sk] = (float)((double)total / (double)n);
   }
@@ -213,29 +282,47 @@ struct RankArgs {
   argus_xr_out_t o;
 };
 
-template <int KCAP>
-__global__ __launch_bounds__(kSelThreads) void xr_rank(RankArgs a) {
-  __shared__ uint32_t rat[KCAP];
-  __shared__ uint8_t fl[KCAP];
-  __shared__ SelShared sh;
+// floor(1000 x / med), saturated at INT32_MAX (x >= 0, med >= 1)
+__device__ __forceinline__ uint32_t ratio_pm(int64_t x, int64_t med) {
+  uint64_t q;
+  if ((uint64_t)x <= ~0ull / 1000u) {
+    q = ((uint64_t)x * 1000u) / (uint64_t)med;
+  } else {
+    const u128 w = ((u128)(uint64_t)x * 1000u) / (u128)(uint64_t)med;
+    q = w > (u128)INT32_MAX ? (uint64_t)INT32_MAX : (uint64_t)w;
+  }
+  return q > (uint64_t)INT32_MAX ? (uint32_t)INT32_MAX : (uint32_t)q;
+}
+
+template <int V>
+__global__ __launch_bounds__(kRankThreads) void xr_rank(RankArgs a) {
+  __shared__ SelShared<1> sh;
   __shared__ uint32_t ne_sh, nf_sh, rmin_sh, rmax_sh;
+  const int tid = threadIdx.x;
   const int32_t K = a.K;
   const int64_t rs = blockIdx.x;  // r * S + s
   const int32_t s = (int32_t)(rs % a.S);
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     ne_sh = 0;
     nf_sh = 0;
     rmin_sh = 0xFFFFFFFFu;
     rmax_sh = 0;
   }
-  __syncthreads();
-  uint32_t nf = 0;
-  for (int k = threadIdx.x; k < K; k += kSelThreads) {
+  uint32_t rat[V];
+  uint32_t fl[(V + 3) / 4];
+#pragma unroll
+  for (int j = 0; j < (V + 3) / 4; ++j) fl[j] = 0;
+  uint32_t em = 0, ne = 0, nf = 0, rmin = 0xFFFFFFFFu, rmax = 0;
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int k = tid + j * kRankThreads;
+    rat[j] = 0;
+    if (k >= K) continue;
     const int64_t c = rs * K + k;
     const int64_t sk = (int64_t)s * K + k;
     const uint32_t cnt = a.count[c];
     float z = 0.0f, mean = 0.0f;
-    uint8_t f = 0;
+    uint32_t f = 0;
     if (cnt) {
       const int64_t sm = a.sum[c];
       mean = (float)((double)sm / (double)cnt);
@@ -253,39 +340,52 @@ __global__ __launch_bounds__(kSelThreads) void xr_rank(RankArgs a) {
           f |= 1;
         if ((i128)1000 * ((i128)x - q3) > (i128)a.p.alpha_pm * iqr) f |= 2;
         if (med >= 1) {
-          uint64_t q;
-          if ((uint64_t)x <= ~0ull / 1000u)
-            q = ((uint64_t)x * 1000u) / (uint64_t)med;
-          else
-            q = (uint64_t)(((u128)(uint64_t)x * 1000u) / (u128)(uint64_t)med > (u128)INT32_MAX
-                               ? (u128)INT32_MAX
-                               : ((u128)(uint64_t)x * 1000u) / (u128)(uint64_t)med);
-          const uint32_t ratio = q > (uint64_t)INT32_MAX ? (uint32_t)INT32_MAX : (uint32_t)q;
-          const uint32_t i = atomicAdd(&ne_sh, 1u);
-          rat[i] = ratio;
-          atomicMin(&rmin_sh, ratio);
-          atomicMax(&rmax_sh, ratio);
-          if (f & 1) nf++;
+          const uint32_t r = ratio_pm(x, med);
+          rat[j] = r;
+          em |= 1u << j;
+          ++ne;
+          rmin = r < rmin ? r : rmin;
+          rmax = r > rmax ? r : rmax;
+          if (f & 1) ++nf;
         }
       }
     }
     a.o.z[c] = z;
     if (a.o.mean_ns) a.o.mean_ns[c] = mean;
-    fl[k] = f;
+    fl[j >> 2] |= f << (8 * (j & 3));
   }
-  atomicAdd(&nf_sh, nf);
+  for (int o = 32; o > 0; o >>= 1) {
+    ne += __shfl_xor(ne, o, 64);
+    nf += __shfl_xor(nf, o, 64);
+    const uint32_t a1 = __shfl_xor(rmin, o, 64), a2 = __shfl_xor(rmax, o, 64);
+    rmin = a1 < rmin ? a1 : rmin;
+    rmax = a2 > rmax ? a2 : rmax;
+  }
   __syncthreads();
-  const int ne = (int)ne_sh;
-  int32_t score = -1;
-  if (ne > 0) {
-    const uint32_t rmin = rmin_sh;
-    for (int i = threadIdx.x; i < ne; i += kSelThreads) rat[i] -= rmin;
-    __syncthreads();
-    score = (int32_t)(rmin + block_select(rat, ne, (uint32_t)(ne - 1) / 2, rmax_sh - rmin, sh));
+  if ((tid & 63) == 0) {
+    atomicAdd(&ne_sh, ne);
+    atomicAdd(&nf_sh, nf);
+    atomicMin(&rmin_sh, rmin);
+    atomicMax(&rmax_sh, rmax);
   }
-  const bool strag = ne >= a.p.min_kernels && (int64_t)score >= 1000 + (int64_t)a.p.tau_rank_pm;
-  for (int k = threadIdx.x; k < K; k += kSelThreads) {
-    uint8_t f = fl[k];
+  __syncthreads();
+  const int n_eval = (int)ne_sh;
+  int32_t score = -1;
+  if (n_eval > 0) {
+    const uint32_t lo = rmin_sh;
+#pragma unroll
+    for (int j = 0; j < V; ++j) rat[j] -= (em >> j) & 1u ? lo : 0u;
+    const uint32_t rk[1] = {(uint32_t)(n_eval - 1) / 2};
+    uint64_t sel[1];
+    select_ranks<V, 1>(rat, em, rmax_sh - lo, rk, sel, sh);
+    score = (int32_t)(lo + (uint32_t)sel[0]);
+  }
+  const bool strag = n_eval >= a.p.min_kernels && (int64_t)score >= 1000 + (int64_t)a.p.tau_rank_pm;
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int k = tid + j * kRankThreads;
+    if (k >= K) continue;
+    uint32_t f = (fl[j >> 2] >> (8 * (j & 3))) & 0xFFu;
     if (f & 1) {
       const int64_t sk = (int64_t)s * K + k;
       atomicAdd(&a.o.n_flag[sk], 1u);
@@ -294,14 +394,24 @@ __global__ __launch_bounds__(kSelThreads) void xr_rank(RankArgs a) {
         atomicAdd(&a.o.n_degraded[sk], 1u);
       }
     }
-    a.o.flags[rs * K + k] = f;
+    a.o.flags[rs * K + k] = (uint8_t)f;
   }
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     a.o.score_pm[rs] = score;
-    a.o.n_eval[rs] = (uint32_t)ne;
+    a.o.n_eval[rs] = (uint32_t)n_eval;
     a.o.n_flag_rank[rs] = nf_sh;
     a.o.straggler[rs] = strag ? 1 : 0;
   }
+}
+
+template <int V>
+void launch_stats(const StatsArgs& sa, dim3 g, hipStream_t st) {
+  hipLaunchKernelGGL(xr_kernel_stats<V>, g, dim3(kStatThreads), 0, st, sa);
+}
+
+template <int V>
+void launch_rank(const RankArgs& ra, dim3 g, hipStream_t st) {
+  hipLaunchKernelGGL(xr_rank<V>, g, dim3(kRankThreads), 0, st, ra);
 }
 
 }  // namespace
@@ -315,18 +425,45 @@ hipError_t launch_cross_rank(const CrossRankLaunch& l, hipStream_t st) {
   StatsArgs sa{l.xT, R, S, K, l.p.min_ranks, l.o.n_present, l.o.med_ns, l.o.mad_ns, l.o.q1_ns, l.o.q3_ns,
                l.o.xmean_ns, l.o.n_flag, l.o.n_degraded};
   const dim3 g2((unsigned)((int64_t)S * K));
-  if (R <= 2048)
-    hipLaunchKernelGGL(xr_kernel_stats<2048>, g2, dim3(kSelThreads), 0, st, sa);
-  else
-    hipLaunchKernelGGL(xr_kernel_stats<ARGUS_MAX_XR_RANKS>, g2, dim3(kSelThreads), 0, st, sa);
+  switch ((R + kStatThreads - 1) / kStatThreads) {  // values per thread, R <= ARGUS_MAX_XR_RANKS
+#define ARGUS_STATS_CASE(v) \
+  case v:                   \
+    launch_stats<v>(sa, g2, st); \
+    break;
+    ARGUS_STATS_CASE(1) ARGUS_STATS_CASE(2) ARGUS_STATS_CASE(3) ARGUS_STATS_CASE(4) ARGUS_STATS_CASE(5)
+    ARGUS_STATS_CASE(6) ARGUS_STATS_CASE(7) ARGUS_STATS_CASE(8) ARGUS_STATS_CASE(9) ARGUS_STATS_CASE(10)
+    ARGUS_STATS_CASE(11) ARGUS_STATS_CASE(12) ARGUS_STATS_CASE(13) ARGUS_STATS_CASE(14) ARGUS_STATS_CASE(15)
+    default:
+      launch_stats<16>(sa, g2, st);
+#undef ARGUS_STATS_CASE
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   RankArgs ra{l.count, l.sum_ns, R, S, K, l.p, l.o};
   const dim3 g3((unsigned)((int64_t)R * S));
-  if (K <= 2048)
-    hipLaunchKernelGGL(xr_rank<2048>, g3, dim3(kSelThreads), 0, st, ra);
-  else
-    hipLaunchKernelGGL(xr_rank<ARGUS_MAX_XR_KERNELS>, g3, dim3(kSelThreads), 0, st, ra);
+  switch ((K + kRankThreads - 1) / kRankThreads) {  // kernels per thread, K <= ARGUS_MAX_XR_KERNELS
+#define ARGUS_RANK_CASE(v) \
+  case v:                  \
+    launch_rank<v>(ra, g3, st); \
+    break;
+    ARGUS_RANK_CASE(1) ARGUS_RANK_CASE(2) ARGUS_RANK_CASE(3) ARGUS_RANK_CASE(4) ARGUS_RANK_CASE(5)
+    ARGUS_RANK_CASE(6) ARGUS_RANK_CASE(7) ARGUS_RANK_CASE(8) ARGUS_RANK_CASE(9) ARGUS_RANK_CASE(10)
+    ARGUS_RANK_CASE(11) ARGUS_RANK_CASE(12) ARGUS_RANK_CASE(13) ARGUS_RANK_CASE(14) ARGUS_RANK_CASE(15)
+    ARGUS_RANK_CASE(16) ARGUS_RANK_CASE(17) ARGUS_RANK_CASE(18) ARGUS_RANK_CASE(20) ARGUS_RANK_CASE(24)
+    ARGUS_RANK_CASE(28)
+    case 19:
+      launch_rank<20>(ra, g3, st);
+      break;
+    case 21: case 22: case 23:
+      launch_rank<24>(ra, g3, st);
+      break;
+    case 25: case 26: case 27:
+      launch_rank<28>(ra, g3, st);
+      break;
+    default:
+      launch_rank<32>(ra, g3, st);
+#undef ARGUS_RANK_CASE
+  }
   return hipGetLastError();
 }
 

@@ -27,6 +27,8 @@
 //   busy time uses LDS atomics.
 // * The flush writes every output element exactly once (identity values for
 //   absent kernels), coalesced, so outputs need no clearing.
+#include <atomic>
+
 #include "argus_internal.h"
 
 namespace argus {
@@ -53,8 +55,7 @@ constexpr uint32_t kMapEmpty = 0xFFFF, kMapBusy = 0xFFFE, kMapDefer = 0xFFFD, kM
 template <int NSLOT, int WIN, bool MAPPED>
 struct Smem {
   unsigned long long sum[NSLOT];
-  long long mn[NSLOT];
-  long long mx[NSLOT];
+  long long mm[NSLOT][2];  // min, max (one 16-byte read per event)
   uint32_t win[NSLOT][WIN];
   uint32_t meta[NSLOT];
   uint32_t pool[kPool][NB];
@@ -76,6 +77,8 @@ struct Args {
   int64_t n_events;
   int32_t n_kernels, n_streams;
   int32_t vec_ok;  // event arrays 16-byte aligned: vector loads allowed
+  int32_t n_seg;
+  uint32_t* queue;  // next segment to take (zeroed before the launch)
   uint32_t* count;
   int64_t* sum_ns;
   int64_t* min_ns;
@@ -185,7 +188,10 @@ struct Seg {
     }
   }
 
-  __device__ __forceinline__ void slot_add(int slot, uint32_t m, uint64_t d) {
+  // mmv: min and max of the slot as read before this event (possibly stale:
+  // min only falls and max only rises, so a stale read can only cause an
+  // extra atomic, never a missed one)
+  __device__ __forceinline__ void slot_add(int slot, uint32_t m, uint64_t d, const v2l& mmv) {
     if (m & kDone) return;
     const int b = octave_bin(d);
     if ((m & 0xFFu) == kBaseUnset) {
@@ -201,14 +207,14 @@ struct Seg {
     else
       pool_add(slot, m, b);
     atomicAdd(&sm.sum[slot], (unsigned long long)d);
-    atomicMin(&sm.mn[slot], (long long)d);
-    atomicMax(&sm.mx[slot], (long long)d);
+    if ((long long)d < mmv.x) atomicMin(&sm.mm[slot][0], (long long)d);
+    if ((long long)d > mmv.y) atomicMax(&sm.mm[slot][1], (long long)d);
   }
 
   __device__ __forceinline__ void slot_reset(int s) {
     sm.sum[s] = 0;
-    sm.mn[s] = INT64_MAX;
-    sm.mx[s] = INT64_MIN;
+    sm.mm[s][0] = INT64_MAX;
+    sm.mm[s][1] = INT64_MIN;
 #pragma unroll
     for (int w = 0; w < WIN; ++w) sm.win[s][w] = 0;
     sm.meta[s] = kBaseUnset;
@@ -258,20 +264,32 @@ __device__ __forceinline__ void process4(Seg<NSLOT, WIN, MAPPED>& sg, const Args
     for (int j = 0; j < 4; ++j) slot[j] = lk[j];
   }
   uint32_t m[4];
+  v2l mmv[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) m[j] = slot[j] >= 0 ? sg.sm.meta[slot[j]] : 0u;
+  for (int j = 0; j < 4; ++j) {
+    m[j] = slot[j] >= 0 ? sg.sm.meta[slot[j]] : 0u;
+    mmv[j] = slot[j] >= 0 ? *reinterpret_cast<const v2l*>(&sg.sm.mm[slot[j]][0]) : v2l{0, 0};
+  }
 #pragma unroll
   for (int j = 0; j < 4; ++j)
-    if (slot[j] >= 0) sg.slot_add(slot[j], m[j], d[j]);
+    if (slot[j] >= 0) sg.slot_add(slot[j], m[j], d[j], mmv[j]);
 }
 
 template <int NSLOT, int WIN, bool MAPPED>
 __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
   __shared__ Smem<NSLOT, WIN, MAPPED> sm;
+  __shared__ int64_t g_next;
   Seg<NSLOT, WIN, MAPPED> sg{sm};
   const int tid = threadIdx.x;
-  const int64_t g = blockIdx.x;
   const int32_t K = a.n_kernels, NS = a.n_streams;
+
+  // Persistent workgroups pull segments from a queue, so the output stores
+  // of one segment drain while the loads of the next are already in flight.
+  while (true) {
+  if (tid == 0) g_next = (int64_t)atomicAdd(a.queue, 1u);
+  __syncthreads();
+  const int64_t g = g_next;
+  if (g >= a.n_seg) break;
 
   int64_t lo = a.seg_off[g], hi = a.seg_off[g + 1];
   const bool bad = !(lo >= 0 && lo <= hi && hi <= a.n_events && hi - lo <= (int64_t)UINT32_MAX);
@@ -422,8 +440,8 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         const int64_t c = g * K + kb + (MAPPED ? (int)sm.slot_kid[s] : s);
         a.count[c] = cnt;
         a.sum_ns[c] = (int64_t)sm.sum[s];
-        a.min_ns[c] = sm.mn[s];
-        a.max_ns[c] = sm.mx[s];
+        a.min_ns[c] = sm.mm[s][0];
+        a.max_ns[c] = sm.mm[s][1];
         if (cnt) wire += 33u + 5u * nnz;
       }
       // flush: histograms, four bins per thread, 16-byte stores
@@ -465,23 +483,8 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
       __syncthreads();
       if (!again) break;
     }
-    if (MAPPED) {
-      // identity values for the ids of this range that never occurred
-      for (int i = tid; i < nk; i += kThreads) {
-        if (sg.map_get(i) != kMapEmpty) continue;
-        const int64_t c = g * K + kb + i;
-        a.count[c] = 0;
-        a.sum_ns[c] = 0;
-        a.min_ns[c] = INT64_MAX;
-        a.max_ns[c] = INT64_MIN;
-      }
-      for (int it = tid; it < nk * (NB / 4); it += kThreads) {
-        if (sg.map_get(it >> 3) != kMapEmpty) continue;
-        const int64_t c = g * K + kb + (it >> 3);
-        *reinterpret_cast<uint4*>(a.hist + c * NB + 4 * (it & 7)) = make_uint4(0u, 0u, 0u, 0u);
-      }
-      __syncthreads();
-    }
+    // (mapped mode: ids of this range that never occurred keep the identity
+    // values written by identity_fill_kernel before this launch)
   }
 
   // per-segment aggregates
@@ -507,15 +510,59 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
     if (a.wire_bytes) a.wire_bytes[g] = (int64_t)sm.red_wire;
   }
   if (tid < NS) a.stream_busy_ns[g * NS + tid] = (int64_t)sm.stream_busy[tid];
+  __syncthreads();
+  }
+}
+
+// Workgroups resident at once (one per CU for the large tables): the grid
+// of the persistent kernel. Cached per device and instantiation.
+template <int NSLOT, int WIN, bool MAPPED>
+int resident_groups() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, summarize_kernel<NSLOT, WIN, MAPPED>, kThreads, 0) !=
+        hipSuccess)
+      return 0;
+    v = cus * (per_cu > 0 ? per_cu : 1);
+    cache[dev].store(v, std::memory_order_relaxed);
+  }
+  return v;
 }
 
 template <int NSLOT, int WIN, bool MAPPED>
 hipError_t launch_t(const Args& args, int32_t n_seg, hipStream_t st) {
-  hipLaunchKernelGGL((summarize_kernel<NSLOT, WIN, MAPPED>), dim3(n_seg), dim3(kThreads), 0, st, args);
+  const int groups = resident_groups<NSLOT, WIN, MAPPED>();
+  if (groups <= 0) return hipErrorInvalidDevice;
+  const int grid = n_seg < groups ? n_seg : groups;
+  hipLaunchKernelGGL((summarize_kernel<NSLOT, WIN, MAPPED>), dim3(grid), dim3(kThreads), 0, st, args);
   return hipGetLastError();
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Identity values of every cell (count 0, sum 0, min INT64_MAX, max
+// INT64_MIN, empty histogram), streamed with 16-byte stores. Used before the
+// mapped-mode kernel, which then writes only the cells of ids that occur:
+// for large, sparse id spaces most cells are absent, and one streaming pass
+// writes them far faster than per-segment bursts at the end of each scan.
+__global__ __launch_bounds__(256) void identity_fill_kernel(uint32_t* count, int64_t* sum, int64_t* mn, int64_t* mx,
+                                                            uint32_t* hist, int64_t cells) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  uint4* h4 = reinterpret_cast<uint4*>(hist);
+  for (int64_t i = t0; i < cells * (NB / 4); i += stride) h4[i] = make_uint4(0u, 0u, 0u, 0u);
+  for (int64_t c = t0; c < cells; c += stride) {
+    count[c] = 0;
+    sum[c] = 0;
+    mn[c] = INT64_MAX;
+    mx[c] = INT64_MIN;
+  }
+}
 
 }  // namespace
 
@@ -523,12 +570,17 @@ hipError_t launch_summarize(const SummarizeLaunch& l, hipStream_t st) {
   const int32_t vec_ok =
       aligned16(l.kernel_id) && aligned16(l.stream) && aligned16(l.start_ns) && aligned16(l.end_ns) ? 1 : 0;
   Args a{l.kernel_id, l.stream, l.start_ns, l.end_ns, l.seg_off, l.n_events, l.n_kernels, l.n_streams, vec_ok,
-         l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist, l.n_valid, l.n_invalid, l.t_first, l.t_last,
+         l.n_seg, l.queue, l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist, l.n_valid, l.n_invalid, l.t_first, l.t_last,
          l.step_ns, l.busy_ns, l.stream_busy_ns, l.wire_bytes, l.dev_status};
   if (l.n_seg == 0) return hipSuccess;
   if (l.n_kernels <= 64) return launch_t<64, 8, false>(a, l.n_seg, st);
   if (l.n_kernels <= 512) return launch_t<512, 8, false>(a, l.n_seg, st);
   if (l.n_kernels <= 2048) return launch_t<2048, 8, false>(a, l.n_seg, st);
+  const int64_t cells = (int64_t)l.n_seg * l.n_kernels;
+  hipLaunchKernelGGL(identity_fill_kernel, dim3(4096), dim3(256), 0, st, l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist,
+                     cells);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   return launch_t<2048, 6, true>(a, l.n_seg, st);
 }
 

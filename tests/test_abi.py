@@ -42,6 +42,8 @@ def test_version_and_defaults():
 def test_workspace_sizes():
     assert pa.lib().argus_cross_rank_workspace(10240, 1, 2048) == 10240 * 2048 * 8
     assert pa.lib().argus_iter_windows_workspace(10, 10) == 0
+    e = A.Events(0, 0, 0, 0, 0, 0, 1, 1, 1, 1)
+    assert pa.lib().argus_summarize_workspace(ctypes.byref(e)) == 256
 
 
 @pytest.mark.parametrize("mutate", [
@@ -52,12 +54,15 @@ def test_workspace_sizes():
     lambda e, s: setattr(e, "seg_off", None),
     lambda e, s: setattr(s, "hist", None),
     lambda e, s: setattr(s, "hist", 0x1008),  # misaligned histogram
+    None,  # no workspace
 ])
 def test_summarize_rejects_bad_arguments(mutate):
     e = A.Events(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 10, 2, 2, 4, 2)
     s = A.Summary(*([0x1000] * 12 + [None, None]))
-    mutate(e, s)
-    assert pa.lib().argus_summarize(ctypes.byref(e), ctypes.byref(s), None, 0, None) == A.EINVAL
+    ws, n = (0x2000, 256) if mutate else (None, 0)
+    if mutate:
+        mutate(e, s)
+    assert pa.lib().argus_summarize(ctypes.byref(e), ctypes.byref(s), ws, n, None) == A.EINVAL
 
 
 def test_cross_rank_and_l1_reject_bad_arguments():

@@ -148,6 +148,43 @@ def test_full_histogram_pool_exhaustion():
     P.assert_int_equal(g, o, P.SUM_INT_FIELDS, "pool")
 
 
+def _random_events(n, K, NS, seed, spread_octaves=3, seg_lengths=None, wide_ids=()):
+    rng = np.random.default_rng(seed)
+    kid = rng.integers(0, K, size=n).astype(np.int32)
+    base = rng.integers(1000, 10**6, size=K)
+    d = (base[kid] * 2.0 ** rng.uniform(0, spread_octaves, size=n)).astype(np.int64)
+    wide = np.isin(kid, np.asarray(wide_ids, dtype=np.int64))
+    d[wide] = (2 ** rng.uniform(0, 34, size=int(wide.sum()))).astype(np.int64)
+    t0 = rng.integers(0, 2**50, size=n).astype(np.int64)
+    lens = [n] if seg_lengths is None else seg_lengths
+    return {"kernel_id": kid, "stream": (kid % NS).astype(np.int32), "start_ns": t0, "end_ns": t0 + d,
+            "seg_off": np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)}
+
+
+def test_mapped_slot_overflow():
+    _announce("mapped ids: more distinct ids in a segment than LDS slots")
+    K = 6000
+    ev = _random_events(60_000, K, 16, seed=21, seg_lengths=[30_000, 25_000, 5_000])
+    g, o = _summarize_both(ev, 3, 1, K, 16)
+    P.assert_int_equal(g, o, P.SUM_INT_FIELDS, "mapped-overflow")
+
+
+def test_mapped_several_id_ranges():
+    _announce("mapped ids: id space of 40,000 (several ranges)")
+    K = 40_000
+    ev = _random_events(50_000, K, 8, seed=22, seg_lengths=[20_000, 0, 30_000, 0])
+    g, o = _summarize_both(ev, 2, 2, K, 8)
+    P.assert_int_equal(g, o, P.SUM_INT_FIELDS, "mapped-ranges")
+
+
+def test_mapped_pool_exhaustion():
+    _announce("mapped ids: wide kernels exhaust the histogram pool")
+    K = 3000
+    ev = _random_events(80_000, K, 4, seed=23, seg_lengths=[40_000, 40_000], wide_ids=range(0, 3000, 15))
+    g, o = _summarize_both(ev, 2, 1, K, 4)
+    P.assert_int_equal(g, o, P.SUM_INT_FIELDS, "mapped-pool")
+
+
 def test_single_kernel_and_stream():
     _announce("K=1 NS=1")
     t = tracegen.make("tiny", n_kernels=1, n_streams=1, n_stragglers=0, n_pairs=0)
