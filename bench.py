@@ -220,6 +220,26 @@ def main():
         "detection": {"stragglers_recovered": strag_ok, "pairs_recovered": pairs_ok,
                       "n_flagged_ranks": int(strag.sum())},
     }
+    # L1 iteration windows on a long series: 10,240 ranks x 1,000 steps of
+    # step times (seeded: 4% noise, a 1.5x regression on every 7th rank from
+    # step 600, a 3x spike on every 11th rank at step 300)
+    rng = np.random.default_rng(7)
+    y = (10**9 * (1 + 0.04 * rng.standard_normal((10_240, 1000)))).astype(np.int64)
+    y[::7, 600:] = y[::7, 600:] * 3 // 2
+    y[::11, 300] *= 3
+    y_d = torch.from_numpy(y.reshape(-1)).to(dev)
+    l1_out = pa.alloc_iter_windows(10_240, 1000, dev)
+    for _ in range(2):
+        pa.iter_windows(y_d, 10_240, 1000, out=l1_out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(5):
+        pa.iter_windows(y_d, 10_240, 1000, out=l1_out)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    result["iter_windows_10240x1000_ms"] = e0.elapsed_time(e1) / 5
+
     if not args.no_cpu_baseline:
         sample = min(args.cpu_sample_ranks, R)
         gs = sample * S

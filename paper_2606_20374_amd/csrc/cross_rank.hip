@@ -23,6 +23,8 @@
 // Digit histograms live in LDS; lanes of a wavefront that hit the same bin
 // are counted by one atomic (values of one kernel cluster tightly around
 // the median, so most lanes share a bin in the leading digits).
+#include <type_traits>
+
 #include "argus_internal.h"
 
 namespace argus {
@@ -31,8 +33,7 @@ namespace {
 typedef unsigned __int128 u128;
 typedef __int128 i128;
 
-constexpr int kStatThreads = 1024;
-constexpr int kRankThreads = 512;
+constexpr int kBins = 256;  // 8-bit digits: the first 256 threads own one bin each
 
 __device__ __forceinline__ int64_t cell_x(uint32_t count, int64_t sum) {
   const uint64_t x = (uint64_t)sum / count;
@@ -67,10 +68,10 @@ struct SelShared {
 };
 
 // MSD radix select of the ranks k[0..T) among the valid register keys of
-// the whole block (bit j of vm: key[j] valid), all keys <= range. Every
-// thread of the block must call it; T * 256 <= blockDim.
-template <int V, int T, typename KeyT>
-__device__ void select_ranks(const KeyT (&key)[V], uint32_t vm, uint64_t range, const uint32_t (&k)[T],
+// the whole block of NT >= 256 threads (bit j of vm: key[j] valid), all keys
+// <= range. Every thread of the block must call it.
+template <int NT, int V, int T, typename KeyT>
+__device__ void select_ranks(const KeyT (&key)[V], uint64_t vm, uint64_t range, const uint32_t (&k)[T],
                              uint64_t (&out)[T], SelShared<T>& sh) {
   uint64_t prefix[T];
   uint32_t kk[T];
@@ -82,11 +83,13 @@ __device__ void select_ranks(const KeyT (&key)[V], uint32_t vm, uint64_t range, 
   if (range != 0) {
     const int nbits = 64 - __builtin_clzll(range);
     const int passes = (nbits + 7) >> 3;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     for (int p = passes - 1; p >= 0; --p) {
       const int shift = p * 8;
       const bool top = p == passes - 1;
-      if (tid < T * 256) (&sh.hist[0][0])[tid] = 0;
+      if (tid < kBins)
+#pragma unroll
+        for (int t = 0; t < T; ++t) sh.hist[t][tid] = 0;
       __syncthreads();
       // targets with equal prefixes share one histogram: rep[t] is the first
       int rep[T];
@@ -108,33 +111,30 @@ __device__ void select_ranks(const KeyT (&key)[V], uint32_t vm, uint64_t range, 
           if (rep[t] == t) hist_add(sh.hist[t], digit, ok && (top || hi == prefix[t]));
       }
       __syncthreads();
-      // per-target inclusive scan over its 256 bins (four wavefronts each)
-      const int t = tid >> 8, b = tid & 255, lane = tid & 63, w = tid >> 6;
-      uint32_t h = 0, v = 0;
-      if (tid < T * 256) {
-        int rt = 0;
+      // per-target inclusive scan over 256 bins, one bin per thread
+      uint32_t h[T], v[T];
+      if (tid < kBins) {
 #pragma unroll
-        for (int q = 0; q < T; ++q)
-          if (q == t) rt = rep[q];
-        h = sh.hist[rt][b];
-        v = h;
-        for (int o = 1; o < 64; o <<= 1) {
-          const uint32_t n = __shfl_up(v, o, 64);
-          if (lane >= o) v += n;
+        for (int t = 0; t < T; ++t) {
+          h[t] = sh.hist[rep[t]][tid];
+          v[t] = h[t];
+          for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t n = __shfl_up(v[t], o, 64);
+            if (lane >= o) v[t] += n;
+          }
+          if (lane == 63) sh.wave_tot[t * 4 + w] = v[t];
         }
-        if (lane == 63) sh.wave_tot[w] = v;
       }
       __syncthreads();
-      if (tid < T * 256) {
-        for (int ww = t * 4; ww < w; ++ww) v += sh.wave_tot[ww];
-        const uint32_t excl = v - h;
-        uint32_t target = 0;
+      if (tid < kBins) {
 #pragma unroll
-        for (int q = 0; q < T; ++q)
-          if (q == t) target = kk[q];
-        if (excl <= target && target < v) {
-          sh.digit[t] = (uint32_t)b;
-          sh.before[t] = excl;
+        for (int t = 0; t < T; ++t) {
+          for (int ww = 0; ww < w; ++ww) v[t] += sh.wave_tot[t * 4 + ww];
+          const uint32_t excl = v[t] - h[t];
+          if (excl <= kk[t] && kk[t] < v[t]) {
+            sh.digit[t] = (uint32_t)tid;
+            sh.before[t] = excl;
+          }
         }
       }
       __syncthreads();
@@ -184,8 +184,8 @@ struct StatsArgs {
   uint32_t *n_flag, *n_degraded;
 };
 
-template <int V>
-__global__ __launch_bounds__(kStatThreads) void xr_kernel_stats(StatsArgs a) {
+template <int NT, int V>
+__global__ __launch_bounds__(NT) void xr_kernel_stats(StatsArgs a) {
   __shared__ SelShared<3> sh3;
   __shared__ SelShared<1> sh1;
   __shared__ uint32_t n_sh;
@@ -201,16 +201,17 @@ __global__ __launch_bounds__(kStatThreads) void xr_kernel_stats(StatsArgs a) {
     red_hi = 0;
   }
   uint64_t key[V];
-  uint32_t vm = 0, cnt = 0;
+  uint64_t vm = 0;
+  uint32_t cnt = 0;
   unsigned long long mn = ~0ull, mx = 0;
   u128 acc = 0;
 #pragma unroll
   for (int j = 0; j < V; ++j) {
-    const int r = tid + j * kStatThreads;
+    const int r = tid + j * NT;
     const int64_t x = r < a.R ? row[r] : -1;
     key[j] = x >= 0 ? (uint64_t)x : 0;
     if (x >= 0) {
-      vm |= 1u << j;
+      vm |= 1ull << j;
       ++cnt;
       mn = (uint64_t)x < mn ? (uint64_t)x : mn;
       mx = (uint64_t)x > mx ? (uint64_t)x : mx;
@@ -255,14 +256,14 @@ __global__ __launch_bounds__(kStatThreads) void xr_kernel_stats(StatsArgs a) {
   const uint32_t nm1 = (uint32_t)(n - 1);
   const uint32_t ranks[3] = {nm1 / 4, nm1 / 2, (uint32_t)((3ull * nm1) / 4)};
   uint64_t qs[3];
-  select_ranks<V, 3>(key, vm, vmax - vmin, ranks, qs, sh3);
+  select_ranks<NT, V, 3>(key, vm, vmax - vmin, ranks, qs, sh3);
   const uint64_t dmed = qs[1];  // median - vmin
 #pragma unroll
   for (int j = 0; j < V; ++j) key[j] = key[j] >= dmed ? key[j] - dmed : dmed - key[j];
   const uint64_t top = vmax - vmin - dmed;
   const uint32_t r1[1] = {nm1 / 2};
   uint64_t md[1];
-  select_ranks<V, 1>(key, vm, top > dmed ? top : dmed, r1, md, sh1);
+  select_ranks<NT, V, 1>(key, vm, top > dmed ? top : dmed, r1, md, sh1);
   if (tid == 0) {
     a.q1[sk] = (int64_t)(vmin + qs[0]);
     a.med[sk] = (int64_t)(vmin + qs[1]);
@@ -294,8 +295,8 @@ __device__ __forceinline__ uint32_t ratio_pm(int64_t x, int64_t med) {
   return q > (uint64_t)INT32_MAX ? (uint32_t)INT32_MAX : (uint32_t)q;
 }
 
-template <int V>
-__global__ __launch_bounds__(kRankThreads) void xr_rank(RankArgs a) {
+template <int NT, int V>
+__global__ __launch_bounds__(NT) void xr_rank(RankArgs a) {
   __shared__ SelShared<1> sh;
   __shared__ uint32_t ne_sh, nf_sh, rmin_sh, rmax_sh;
   const int tid = threadIdx.x;
@@ -312,10 +313,11 @@ __global__ __launch_bounds__(kRankThreads) void xr_rank(RankArgs a) {
   uint32_t fl[(V + 3) / 4];
 #pragma unroll
   for (int j = 0; j < (V + 3) / 4; ++j) fl[j] = 0;
-  uint32_t em = 0, ne = 0, nf = 0, rmin = 0xFFFFFFFFu, rmax = 0;
+  uint64_t em = 0;
+  uint32_t ne = 0, nf = 0, rmin = 0xFFFFFFFFu, rmax = 0;
 #pragma unroll
   for (int j = 0; j < V; ++j) {
-    const int k = tid + j * kRankThreads;
+    const int k = tid + j * NT;
     rat[j] = 0;
     if (k >= K) continue;
     const int64_t c = rs * K + k;
@@ -342,7 +344,7 @@ __global__ __launch_bounds__(kRankThreads) void xr_rank(RankArgs a) {
         if (med >= 1) {
           const uint32_t r = ratio_pm(x, med);
           rat[j] = r;
-          em |= 1u << j;
+          em |= 1ull << j;
           ++ne;
           rmin = r < rmin ? r : rmin;
           rmax = r > rmax ? r : rmax;
@@ -377,13 +379,13 @@ __global__ __launch_bounds__(kRankThreads) void xr_rank(RankArgs a) {
     for (int j = 0; j < V; ++j) rat[j] -= (em >> j) & 1u ? lo : 0u;
     const uint32_t rk[1] = {(uint32_t)(n_eval - 1) / 2};
     uint64_t sel[1];
-    select_ranks<V, 1>(rat, em, rmax_sh - lo, rk, sel, sh);
+    select_ranks<NT, V, 1>(rat, em, rmax_sh - lo, rk, sel, sh);
     score = (int32_t)(lo + (uint32_t)sel[0]);
   }
   const bool strag = n_eval >= a.p.min_kernels && (int64_t)score >= 1000 + (int64_t)a.p.tau_rank_pm;
 #pragma unroll
   for (int j = 0; j < V; ++j) {
-    const int k = tid + j * kRankThreads;
+    const int k = tid + j * NT;
     if (k >= K) continue;
     uint32_t f = (fl[j >> 2] >> (8 * (j & 3))) & 0xFFu;
     if (f & 1) {
@@ -404,14 +406,38 @@ __global__ __launch_bounds__(kRankThreads) void xr_rank(RankArgs a) {
   }
 }
 
-template <int V>
-void launch_stats(const StatsArgs& sa, dim3 g, hipStream_t st) {
-  hipLaunchKernelGGL(xr_kernel_stats<V>, g, dim3(kStatThreads), 0, st, sa);
+// Call f(std::integral_constant<int, NT>, std::integral_constant<int, V>)
+// with a block size NT and the smallest instantiated per-thread count V such
+// that NT * V >= n (n <= 16384): at most 24 values per thread stay in
+// registers without spilling.
+template <typename F>
+void dispatch_block(int n, F&& f) {
+  using std::integral_constant;
+  auto pick = [&](auto nt) {
+    constexpr int NT = decltype(nt)::value;
+    const int v = (n + NT - 1) / NT;
+    if (v <= 1) return f(nt, integral_constant<int, 1>{});
+    if (v <= 2) return f(nt, integral_constant<int, 2>{});
+    if (v <= 4) return f(nt, integral_constant<int, 4>{});
+    if (v <= 8) return f(nt, integral_constant<int, 8>{});
+    if (v <= 12) return f(nt, integral_constant<int, 12>{});
+    if (v <= 16) return f(nt, integral_constant<int, 16>{});
+    if (v <= 20) return f(nt, integral_constant<int, 20>{});
+    return f(nt, integral_constant<int, 24>{});
+  };
+  if (n <= 24 * 256) return pick(integral_constant<int, 256>{});
+  if (n <= 24 * 512) return pick(integral_constant<int, 512>{});
+  return pick(integral_constant<int, 1024>{});
 }
 
-template <int V>
+template <int NT, int V>
+void launch_stats(const StatsArgs& sa, dim3 g, hipStream_t st) {
+  hipLaunchKernelGGL((xr_kernel_stats<NT, V>), g, dim3(NT), 0, st, sa);
+}
+
+template <int NT, int V>
 void launch_rank(const RankArgs& ra, dim3 g, hipStream_t st) {
-  hipLaunchKernelGGL(xr_rank<V>, g, dim3(kRankThreads), 0, st, ra);
+  hipLaunchKernelGGL((xr_rank<NT, V>), g, dim3(NT), 0, st, ra);
 }
 
 }  // namespace
@@ -425,45 +451,12 @@ hipError_t launch_cross_rank(const CrossRankLaunch& l, hipStream_t st) {
   StatsArgs sa{l.xT, R, S, K, l.p.min_ranks, l.o.n_present, l.o.med_ns, l.o.mad_ns, l.o.q1_ns, l.o.q3_ns,
                l.o.xmean_ns, l.o.n_flag, l.o.n_degraded};
   const dim3 g2((unsigned)((int64_t)S * K));
-  switch ((R + kStatThreads - 1) / kStatThreads) {  // values per thread, R <= ARGUS_MAX_XR_RANKS
-#define ARGUS_STATS_CASE(v) \
-  case v:                   \
-    launch_stats<v>(sa, g2, st); \
-    break;
-    ARGUS_STATS_CASE(1) ARGUS_STATS_CASE(2) ARGUS_STATS_CASE(3) ARGUS_STATS_CASE(4) ARGUS_STATS_CASE(5)
-    ARGUS_STATS_CASE(6) ARGUS_STATS_CASE(7) ARGUS_STATS_CASE(8) ARGUS_STATS_CASE(9) ARGUS_STATS_CASE(10)
-    ARGUS_STATS_CASE(11) ARGUS_STATS_CASE(12) ARGUS_STATS_CASE(13) ARGUS_STATS_CASE(14) ARGUS_STATS_CASE(15)
-    default:
-      launch_stats<16>(sa, g2, st);
-#undef ARGUS_STATS_CASE
-  }
+  dispatch_block(R, [&](auto nt, auto v) { launch_stats<decltype(nt)::value, decltype(v)::value>(sa, g2, st); });
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   RankArgs ra{l.count, l.sum_ns, R, S, K, l.p, l.o};
   const dim3 g3((unsigned)((int64_t)R * S));
-  switch ((K + kRankThreads - 1) / kRankThreads) {  // kernels per thread, K <= ARGUS_MAX_XR_KERNELS
-#define ARGUS_RANK_CASE(v) \
-  case v:                  \
-    launch_rank<v>(ra, g3, st); \
-    break;
-    ARGUS_RANK_CASE(1) ARGUS_RANK_CASE(2) ARGUS_RANK_CASE(3) ARGUS_RANK_CASE(4) ARGUS_RANK_CASE(5)
-    ARGUS_RANK_CASE(6) ARGUS_RANK_CASE(7) ARGUS_RANK_CASE(8) ARGUS_RANK_CASE(9) ARGUS_RANK_CASE(10)
-    ARGUS_RANK_CASE(11) ARGUS_RANK_CASE(12) ARGUS_RANK_CASE(13) ARGUS_RANK_CASE(14) ARGUS_RANK_CASE(15)
-    ARGUS_RANK_CASE(16) ARGUS_RANK_CASE(17) ARGUS_RANK_CASE(18) ARGUS_RANK_CASE(20) ARGUS_RANK_CASE(24)
-    ARGUS_RANK_CASE(28)
-    case 19:
-      launch_rank<20>(ra, g3, st);
-      break;
-    case 21: case 22: case 23:
-      launch_rank<24>(ra, g3, st);
-      break;
-    case 25: case 26: case 27:
-      launch_rank<28>(ra, g3, st);
-      break;
-    default:
-      launch_rank<32>(ra, g3, st);
-#undef ARGUS_RANK_CASE
-  }
+  dispatch_block(K, [&](auto nt, auto v) { launch_rank<decltype(nt)::value, decltype(v)::value>(ra, g3, st); });
   return hipGetLastError();
 }
 

@@ -238,6 +238,7 @@ hipError_t launch_iter_windows(const IterWindowsLaunch& l, hipStream_t st) {
   if (l.R == 0) return hipSuccess;
   if (l.S <= 64) return launch_t<64>(a, st);
   if (l.S <= 512) return launch_t<512>(a, st);
+  if (l.S <= 1024) return launch_t<1024>(a, st);
   return launch_t<ARGUS_MAX_L1_STEPS>(a, st);
 }
 
