@@ -3,9 +3,13 @@
 // effective-width measurement, and full-scan change-point detection; the two
 // together classify a rank's series as stable, jitter, regression or both.
 //
-// One 64-lane wavefront per rank; the series, candidate marks and prefix
-// sums live in LDS. All decisions are exact integer comparisons (128-bit
-// products, 256-bit where the relative-std test needs them).
+// One 64-lane wavefront per rank. The series lives in LDS; per-point marks
+// (covered by a candidate window, above the baseline) are 64-bit ballot
+// words, so merged intervals and longest runs come from bit operations; the
+// baseline median is a wavefront radix select; prefix sums for the change
+// point are a chunked wavefront scan. All decisions are exact integer
+// comparisons (128-bit products, 256-bit where the relative-std test needs
+// them).
 #include "argus_internal.h"
 
 namespace argus {
@@ -39,6 +43,16 @@ __device__ __forceinline__ bool rel_std_ok(int64_t n, u128 s, u128 q, int32_t cm
   return cmp_prod((u128)1000000u * (u128)n, v, (u128)cmax_pm * (u128)cmax_pm * (u128)(n - 1), s * s) <= 0;
 }
 
+// inclusive prefix over the wavefront of a 128-bit value
+__device__ __forceinline__ u128 wave_incl_scan128(u128 v) {
+  const int lane = threadIdx.x & 63;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t lo = __shfl_up((uint64_t)v, o, 64), hi = __shfl_up((uint64_t)(v >> 64), o, 64);
+    if (lane >= o) v += ((u128)hi << 64) | lo;
+  }
+  return v;
+}
+
 struct Args {
   const int64_t* step_ns;
   int32_t R, S;
@@ -52,17 +66,71 @@ struct Args {
 };
 
 template <int SCAP>
-__global__ __launch_bounds__(64) void l1_kernel(Args a) {
-  __shared__ int64_t y[SCAP];
-  __shared__ uint8_t cand[SCAP];
-  __shared__ uint8_t fl[SCAP];
-  __shared__ uint64_t pre_s[SCAP + 1];
-  __shared__ u128 pre_q[SCAP + 1];
-  __shared__ u128 best_num[64], best_den[64];
-  __shared__ int32_t best_t[64];
-  __shared__ int32_t iv_a, iv_b, width_sh;
-  __shared__ int64_t base_sh;
+struct L1Smem {
+  int64_t y[SCAP];
+  uint64_t pre_s[SCAP + 1];
+  u128 pre_q[SCAP + 1];
+  uint8_t candw[SCAP];      // window t is a candidate
+  uint8_t fl[SCAP];         // output flag bits 0-1 per point
+  uint64_t cov[SCAP / 64];  // bit i: point i covered by a candidate window
+  uint32_t hist[256];
+  int32_t iv[SCAP / 2 + 1][2];  // merged intervals [a, b] (separated by uncovered points)
+  u128 best_num[64], best_den[64];
+  int32_t best_t[64];
+  int32_t n_iv, width, cpt;
+  uint32_t digit, before;
+};
 
+// Lower median (rank (m-1)/2) of y over the m points outside [ea, eb] (no
+// exclusion when ea > eb), by MSD radix select over 8-bit digits of y
+// (every y < 2^40). Wavefront-wide.
+template <int SCAP>
+__device__ int64_t wave_lower_median(L1Smem<SCAP>& sm, int S, int ea, int eb) {
+  const int lane = threadIdx.x & 63;
+  uint32_t m = 0;
+  for (int i = lane; i < S; i += 64) m += !(i >= ea && i <= eb);
+  for (int o = 32; o > 0; o >>= 1) m += __shfl_xor(m, o, 64);
+  uint32_t k = (m - 1) / 2;
+  uint64_t prefix = 0;
+  for (int shift = 32; shift >= 0; shift -= 8) {
+    for (int b = lane; b < 256; b += 64) sm.hist[b] = 0;
+    __syncthreads();
+    for (int i = lane; i < S; i += 64) {
+      if (i >= ea && i <= eb) continue;
+      const uint64_t v = (uint64_t)sm.y[i];
+      if (shift == 32 || (v >> (shift + 8)) == prefix) atomicAdd(&sm.hist[(v >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    // lane owns bins 4 lane .. 4 lane + 3
+    uint32_t h[4], tot = 0;
+    for (int j = 0; j < 4; ++j) {
+      h[j] = sm.hist[4 * lane + j];
+      tot += h[j];
+    }
+    uint32_t incl = tot;
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t n = __shfl_up(incl, o, 64);
+      if (lane >= o) incl += n;
+    }
+    uint32_t run = incl - tot;
+    for (int j = 0; j < 4; ++j) {
+      if (run <= k && k < run + h[j]) {
+        sm.digit = 4 * lane + j;
+        sm.before = run;
+      }
+      run += h[j];
+    }
+    __syncthreads();
+    prefix = (prefix << 8) | sm.digit;
+    k -= sm.before;
+    __syncthreads();
+  }
+  return (int64_t)prefix;
+}
+
+template <int SCAP>
+__global__ __launch_bounds__(64) void l1_kernel(Args a) {
+  __shared__ L1Smem<SCAP> sm;
   const int lane = threadIdx.x;
   const int64_t r = blockIdx.x;
   const int S = a.S;
@@ -79,9 +147,8 @@ __global__ __launch_bounds__(64) void l1_kernel(Args a) {
   bool ok = true;
   for (int i = lane; i < S; i += 64) {
     const int64_t v = yr[i];
-    y[i] = v;
-    cand[i] = 0;
-    fl[i] = 0;
+    sm.y[i] = v;
+    sm.fl[i] = 0;
     ok &= v >= 0 && v < kYLimit;
   }
   ok = __all(ok);
@@ -98,96 +165,136 @@ __global__ __launch_bounds__(64) void l1_kernel(Args a) {
     return;
   }
 
-  // sensitivity gating: windows whose max/min ratio exceeds theta
+  // sensitivity gating: window t = [t, t+w-1] is a candidate when its
+  // max/min ratio exceeds theta
   const int w = a.p.W < S ? a.p.W : S;
-  for (int t = lane; t + w <= S; t += 64) {
-    int64_t mx = y[t], mn = y[t];
+  const int nwin = S - w + 1;
+  for (int t = lane; t < nwin; t += 64) {
+    int64_t mx = sm.y[t], mn = sm.y[t];
     for (int i = t + 1; i < t + w; ++i) {
-      mx = y[i] > mx ? y[i] : mx;
-      mn = y[i] < mn ? y[i] : mn;
+      mx = sm.y[i] > mx ? sm.y[i] : mx;
+      mn = sm.y[i] < mn ? sm.y[i] : mn;
     }
-    if ((u128)1000u * (u128)mx > (u128)a.p.theta_pm * (u128)mn)
-      for (int i = t; i < t + w; ++i) cand[i] = 1;
+    sm.candw[t] = (u128)1000u * (u128)mx > (u128)a.p.theta_pm * (u128)mn;
   }
   __syncthreads();
-
-  // effective width per merged interval (maximal run of candidate points)
+  // point i is covered when a candidate window contains it
+  for (int i0 = 0; i0 < S; i0 += 64) {
+    const int i = i0 + lane;
+    bool c = false;
+    if (i < S) {
+      const int t_lo = i - w + 1 > 0 ? i - w + 1 : 0, t_hi = i < nwin - 1 ? i : nwin - 1;
+      for (int t = t_lo; t <= t_hi && !c; ++t) c = sm.candw[t] != 0;
+    }
+    const unsigned long long word = __ballot(c);
+    if (lane == 0) sm.cov[i0 >> 6] = word;
+  }
+  __syncthreads();
+  // merged intervals: maximal runs of covered points (overlapping or
+  // touching candidate windows merge)
   if (lane == 0) {
-    width_sh = 0;
-    iv_b = -1;
+    int n = 0, i = 0;
+    while (i < S) {
+      const uint64_t rest = sm.cov[i >> 6] >> (i & 63);
+      if (rest == 0) {
+        i = ((i >> 6) + 1) << 6;
+        continue;
+      }
+      i += __builtin_ctzll(rest);
+      if (i >= S) break;
+      int j = i;  // first uncovered point at or after i
+      while (j < S) {
+        const uint64_t ones = sm.cov[j >> 6] >> (j & 63);
+        const int avail = 64 - (j & 63);
+        int len = ~ones == 0 ? 64 : __builtin_ctzll(~ones);
+        if (len > avail) len = avail;
+        j += len;
+        if (len < avail) break;
+      }
+      if (j > S) j = S;
+      sm.iv[n][0] = i;
+      sm.iv[n][1] = j - 1;
+      ++n;
+      i = j;
+    }
+    sm.n_iv = n;
+    sm.width = 0;
   }
   __syncthreads();
-  while (true) {
-    if (lane == 0) {
-      int s0 = iv_b + 1;
-      while (s0 < S && !cand[s0]) ++s0;
-      int e0 = s0;
-      while (e0 + 1 < S && cand[e0 + 1]) ++e0;
-      iv_a = s0 < S ? s0 : -1;
-      iv_b = e0;
-    }
-    __syncthreads();
-    const int ia = iv_a, ib = iv_b;
-    if (ia < 0) break;
-    // baseline: lower median of the points outside [ia, ib] (all if none),
-    // found by counting: v is the target-th smallest iff
-    // #{< v} <= target < #{<= v}
-    const int m_out = S - (ib - ia + 1);
-    const bool use_all = m_out == 0;
-    const int target = ((use_all ? S : m_out) - 1) / 2;
-    for (int j = lane; j < S; j += 64) {
-      if (!use_all && j >= ia && j <= ib) continue;
-      const int64_t v = y[j];
-      int lt = 0, le = 0;
-      for (int i = 0; i < S; ++i) {
-        if (!use_all && i >= ia && i <= ib) continue;
-        lt += y[i] < v;
-        le += y[i] <= v;
+  const int n_iv = sm.n_iv;
+  for (int q = 0; q < n_iv; ++q) {
+    const int ia = sm.iv[q][0], ib = sm.iv[q][1];
+    // baseline: lower median of the points outside [ia, ib], of all points
+    // when none lie outside
+    const bool all_inside = ia == 0 && ib == S - 1;
+    const int64_t base = all_inside ? wave_lower_median(sm, S, 1, 0) : wave_lower_median(sm, S, ia, ib);
+    // points significantly above the baseline; the longest contiguous run
+    // of them is the interval's effective width (wave-uniform bit scan)
+    int best = 0, run = 0;
+    for (int i0 = ia; i0 <= ib; i0 += 64) {
+      const int i = i0 + lane;
+      bool ex = false;
+      if (i <= ib) {
+        ex = (u128)1000u * (u128)sm.y[i] > (u128)a.p.beta_pm * (u128)base;
+        sm.fl[i] = ex ? 3 : 1;
       }
-      if (lt <= target && target < le) base_sh = v;
-    }
-    __syncthreads();
-    if (lane == 0) {
-      const int64_t base = base_sh;
-      int run = 0, best = width_sh;
-      for (int i = ia; i <= ib; ++i) {
-        uint8_t f = 1;
-        if ((u128)1000u * (u128)y[i] > (u128)a.p.beta_pm * (u128)base) {
-          f |= 2;
-          ++run;
+      const uint64_t word = __ballot(ex);
+      const int nbits = ib - i0 + 1 < 64 ? ib - i0 + 1 : 64;
+      int b = 0;
+      while (b < nbits) {
+        const uint64_t rest = word >> b;
+        if (rest & 1u) {
+          int len = ~rest == 0 ? 64 - b : __builtin_ctzll(~rest);
+          if (b + len > nbits) len = nbits - b;
+          run += len;
           best = run > best ? run : best;
+          b += len;
         } else {
           run = 0;
+          b = rest == 0 ? nbits : b + __builtin_ctzll(rest);
         }
-        fl[i] = f;
       }
-      width_sh = best;
     }
+    if (lane == 0 && best > sm.width) sm.width = best;
     __syncthreads();
   }
 
-  // change point: prefix sums, then each lane scans its share of splits
+  // change point: chunked prefix sums (each lane sums a contiguous chunk,
+  // one wavefront scan of the chunk totals, then each lane fills its chunk)
+  const int chunk = (S + 63) / 64;
+  const int c0 = lane * chunk, c1 = c0 + chunk < S ? c0 + chunk : S;
+  uint64_t ls = 0;
+  u128 lq = 0;
+  for (int i = c0; i < c1; ++i) {
+    ls += (uint64_t)sm.y[i];
+    lq += (u128)(uint64_t)sm.y[i] * (u128)(uint64_t)sm.y[i];
+  }
+  uint64_t es = ls;
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t n = __shfl_up(es, o, 64);
+    if (lane >= o) es += n;
+  }
+  es -= ls;
+  u128 eq = wave_incl_scan128(lq) - lq;
   if (lane == 0) {
-    uint64_t s = 0;
-    u128 q = 0;
-    pre_s[0] = 0;
-    pre_q[0] = 0;
-    for (int i = 0; i < S; ++i) {
-      s += (uint64_t)y[i];
-      q += (u128)(uint64_t)y[i] * (u128)(uint64_t)y[i];
-      pre_s[i + 1] = s;
-      pre_q[i + 1] = q;
-    }
+    sm.pre_s[0] = 0;
+    sm.pre_q[0] = 0;
+  }
+  for (int i = c0; i < c1; ++i) {
+    es += (uint64_t)sm.y[i];
+    eq += (u128)(uint64_t)sm.y[i] * (u128)(uint64_t)sm.y[i];
+    sm.pre_s[i + 1] = es;
+    sm.pre_q[i + 1] = eq;
   }
   __syncthreads();
   int32_t bt = -1;
   u128 bn = 0, bd = 1;
   const int ms = a.p.min_seg;
   for (int t = (ms > 1 ? ms : 1) + lane; t <= S - ms; t += 64) {
-    const u128 sl = pre_s[t], ql = pre_q[t];
-    const u128 sr = (u128)pre_s[S] - sl, qr = pre_q[S] - ql;
+    const u128 sl = sm.pre_s[t], ql = sm.pre_q[t];
+    const u128 sr = (u128)sm.pre_s[S] - sl, qr = sm.pre_q[S] - ql;
     const int64_t nl = t, nr = S - t;
-    if (sl == 0) continue;
+    if (sl == 0) continue;  // the ratio needs a positive left mean
     const u128 num = sr * (u128)nl, den = sl * (u128)nr;
     if ((u128)1000u * num < (u128)a.p.rho_pm * den) continue;
     if (!rel_std_ok(nl, sl, ql, a.p.cmax_pm) || !rel_std_ok(nr, sr, qr, a.p.cmax_pm)) continue;
@@ -197,32 +304,32 @@ __global__ __launch_bounds__(64) void l1_kernel(Args a) {
       bd = den;
     }
   }
-  best_t[lane] = bt;
-  best_num[lane] = bn;
-  best_den[lane] = bd;
+  sm.best_t[lane] = bt;
+  sm.best_num[lane] = bn;
+  sm.best_den[lane] = bd;
   __syncthreads();
   if (lane == 0) {
     int32_t t0 = -1;
     u128 n0 = 0, d0 = 1;
     for (int l = 0; l < 64; ++l) {
-      const int32_t t = best_t[l];
+      const int32_t t = sm.best_t[l];
       if (t < 0) continue;
-      const int c = t0 < 0 ? 1 : cmp_prod(best_num[l], d0, n0, best_den[l]);
+      const int c = t0 < 0 ? 1 : cmp_prod(sm.best_num[l], d0, n0, sm.best_den[l]);
       if (c > 0 || (c == 0 && t < t0)) {
         t0 = t;
-        n0 = best_num[l];
-        d0 = best_den[l];
+        n0 = sm.best_num[l];
+        d0 = sm.best_den[l];
       }
     }
-    iv_a = t0;
+    sm.cpt = t0;
     a.cp[r] = t0;
     if (a.cp_ratio) a.cp_ratio[r] = t0 >= 0 ? (float)((double)n0 / (double)d0) : 0.0f;
-    a.eff_width[r] = width_sh;
-    a.cls[r] = (uint8_t)((width_sh > 0 ? 1 : 0) | (t0 >= 0 ? 2 : 0));
+    a.eff_width[r] = sm.width;
+    a.cls[r] = (uint8_t)((sm.width > 0 ? 1 : 0) | (t0 >= 0 ? 2 : 0));
   }
   __syncthreads();
-  const int cpt = iv_a;
-  for (int i = lane; i < S; i += 64) a.flags[r * S + i] = fl[i] | ((cpt >= 0 && i >= cpt) ? 4 : 0);
+  const int cpt = sm.cpt;
+  for (int i = lane; i < S; i += 64) a.flags[r * S + i] = sm.fl[i] | ((cpt >= 0 && i >= cpt) ? 4 : 0);
 }
 
 template <int SCAP>

@@ -221,8 +221,8 @@ struct Seg {
   }
 };
 
-// Four events of one thread: validity, per-segment aggregates, then the
-// per-kernel updates with the LDS lookups of all four issued up front.
+// Four events of one thread: validity and per-segment aggregates, then the
+// per-kernel updates.
 template <int NSLOT, int WIN, bool MAPPED>
 __device__ __forceinline__ void process4(Seg<NSLOT, WIN, MAPPED>& sg, const Args& a, const int32_t (&kid)[4],
                                          const int32_t (&st)[4], const int64_t (&t0)[4], const int64_t (&t1)[4],
@@ -248,31 +248,37 @@ __device__ __forceinline__ void process4(Seg<NSLOT, WIN, MAPPED>& sg, const Args
     }
     lk[j] = valid && (unsigned)(kid[j] - kb) < (unsigned)nk ? kid[j] - kb : -1;
   }
-  int slot[4];
-  if (MAPPED) {
-    uint32_t e[4];
+  // per-kernel updates two events at a time: their LDS lookups are issued
+  // together, and the live register set stays small enough that nothing
+  // spills around the scan loop
 #pragma unroll
-    for (int j = 0; j < 4; ++j) e[j] = lk[j] >= 0 ? sg.map_get(lk[j]) : kMapDone;
+  for (int h = 0; h < 4; h += 2) {
+    int slot[2];
+    if (MAPPED) {
+      uint32_t e[2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) slot[j] = e[j] < (uint32_t)NSLOT ? (int)e[j] : -1;
+      for (int j = 0; j < 2; ++j) e[j] = lk[h + j] >= 0 ? sg.map_get(lk[h + j]) : kMapDone;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (lk[j] >= 0 && e[j] >= (uint32_t)NSLOT && e[j] != kMapDone && e[j] != kMapDefer)
-        slot[j] = sg.map_claim(lk[j], e[j]);
-  } else {
+      for (int j = 0; j < 2; ++j) {
+        slot[j] = e[j] < (uint32_t)NSLOT ? (int)e[j] : -1;
+        if (lk[h + j] >= 0 && e[j] >= (uint32_t)NSLOT && e[j] != kMapDone && e[j] != kMapDefer)
+          slot[j] = sg.map_claim(lk[h + j], e[j]);
+      }
+    } else {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) slot[j] = lk[j];
+      for (int j = 0; j < 2; ++j) slot[j] = lk[h + j];
+    }
+    uint32_t m[2];
+    v2l mmv[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      m[j] = slot[j] >= 0 ? sg.sm.meta[slot[j]] : 0u;
+      mmv[j] = slot[j] >= 0 ? *reinterpret_cast<const v2l*>(&sg.sm.mm[slot[j]][0]) : v2l{0, 0};
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      if (slot[j] >= 0) sg.slot_add(slot[j], m[j], d[h + j], mmv[j]);
   }
-  uint32_t m[4];
-  v2l mmv[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    m[j] = slot[j] >= 0 ? sg.sm.meta[slot[j]] : 0u;
-    mmv[j] = slot[j] >= 0 ? *reinterpret_cast<const v2l*>(&sg.sm.mm[slot[j]][0]) : v2l{0, 0};
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    if (slot[j] >= 0) sg.slot_add(slot[j], m[j], d[j], mmv[j]);
 }
 
 template <int NSLOT, int WIN, bool MAPPED>
@@ -288,7 +294,9 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
   while (true) {
   if (tid == 0) g_next = (int64_t)atomicAdd(a.queue, 1u);
   __syncthreads();
-  const int64_t g = g_next;
+  // the segment index is wave-uniform: keep it (and what derives from it:
+  // bounds, loop limits) in scalar registers
+  const int64_t g = (int64_t)__builtin_amdgcn_readfirstlane((int)g_next);
   if (g >= a.n_seg) break;
 
   int64_t lo = a.seg_off[g], hi = a.seg_off[g + 1];
