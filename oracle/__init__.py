@@ -19,6 +19,8 @@ NB = 32
 XR_DEFAULTS = dict(min_ranks=3, c_min_pair=8, min_kernels=8, k_mad_pm=5189, ratio_pm=1250, alpha_pm=1500,
                    tau_rank_pm=20)
 L1_DEFAULTS = dict(W=5, theta_pm=1500, beta_pm=1200, rho_pm=1300, cmax_pm=100, min_seg=2)
+KDE_DEFAULTS = dict(sub_bits=6, frac_pm=50, min_count=3, gap=48)
+KDE_MAXC = 4
 
 _lib = None
 
@@ -38,6 +40,12 @@ def lib():
         L.orc_cross_rank.restype = ctypes.c_int
         L.orc_iter_windows.argtypes = [I32, I32, V] + [I32] * 6 + [V] * 5
         L.orc_iter_windows.restype = ctypes.c_int
+        L.orc_kde_thresholds.argtypes = [V]
+        L.orc_kde_bin.argtypes = [ctypes.c_uint64, I32]
+        L.orc_kde_bin.restype = ctypes.c_int
+        L.orc_kde_group.argtypes = [I64, V] + [I32] * 4 + [V] * 8
+        L.orc_kde.argtypes = [I64, I32, I32, I64] + [V] * 5 + [I32] * 4 + [V] * 5
+        L.orc_kde.restype = I64
         _lib = L
     return _lib
 
@@ -116,4 +124,71 @@ def iter_windows(step_ns: np.ndarray, R: int, S: int, **params) -> dict:
                                 p["min_seg"], *[_p(out[k]) for k in ("flags", "cls", "eff_width", "cp", "cp_ratio")])
     if rc != 0:
         raise RuntimeError(f"orc_iter_windows failed: {rc}")
+    return out
+
+
+def kde_thresholds() -> np.ndarray:
+    """The 64 mantissa thresholds ceil(2^(23 + t/64)) of the KDE log grid."""
+    th = np.empty(64, np.uint32)
+    lib().orc_kde_thresholds(_p(th))
+    return th
+
+
+def kde_bin(d: int, sub_bits: int = 6) -> int:
+    return lib().orc_kde_bin(d, sub_bits)
+
+
+def _kde_params(params: dict) -> dict:
+    p = dict(KDE_DEFAULTS, **params)
+    assert 1 <= p["sub_bits"] <= 6
+    return p
+
+
+def kde_group(durations, debug: bool = False, **params) -> dict:
+    """Clusters of one group of durations (any order): n_clusters, count,
+    p50, p99 (KDE_MAXC slots), bw_q8 (bandwidth in 1/256 grid steps) and
+    n_cand (valleys before filtering). With debug, also the grid density
+    "f" and the unfiltered valley positions "cand" (grid indices)."""
+    p = _kde_params(params)
+    d = np.ascontiguousarray(np.asarray(durations, dtype=np.uint64).reshape(-1))
+    ncl = np.zeros(1, np.uint8)
+    cnt = np.zeros(KDE_MAXC, np.uint32)
+    p50 = np.zeros(KDE_MAXC, np.int64)
+    p99 = np.zeros(KDE_MAXC, np.int64)
+    bw = np.zeros(1, np.int32)
+    nc = np.zeros(1, np.int32)
+    f = np.zeros(4096, np.uint64) if debug else None
+    cand = np.zeros(4096, np.int32) if debug else None
+    lib().orc_kde_group(d.size, _p(d) if d.size else None, p["sub_bits"], p["frac_pm"], p["min_count"], p["gap"],
+                        _p(ncl), _p(cnt), _p(p50), _p(p99), _p(bw), _p(nc), None if f is None else _p(f),
+                        None if cand is None else _p(cand))
+    out = {"n_clusters": int(ncl[0]), "count": cnt, "p50_ns": p50, "p99_ns": p99, "bw_q8": int(bw[0]),
+           "n_cand": int(nc[0])}
+    if debug and d.size:
+        G = kde_bin(int(d.max()), p["sub_bits"]) - kde_bin(int(d.min()), p["sub_bits"]) + 1
+        out["f"] = f[:G]
+        out["cand"] = cand[:out["n_cand"]]
+    return out
+
+
+def kde(ev: dict, n_kernels: int, n_streams: int, n_events: int | None = None, **params) -> dict:
+    """Clusters of every (segment, kernel) group of a raw event trace."""
+    p = _kde_params(params)
+    kid = np.ascontiguousarray(ev["kernel_id"], dtype=np.int32)
+    st = np.ascontiguousarray(ev["stream"], dtype=np.int32)
+    t0 = np.ascontiguousarray(ev["start_ns"], dtype=np.int64)
+    t1 = np.ascontiguousarray(ev["end_ns"], dtype=np.int64)
+    off = np.ascontiguousarray(ev["seg_off"], dtype=np.int64)
+    G = len(off) - 1
+    C = G * n_kernels
+    n = len(kid) if n_events is None else n_events
+    out = {"n_clusters": np.empty(C, np.uint8), "count": np.empty(C * KDE_MAXC, np.uint32),
+           "p50_ns": np.empty(C * KDE_MAXC, np.int64), "p99_ns": np.empty(C * KDE_MAXC, np.int64),
+           "bw_q8": np.empty(C, np.int32)}
+    bad = lib().orc_kde(G, n_kernels, n_streams, n, _p(kid), _p(st), _p(t0), _p(t1), _p(off), p["sub_bits"],
+                        p["frac_pm"], p["min_count"], p["gap"],
+                        *[_p(out[k]) for k in ("n_clusters", "count", "p50_ns", "p99_ns", "bw_q8")])
+    for k in ("count", "p50_ns", "p99_ns"):
+        out[k] = out[k].reshape(C, KDE_MAXC)
+    out["bad_segments"] = int(bad)
     return out

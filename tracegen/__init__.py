@@ -13,7 +13,9 @@ Workload shapes:
   section 5.2); stream = kernel id mod n_streams;
 * durations are lognormal around a per-kernel base (log of the base uniform
   over [ln 2 us, ln 5 ms], sigma 0.1 in ln), or Pareto(alpha 1.5, x_m 10 us)
-  for the "hot" communication-like ids of the skew workload;
+  for the "hot" communication-like ids of the skew workload; a share of the
+  lognormal ids runs at 2 or 3 scales (x1, x3, x9) depending on the template
+  position, the multimodal per-kernel durations of section 5.2;
 * injected faults follow the case-study shapes: whole-rank slowdowns
   (stragglers, section 9.1), single degraded (rank, kernel) pairs (Appendix D
   table), host stalls that stretch one step without slowing any kernel
@@ -64,6 +66,7 @@ class TraceConfig:
     pair_pm: tuple = (1000, 1000)
     n_anomalous: int = 0           # host-stalled (rank, step) segments
     masked_straggler: bool = False  # skew: one rank slow on cold ids, peers slow on hot ids
+    modal_pm: int = 300            # permille of lognormal ids whose positions run at several scales
 
     @property
     def n_segments(self) -> int:
@@ -111,7 +114,7 @@ class _Params(ctypes.Structure):
     ]
 
 
-_TABLE_FIELDS = ["tmpl_kid", "tmpl_off", "base_ns", "ln_q24", "pareto_ns", "mult_hot_pm", "mult_cold_pm",
+_TABLE_FIELDS = ["tmpl_kid", "tmpl_off", "tmpl_base_ns", "ln_q24", "pareto_ns", "mult_hot_pm", "mult_cold_pm",
                  "pair_off", "pair_kid", "pair_pm", "stall_rep", "stall_ns"]
 
 
@@ -202,9 +205,22 @@ class Trace:
         else:
             raise ValueError(cfg.ids)
         self.tmpl_kid = kid
+        # multimodal ids: the same kernel at different template positions runs
+        # at different scales (section 5.2: one collective at two positions
+        # moving different volumes). Half of the chosen ids are bimodal
+        # (x1, x3), half trimodal (x1, x3, x9); each position draws its scale
+        # uniformly from its id's set. Drawn from a stream of its own so the
+        # injections below do not depend on it.
+        mrng = np.random.default_rng([cfg.seed, 0x4D4F4445])
+        modal = (mrng.random(K) < cfg.modal_pm / 1000.0) & (np.arange(K) >= cfg.n_hot)
+        n_modes = np.where(modal, np.where(mrng.random(K) < 0.5, 2, 3), 1)
+        mode = (mrng.random(T) * n_modes[kid]).astype(np.int64)
+        self.tmpl_mode_pm = (1000 * 3 ** mode).astype(np.int64)
+        self.n_modes = n_modes
+        self.tmpl_base_ns = np.where(kid < cfg.n_hot, 0, self.base_ns[kid] * self.tmpl_mode_pm // 1000)
         # per-stream cursors: each stream runs its template launches back to
         # back with 1-20 us gaps
-        nominal = np.where(kid < cfg.n_hot, 3 * PARETO_XM_NS, self.base_ns[kid])
+        nominal = np.where(kid < cfg.n_hot, 3 * PARETO_XM_NS, self.tmpl_base_ns)
         gaps = rng.integers(1_000, 20_001, size=T)
         cursor = np.zeros(NS, dtype=np.int64)
         off = np.zeros(T, dtype=np.int64)
@@ -275,7 +291,7 @@ class Trace:
         self._params = _Params(cfg.seed, R, S, K, NS, T, cfg.n_hot, cfg.swap_pm, cfg.invalid_ppm,
                                EPOCH_NS, self.step_period_ns, self.t_span_ns)
         self._host_tables = {
-            "tmpl_kid": self.tmpl_kid, "tmpl_off": self.tmpl_off, "base_ns": self.base_ns,
+            "tmpl_kid": self.tmpl_kid, "tmpl_off": self.tmpl_off, "tmpl_base_ns": self.tmpl_base_ns,
             "ln_q24": self.ln_q24, "pareto_ns": self.pareto_ns, "mult_hot_pm": self.mult_hot_pm,
             "mult_cold_pm": self.mult_cold_pm, "pair_off": self.pair_off, "pair_kid": self.pair_kid,
             "pair_pm": self.pair_pm, "stall_rep": self.stall_rep, "stall_ns": self.stall_ns,

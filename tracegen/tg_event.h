@@ -50,7 +50,7 @@ typedef struct tg_params {
 typedef struct tg_tables {
   const int32_t* tmpl_kid;     /* [T] kernel id of template position p */
   const int64_t* tmpl_off;     /* [T] nominal start offset of position p within a repetition */
-  const int64_t* base_ns;      /* [K] nominal duration of kernel id k */
+  const int64_t* tmpl_base_ns; /* [T] nominal duration at position p (kernel base x position mode) */
   const uint32_t* ln_q24;      /* [65536] lognormal multipliers in 8.24 fixed point */
   const uint32_t* pareto_ns;   /* [65536] Pareto quantiles in ns */
   const int32_t* mult_hot_pm;  /* [R] per-rank multiplier (permille) for ids < n_hot */
@@ -100,7 +100,7 @@ TG_HD void tg_event(const tg_params_t* P, const tg_tables_t* Tb, int32_t r, int3
     d = (int64_t)Tb->pareto_ns[u & 0xFFFFu];
     m = Tb->mult_hot_pm[r];
   } else {
-    d = (int64_t)(((uint64_t)Tb->base_ns[kid] * (uint64_t)Tb->ln_q24[u & 0xFFFFu]) >> 24);
+    d = (int64_t)(((uint64_t)Tb->tmpl_base_ns[p] * (uint64_t)Tb->ln_q24[u & 0xFFFFu]) >> 24);
     m = Tb->mult_cold_pm[r];
   }
   d = d * m / 1000;
