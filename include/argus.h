@@ -16,6 +16,10 @@
  *   argus_iter_windows  per-rank step times -> L1 jitter windows, effective
  *                       width, change point and class (section 6.1,
  *                       Appendix B).
+ *   argus_kde           raw events + their summaries -> per (rank, step,
+ *                       kernel id) duration clusters from the valleys of a
+ *                       Gaussian KDE over log-duration, each reported as
+ *                       (count, p50, p99) (section 5.2, Eq. 1).
  *
  * Conventions for every entry point:
  *   - All array pointers are DEVICE pointers owned by the caller. The library
@@ -53,6 +57,8 @@ extern "C" {
 #define ARGUS_MAX_XR_RANKS 16384 /* argus_cross_rank: n_ranks limit */
 #define ARGUS_MAX_XR_KERNELS 16384 /* argus_cross_rank: n_kernels limit */
 #define ARGUS_MAX_L1_STEPS 4096  /* argus_iter_windows: n_steps limit */
+#define ARGUS_MAX_KDE_KERNELS 16384 /* argus_kde: n_kernels limit */
+#define ARGUS_KDE_MAXC 4         /* argus_kde: clusters reported per cell */
 
 enum {
   ARGUS_OK = 0,
@@ -65,7 +71,9 @@ enum {
 /* device-detected condition bits OR-ed into *dev_status */
 enum {
   ARGUS_DEV_BAD_SEGMENT = 1, /* some seg_off range was malformed; that segment was summarized as empty */
-  ARGUS_DEV_L1_DOMAIN = 2    /* some rank had a step time outside [0, 2^40) ns; that rank got class 0x80 */
+  ARGUS_DEV_L1_DOMAIN = 2,   /* some rank had a step time outside [0, 2^40) ns; that rank got class 0x80 */
+  ARGUS_DEV_KDE_SUMMARY = 4  /* argus_kde: the summaries passed in do not match the events (counts, min or
+                                max); the affected cells report 0 clusters */
 };
 
 int argus_abi_version(void);
@@ -230,6 +238,74 @@ int argus_iter_windows(const int64_t* step_ns, int32_t n_ranks, int32_t n_steps,
                        int32_t* eff_width /* [n_ranks] */, int32_t* cp /* [n_ranks] */,
                        float* cp_ratio /* [n_ranks] */, int32_t* dev_status, void* workspace, size_t workspace_bytes,
                        void* stream);
+
+/* ---------------------------------------------------------------------- KDE
+ *
+ * Section 5.2 (Eq. 1): every (rank, step, kernel id) group of valid
+ * durations is clustered at the valleys of a Gaussian kernel density
+ * estimate over log-duration, and each cluster is summarised as (count, p50,
+ * p99). Definition, step by step (every step is exact integer arithmetic
+ * except where noted):
+ *  1. Grid: x(d) = floor(2^sub_bits * log2 d'), with d' = d truncated to its
+ *     24 leading significant bits (exact for d < 2^24) and x(0) = x(1) = 0.
+ *     The group's grid is every integer from x(min) to x(max), G points.
+ *  2. Bandwidth (Scott's rule as the paper prints it, in grid steps):
+ *     var = (n * sum x^2 - (sum x)^2) / (n (n - 1)) evaluated in double from
+ *     exact integer sums, h = (1.06 * sqrt(var)) * n^-0.2,
+ *     H = floor(256 h + 0.5); n < 2 gives H = 0. Reported as bw_q8.
+ *  3. Density: w(t) = floor(65536 exp(-32768 t^2 / H^2) + 0.5) (double),
+ *     f(j) = sum_b c(b) w(|j - b|) over the group's grid histogram c.
+ *  4. Valleys (H > 0, G >= 3): each maximal run of equal f strictly below
+ *     both neighbouring values, at the middle of the run (rounded down);
+ *     a boundary keeps its own grid point in the lower cluster.
+ *  5. Cluster-level filter: while the smallest cluster (the lowest one on
+ *     ties) has fewer than max(min_count, ceil(frac_pm * n / 1000)) samples,
+ *     drop a valley next to it: the only one at either end, else the one
+ *     with the larger f (the upper one on ties).
+ *  6. Spacing filter: over the boundary list (lowest grid value, valleys,
+ *     highest grid value), while two neighbours lie fewer than gap grid
+ *     steps apart, take the lowest such pair and drop its valley, or of two
+ *     valleys the one with the larger f (the upper one on ties).
+ *  7. Cap: while more than ARGUS_KDE_MAXC clusters remain, drop the valley
+ *     with the largest f (the upper one on ties).
+ *  8. Per cluster, ascending: count; p50 = the lower median and p99 = the
+ *     element ceil(0.99 m) (nearest rank) of its m raw durations, sorted.
+ * The only floating-point steps are sqrt, n^-0.2 and exp in step 2 and 3;
+ * integer outputs follow from them exactly. Thresholds and tie rules are
+ * this library's readings: the paper names the filters but gives no values.
+ *
+ * Inputs: the events (same rules as argus_summarize) and the count, min_ns
+ * and max_ns outputs of argus_summarize over those same events. If they do
+ * not match, the affected cells report 0 clusters and ARGUS_DEV_KDE_SUMMARY
+ * is raised; nothing outside the outputs and the workspace is written.
+ * Malformed segments contribute nothing (their summarized counts are 0).
+ */
+typedef struct argus_kde_params {
+  int32_t sub_bits;  /* grid points per octave = 2^sub_bits, 1..6, default 6 */
+  int32_t frac_pm;   /* cluster-level filter share in permille, 0..1000, default 50 */
+  int32_t min_count; /* cluster-level filter minimum, >= 1, default 3 */
+  int32_t gap;       /* spacing filter, grid steps, >= 0, default 48 (0.75 octave at sub_bits 6) */
+} argus_kde_params_t;
+
+typedef struct argus_kde_out {
+  uint8_t* n_clusters; /* [n_ranks][n_steps][n_kernels]; 0 for empty cells */
+  uint32_t* count;     /* [..][ARGUS_KDE_MAXC]; slots past n_clusters are 0 */
+  int64_t* p50_ns;     /* [..][ARGUS_KDE_MAXC]; slots past n_clusters are 0 */
+  int64_t* p99_ns;     /* [..][ARGUS_KDE_MAXC]; slots past n_clusters are 0 */
+  int32_t* bw_q8;      /* optional [..]: H of step 2 */
+  int32_t* dev_status; /* optional */
+} argus_kde_out_t;
+
+void argus_kde_default(argus_kde_params_t* p);
+
+/* Workspace bytes: 8 per event plus 8 per cell plus a fixed part. */
+size_t argus_kde_workspace(const argus_events_t* ev);
+
+/* ev: as for argus_summarize, n_kernels <= ARGUS_MAX_KDE_KERNELS.
+ * sum: only count, min_ns and max_ns are read. The workspace must be
+ * 256-byte aligned. */
+int argus_kde(const argus_events_t* ev, const argus_summary_t* sum, const argus_kde_params_t* params,
+              const argus_kde_out_t* out, void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

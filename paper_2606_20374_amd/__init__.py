@@ -4,11 +4,12 @@ as hand-written gfx950 HIP kernels behind the C ABI of include/argus.h.
 
 The Python layer only marshals arguments; see argus.py.
 """
-from .argus import (ArgusError, alloc_cross_rank, alloc_iter_windows, alloc_summary, cross_rank, iter_windows,
-                    l1_defaults, lib, summarize, xr_defaults)
+from .argus import (ArgusError, alloc_cross_rank, alloc_iter_windows, alloc_kde, alloc_summary, cross_rank,
+                    iter_windows, kde, kde_defaults, kde_workspace_bytes, l1_defaults, lib, summarize, xr_defaults)
 
-__all__ = ["ArgusError", "alloc_cross_rank", "alloc_iter_windows", "alloc_summary", "cross_rank", "iter_windows",
-           "l1_defaults", "lib", "summarize", "xr_defaults", "run_step"]
+__all__ = ["ArgusError", "alloc_cross_rank", "alloc_iter_windows", "alloc_kde", "alloc_summary", "cross_rank",
+           "iter_windows", "kde", "kde_defaults", "kde_workspace_bytes", "l1_defaults", "lib", "summarize",
+           "xr_defaults", "run_step"]
 
 
 def run_step(ev, n_ranks, n_steps, n_kernels, n_streams, bufs=None):

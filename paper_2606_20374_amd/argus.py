@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(HERE, "libargus.so")
 NBINS = 32
 
 OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
-DEV_BAD_SEGMENT, DEV_L1_DOMAIN = 1, 2
+DEV_BAD_SEGMENT, DEV_L1_DOMAIN, DEV_KDE_SUMMARY = 1, 2, 4
+KDE_MAXC = 4
 
 V, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
 
@@ -54,6 +55,17 @@ class L1Params(ctypes.Structure):
     _fields_ = [(f, I32) for f in ("W", "theta_pm", "beta_pm", "rho_pm", "cmax_pm", "min_seg")]
 
 
+class KdeParams(ctypes.Structure):
+    _fields_ = [(f, I32) for f in ("sub_bits", "frac_pm", "min_count", "gap")]
+
+
+KDE_FIELDS = ["n_clusters", "count", "p50_ns", "p99_ns", "bw_q8", "dev_status"]
+
+
+class KdeOut(ctypes.Structure):
+    _fields_ = [(f, V) for f in KDE_FIELDS]
+
+
 class ArgusError(RuntimeError):
     pass
 
@@ -86,6 +98,11 @@ def lib():
         L.argus_iter_windows_workspace.restype = ctypes.c_size_t
         L.argus_iter_windows.argtypes = [V, I32, I32, P(L1Params), V, V, V, V, V, V, V, ctypes.c_size_t, V]
         L.argus_iter_windows.restype = ctypes.c_int
+        L.argus_kde_default.argtypes = [P(KdeParams)]
+        L.argus_kde_workspace.argtypes = [P(Events)]
+        L.argus_kde_workspace.restype = ctypes.c_size_t
+        L.argus_kde.argtypes = [P(Events), P(Summary), P(KdeParams), P(KdeOut), V, ctypes.c_size_t, V]
+        L.argus_kde.restype = ctypes.c_int
         if L.argus_abi_version() != 1:
             raise ArgusError("libargus ABI version mismatch")
         _lib = L
@@ -120,6 +137,17 @@ def l1_defaults() -> dict:
     return {f: getattr(p, f) for f, _ in L1Params._fields_}
 
 
+def kde_defaults() -> dict:
+    p = KdeParams()
+    lib().argus_kde_default(ctypes.byref(p))
+    return {f: getattr(p, f) for f, _ in KdeParams._fields_}
+
+
+def _events(ev: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: int) -> Events:
+    return Events(_ptr(ev["kernel_id"]), _ptr(ev["stream"]), _ptr(ev["start_ns"]), _ptr(ev["end_ns"]),
+                  _ptr(ev["seg_off"]), ev["kernel_id"].numel(), n_ranks, n_steps, n_kernels, n_streams)
+
+
 # ------------------------------------------------------------------ summarize
 def alloc_summary(n_ranks: int, n_steps: int, n_kernels: int, n_streams: int, device="cuda") -> dict:
     G, C = n_ranks * n_steps, n_ranks * n_steps * n_kernels
@@ -142,8 +170,7 @@ def summarize(ev: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: i
     dev = ev["kernel_id"].device
     if out is None:
         out = alloc_summary(n_ranks, n_steps, n_kernels, n_streams, dev)
-    e = Events(_ptr(ev["kernel_id"]), _ptr(ev["stream"]), _ptr(ev["start_ns"]), _ptr(ev["end_ns"]),
-               _ptr(ev["seg_off"]), ev["kernel_id"].numel(), n_ranks, n_steps, n_kernels, n_streams)
+    e = _events(ev, n_ranks, n_steps, n_kernels, n_streams)
     s = Summary(*[_ptr(out.get(f)) for f in SUMMARY_FIELDS])
     ws = out["_workspace"]
     assert ws.numel() >= lib().argus_summarize_workspace(ctypes.byref(e))
@@ -204,4 +231,40 @@ def iter_windows(step_ns: torch.Tensor, n_ranks: int, n_steps: int, out: Optiona
                                     _ptr(out["cls"]), _ptr(out["eff_width"]), _ptr(out["cp"]),
                                     _ptr(out["cp_ratio"]), _ptr(out["dev_status"]), None, 0, _stream(dev)),
            "argus_iter_windows")
+    return out
+
+
+# ------------------------------------------------------------------------ KDE
+def kde_workspace_bytes(n_events: int, n_ranks: int, n_steps: int, n_kernels: int) -> int:
+    e = Events(0, 0, 0, 0, 0, n_events, n_ranks, n_steps, n_kernels, 1)
+    return lib().argus_kde_workspace(ctypes.byref(e))
+
+
+def alloc_kde(n_events: int, n_ranks: int, n_steps: int, n_kernels: int, device="cuda") -> dict:
+    C = n_ranks * n_steps * n_kernels
+    e = lambda n, dt: torch.empty(n, dtype=dt, device=device)  # noqa: E731
+    ws = kde_workspace_bytes(n_events, n_ranks, n_steps, n_kernels)
+    return {"n_clusters": e(C, torch.uint8), "count": e(C * KDE_MAXC, torch.int32),
+            "p50_ns": e(C * KDE_MAXC, torch.int64), "p99_ns": e(C * KDE_MAXC, torch.int64),
+            "bw_q8": e(C, torch.int32), "dev_status": e(1, torch.int32),
+            "_workspace": e(max(ws, 256), torch.uint8)}
+
+
+def kde(ev: dict, summary: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: int,
+        out: Optional[dict] = None, **params) -> dict:
+    """argus_kde: per-cell duration clusters (n_clusters, count, p50_ns,
+    p99_ns, bw_q8) from the events and their argus_summarize output."""
+    dev = ev["kernel_id"].device
+    if out is None:
+        out = alloc_kde(ev["kernel_id"].numel(), n_ranks, n_steps, n_kernels, dev)
+    p = KdeParams()
+    lib().argus_kde_default(ctypes.byref(p))
+    for k, v in params.items():
+        setattr(p, k, v)
+    e = _events(ev, n_ranks, n_steps, n_kernels, n_streams)
+    s = Summary(*[_ptr(summary.get(f)) if f in ("count", "min_ns", "max_ns") else None for f in SUMMARY_FIELDS])
+    o = KdeOut(*[_ptr(out.get(f)) for f in KDE_FIELDS])
+    ws = out["_workspace"]
+    _check(lib().argus_kde(ctypes.byref(e), ctypes.byref(s), ctypes.byref(p), ctypes.byref(o), _ptr(ws),
+                           ws.numel(), _stream(dev)), "argus_kde")
     return out

@@ -171,4 +171,42 @@ int argus_iter_windows(const int64_t* step_ns, int32_t n_ranks, int32_t n_steps,
   return status_of(launch_iter_windows(l, st));
 }
 
+void argus_kde_default(argus_kde_params_t* p) {
+  if (!p) return;
+  p->sub_bits = 6;
+  p->frac_pm = 50;
+  p->min_count = 3;
+  p->gap = 48;
+}
+
+size_t argus_kde_workspace(const argus_events_t* ev) {
+  if (!ev || ev->n_ranks < 0 || ev->n_steps < 0 || ev->n_kernels < 0 || ev->n_events < 0) return 0;
+  return kde_workspace_bytes(ev->n_events, (int64_t)ev->n_ranks * ev->n_steps * ev->n_kernels);
+}
+
+int argus_kde(const argus_events_t* ev, const argus_summary_t* sum, const argus_kde_params_t* params,
+              const argus_kde_out_t* out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!ev || !sum || !params || !out) return ARGUS_EINVAL;
+  if (ev->n_ranks < 0 || ev->n_steps < 0 || ev->n_events < 0) return ARGUS_EINVAL;
+  if (ev->n_kernels < 1 || ev->n_kernels > ARGUS_MAX_KDE_KERNELS) return ARGUS_EINVAL;
+  if (ev->n_streams < 1 || ev->n_streams > ARGUS_MAX_STREAMS) return ARGUS_EINVAL;
+  const int64_t n_seg = (int64_t)ev->n_ranks * ev->n_steps;
+  if (n_seg > INT32_MAX || n_seg * ev->n_kernels > (int64_t)UINT32_MAX) return ARGUS_EINVAL;
+  if (!ev->seg_off) return ARGUS_EINVAL;
+  if (ev->n_events > 0 && (!ev->kernel_id || !ev->stream || !ev->start_ns || !ev->end_ns)) return ARGUS_EINVAL;
+  if (!sum->count || !sum->min_ns || !sum->max_ns) return ARGUS_EINVAL;
+  if (!out->n_clusters || !out->count || !out->p50_ns || !out->p99_ns) return ARGUS_EINVAL;
+  const argus_kde_params_t& p = *params;
+  if (p.sub_bits < 1 || p.sub_bits > 6 || p.frac_pm < 0 || p.frac_pm > 1000 || p.min_count < 1 || p.gap < 0)
+    return ARGUS_EINVAL;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0 ||
+      workspace_bytes < argus_kde_workspace(ev))
+    return ARGUS_EINVAL;
+  int rc = check_device();
+  if (rc != ARGUS_OK) return rc;
+  KdeLaunch l{ev->kernel_id, ev->stream, ev->start_ns, ev->end_ns, ev->seg_off, ev->n_events, (int32_t)n_seg,
+              ev->n_kernels, ev->n_streams, sum->count, sum->min_ns, sum->max_ns, p, *out, workspace};
+  return status_of(launch_kde(l, (hipStream_t)stream));
+}
+
 }  // extern "C"

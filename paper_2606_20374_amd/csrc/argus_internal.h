@@ -97,6 +97,24 @@ struct IterWindowsLaunch {
 };
 hipError_t launch_iter_windows(const IterWindowsLaunch& a, hipStream_t st);
 
+struct KdeLaunch {
+  const int32_t* kernel_id;
+  const int32_t* stream;
+  const int64_t* start_ns;
+  const int64_t* end_ns;
+  const int64_t* seg_off;
+  int64_t n_events;
+  int32_t n_seg, n_kernels, n_streams;
+  const uint32_t* count;
+  const int64_t* min_ns;
+  const int64_t* max_ns;
+  argus_kde_params_t p;
+  argus_kde_out_t o;
+  void* workspace;  // kde_workspace_bytes(n_events, n_seg * n_kernels), 256-byte aligned
+};
+hipError_t launch_kde(const KdeLaunch& a, hipStream_t st);
+size_t kde_workspace_bytes(int64_t n_events, int64_t cells);
+
 // Zero the optional device status word and the optional queue counter.
 hipError_t launch_clear(int32_t* dev_status, uint32_t* queue, hipStream_t st);
 

@@ -91,3 +91,49 @@ def oracle_summary_sharded(trace, g_begin=0, g_end=None, chunk=32, n_threads=Non
     with ThreadPoolExecutor(n_threads) as ex:
         list(ex.map(work, range(g_begin, g_end, chunk)))
     return out
+
+
+KDE_FIELDS = ["n_clusters", "count", "p50_ns", "p99_ns", "bw_q8"]
+
+
+def oracle_kde_segments(trace, segments, n_threads=None, **params) -> dict:
+    """Oracle KDE clusters of the listed segments (each regenerated on the
+    host and clustered by the unmodified oracle, segments in parallel).
+    Returns arrays stacked in the order of `segments`."""
+    cfg = trace.cfg
+    K = cfg.n_kernels
+    segments = list(segments)
+    n_threads = n_threads or host_threads()
+    out = {"n_clusters": np.empty(len(segments) * K, np.uint8),
+           "count": np.empty((len(segments) * K, oracle.KDE_MAXC), np.uint32),
+           "p50_ns": np.empty((len(segments) * K, oracle.KDE_MAXC), np.int64),
+           "p99_ns": np.empty((len(segments) * K, oracle.KDE_MAXC), np.int64),
+           "bw_q8": np.empty(len(segments) * K, np.int32)}
+
+    def work(i):
+        g = segments[i]
+        ev = trace.fill_host(g, g + 1, n_threads=1)
+        o = oracle.kde(ev, K, cfg.n_streams, **params)
+        for f in KDE_FIELDS:
+            out[f][i * K:(i + 1) * K] = o[f]
+
+    with ThreadPoolExecutor(n_threads) as ex:
+        list(ex.map(work, range(len(segments))))
+    return out
+
+
+def assert_kde_equal(gpu: dict, ref: dict, what="", rows=None):
+    """Exact comparison of KDE outputs; rows: optional cell indices of the
+    GPU arrays that correspond to the reference rows."""
+    for f in KDE_FIELDS:
+        r = np.asarray(ref[f])
+        g = to_np(gpu[f], r)
+        if r.ndim == 2:
+            g = g.reshape(-1, r.shape[1])
+        if rows is not None:
+            g = g[rows]
+        g = g.reshape(r.shape)
+        if not np.array_equal(g, r):
+            bad = np.nonzero((g != r).reshape(len(r), -1).any(axis=1))[0]
+            raise AssertionError(f"{what} {f}: {len(bad)} cells differ, first {bad[:5]}: gpu {g[bad[:3]]} "
+                                 f"oracle {r[bad[:3]]}")

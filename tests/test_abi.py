@@ -37,6 +37,7 @@ def test_version_and_defaults():
                                      alpha_pm=1500, tau_rank_pm=20)
     assert pa.l1_defaults() == dict(W=5, theta_pm=1500, beta_pm=1200, rho_pm=1300, cmax_pm=100, min_seg=2)
     assert pa.lib().argus_status_string(-1) == b"invalid argument"
+    assert pa.kde_defaults() == dict(sub_bits=6, frac_pm=50, min_count=3, gap=48)
 
 
 def test_workspace_sizes():
@@ -44,6 +45,9 @@ def test_workspace_sizes():
     assert pa.lib().argus_iter_windows_workspace(10, 10) == 0
     e = A.Events(0, 0, 0, 0, 0, 0, 1, 1, 1, 1)
     assert pa.lib().argus_summarize_workspace(ctypes.byref(e)) == 256
+    # 256 fixed + 8 B per event + 2 x 4 B per cell, each part 256-byte aligned
+    assert pa.kde_workspace_bytes(4_096_000_000, 10240, 1, 2048) == 256 + 4_096_000_000 * 8 + 2 * 10240 * 2048 * 4
+    assert pa.kde_workspace_bytes(10, 1, 1, 3) == 256 + 256 + 256 + 256
 
 
 @pytest.mark.parametrize("mutate", [
@@ -83,3 +87,30 @@ def test_cross_rank_and_l1_reject_bad_arguments():
     q.W = 0
     assert L.argus_iter_windows(0x1000, 4, 8, ctypes.byref(q), 0x1000, 0x1000, 0x1000, 0x1000, None, None, None, 0,
                                 None) == A.EINVAL
+
+
+@pytest.mark.parametrize("mutate", [
+    lambda e, s, p: setattr(e, "n_kernels", 16385),
+    lambda e, s, p: setattr(s, "min_ns", None),
+    lambda e, s, p: setattr(p, "sub_bits", 7),
+    lambda e, s, p: setattr(p, "sub_bits", 0),
+    lambda e, s, p: setattr(p, "frac_pm", 1001),
+    lambda e, s, p: setattr(p, "min_count", 0),
+    lambda e, s, p: setattr(p, "gap", -1),
+    "misaligned", "small",
+])
+def test_kde_rejects_bad_arguments(mutate):
+    e = A.Events(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 10, 2, 2, 4, 2)
+    s = A.Summary(*([0x1000] * 12 + [None, None]))
+    p = A.KdeParams()
+    pa.lib().argus_kde_default(ctypes.byref(p))
+    o = A.KdeOut(0x1000, 0x1000, 0x1000, 0x1000, None, None)
+    ws, n = 0x10000, 1 << 20
+    if mutate == "misaligned":
+        ws = 0x10080
+    elif mutate == "small":
+        n = 256
+    else:
+        mutate(e, s, p)
+    assert pa.lib().argus_kde(ctypes.byref(e), ctypes.byref(s), ctypes.byref(p), ctypes.byref(o), ws, n,
+                              None) == A.EINVAL
