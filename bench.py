@@ -113,6 +113,7 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes (counter calibration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kde-reps", type=int, default=5, help="timed argus_kde calls (0: skip the KDE leg)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -239,6 +240,38 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     result["iter_windows_10240x1000_ms"] = e0.elapsed_time(e1) / 5
+
+    if args.kde_reps > 0:
+        # KDE valley clustering of every (rank, step, kernel) group (section
+        # 5.2): bucketing scatter + per-cell density, valleys, filters, exact
+        # p50 / p99, over the summaries of the last step
+        kde_out = pa.alloc_kde(trace.n_events, R, S, K, dev)
+        for _ in range(2):
+            pa.kde(ev, s, R, S, K, NS, out=kde_out)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.kde_reps):
+            pa.kde(ev, s, R, S, K, NS, out=kde_out)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        kde_ms = e0.elapsed_time(e1) / args.kde_reps
+        assert int(kde_out["dev_status"].item()) == 0
+        ncl = kde_out["n_clusters"].cpu().numpy()
+        n_valid = int(s["n_valid"].cpu().numpy().view(np.uint32).astype(np.int64).sum())
+        # summary record per present cell: kernel id 4 B + cluster count 1 B,
+        # then (count 4, p50 8, p99 8) per cluster
+        wire = int(5 * np.count_nonzero(ncl) + 20 * ncl.astype(np.int64).sum())
+        result["kde"] = {
+            "ms": kde_ms, "events_per_s": trace.n_events / (kde_ms * 1e-3),
+            "scatter_algorithmic_bytes": 24 * trace.n_events + 8 * n_valid + 8 * G * K,
+            "cells": G * K, "present_cells": int(np.count_nonzero(ncl)),
+            "mean_clusters_per_present_cell": float(ncl[ncl > 0].mean()) if (ncl > 0).any() else 0.0,
+            "cells_with_several_clusters": int((ncl > 1).sum()),
+            "summary_bytes_per_rank_step": wire / G,
+            "raw_bytes_per_rank_step": 24 * trace.n_events / G,
+        }
+        del kde_out
+        torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
         sample = min(args.cpu_sample_ranks, R)

@@ -2,19 +2,26 @@
 // over log-duration, each cluster reported as (count, p50, p99) (section 5.2,
 // Eq. 1; the step-by-step definition is in include/argus.h).
 //
-// Three kernels:
-//   kde_scatter_kernel  one workgroup per segment (persistent queue): the
-//                       segment's valid durations are bucketed by kernel id
-//                       into the workspace (a counting sort whose counts come
-//                       from argus_summarize), so every cell's durations are
-//                       contiguous. HBM bound: 24 B read + 8 B written per event.
-//   kde_cell_kernel<fast>  one wavefront per cell, cells claimed 64 at a time:
-//                       grid histogram in LDS, exact bandwidth, integer-weight
-//                       density, valleys, filters, and exact order statistics
-//                       by radix selection inside the target grid bin. Cells
-//                       whose grid, kernel or valley list exceed its 19 KB of
-//                       LDS are appended to a deferred list.
-//   kde_cell_kernel<slow>  the deferred cells, 56 KB of LDS per wavefront.
+// Kernels, in launch order:
+//   kde_scatter_kernel   one 512-thread workgroup per segment (persistent
+//                        queue): the segment's valid durations are bucketed
+//                        by kernel id into the workspace, a counting sort
+//                        whose counts are argus_summarize's, so each cell's
+//                        durations become contiguous. 16-byte loads of four
+//                        events per thread, next group in flight. HBM bound:
+//                        24 B read and 8 B written per event.
+//   kde_cell_kernel<0>   one wavefront per cell, cells claimed 64 at a time
+//                        with their summaries, n^-0.2 and (for cells of up to
+//                        256 durations) the next cell's durations prefetched
+//                        while the current cell is processed: grid histogram
+//                        in LDS, exact bandwidth, integer-weight density
+//                        (sparse over occupied grid points when that is
+//                        cheaper), valleys, filters, and p50 / p99 by exact
+//                        radix selection inside the target grid bin. 6 KB of
+//                        LDS per wavefront; cells that need more go to a list.
+//   kde_cell_kernel<1>   the listed cells with 22 KB per wavefront;
+//   kde_cell_kernel<2>   what still does not fit, 56 KB per wavefront (any
+//                        grid of the 64-bit duration range fits).
 #include <atomic>
 #include <cmath>
 #include <mutex>
@@ -25,16 +32,33 @@
 namespace argus {
 namespace {
 
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef long long v2l __attribute__((ext_vector_type(2)));
+
 constexpr int kScatterThreads = 512;
 constexpr int kWave = 64;
-constexpr int kFastWords = 4096;  // grid histogram + kernel weights, fast path
-constexpr int kFastCand = 256;
-constexpr int kSlowWords = 8192;  // 4096-point grid + 4096 weights
-constexpr int kSlowCand = 2047;   // a 4096-point grid has at most 2047 valleys
 constexpr int kMaxC = ARGUS_KDE_MAXC;
 constexpr int kMaxT = 2 * kMaxC;  // selection targets: p50 and p99 per cluster
 constexpr int kPowTab = 65536;    // n^-0.2 for n below this, from the host libm
 constexpr int kRegVals = 4;       // cells of up to 256 durations stay in registers
+constexpr int kDigit = 6;         // radix-selection digit width (64 counters per target)
+
+// LDS per tier: grid words (histogram + weights), valley capacity, capacity
+// of the occupied-grid-point list used by the sparse density.
+template <int TIER>
+struct Tier;
+template <>
+struct Tier<0> {
+  static constexpr int kWords = 1024, kCand = 64, kNz = 128;
+};
+template <>
+struct Tier<1> {
+  static constexpr int kWords = 4096, kCand = 256, kNz = 512;
+};
+template <>
+struct Tier<2> {
+  static constexpr int kWords = 8192, kCand = 2047, kNz = 1;  // 4,032-point grids at most
+};
 
 // n^-0.2 for small n, filled once per device from the host's pow().
 __device__ double g_kde_pow[kPowTab];
@@ -46,7 +70,7 @@ struct KdeArgs {
   const int64_t* end_ns;
   const int64_t* seg_off;
   int64_t n_events;
-  int32_t n_seg, K, NS;
+  int32_t n_seg, K, NS, vec_ok;
   int32_t sub_bits, frac_pm, min_count, gap;
   const uint32_t* count;
   const int64_t* min_ns;
@@ -57,10 +81,13 @@ struct KdeArgs {
   int64_t* p99;
   int32_t* bw_q8;
   int32_t* dev_status;
-  uint32_t* counters;  // [0] scatter queue, [1] cell queue, [2] deferred count, [3] deferred queue
-  uint64_t* bucket;    // [n_events], segment g's durations at seg_off[g] + local position
+  // [0] scatter queue, [1] tier-0 queue, [2] list-1 length, [3] list-1 queue,
+  // [4] list-2 length, [5] list-2 queue
+  uint32_t* counters;
+  uint64_t* bucket;    // [n_events]: segment g's durations at seg_off[g] + local position
   uint32_t* cell_end;  // [cells]: local end offset of each cell's durations
-  uint32_t* deferred;  // [cells]
+  uint32_t* list1;     // [cells]: cells handed from tier 0 to tier 1
+  uint32_t* list2;     // [cells]: cells handed from tier 1 to tier 2
   uint32_t theta[64];  // ceil(2^(23 + t/64))
 };
 
@@ -107,6 +134,10 @@ __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
   return ((uint64_t)hi << 32) | lo;
 }
 
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  return __builtin_bit_cast(double, readlane64(__builtin_bit_cast(uint64_t, v), l));
+}
+
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
   for (int o = 32; o > 0; o >>= 1) {
     const uint64_t w = __shfl_xor(v, o, kWave);
@@ -138,12 +169,30 @@ __device__ __forceinline__ void flag(const KdeArgs& a, int bit) {
 
 // ----------------------------------------------------------------- scatter
 
+struct ScatterCtx {
+  uint32_t* cur;
+  uint64_t* out;
+  uint32_t len;
+  int32_t K, NS;
+};
+
+__device__ __forceinline__ void scatter_one(const ScatterCtx& s, int32_t kid, int32_t st, int64_t t0, int64_t t1) {
+  if (kid >= 0 && kid < s.K && st >= 0 && st < s.NS && t0 >= 0 && t1 >= t0) {
+    const uint32_t p = atomicAdd(&s.cur[kid], 1u);
+    if (p < s.len) s.out[p] = (uint64_t)t1 - (uint64_t)t0;
+  }
+}
+
 __global__ __launch_bounds__(kScatterThreads) void kde_scatter_kernel(KdeArgs a) {
   __shared__ uint32_t cur[ARGUS_MAX_KDE_KERNELS];
   __shared__ uint32_t wave_tot[kScatterThreads / kWave];
   __shared__ uint32_t claim;
   const int tid = threadIdx.x, K = a.K;
   const int per = (K + kScatterThreads - 1) / kScatterThreads;
+  const v4i* K4 = reinterpret_cast<const v4i*>(a.kernel_id);
+  const v4i* S4 = reinterpret_cast<const v4i*>(a.stream);
+  const v2l* T0 = reinterpret_cast<const v2l*>(a.start_ns);
+  const v2l* T1 = reinterpret_cast<const v2l*>(a.end_ns);
   while (true) {
     if (tid == 0) claim = atomicAdd(&a.counters[0], 1u);
     __syncthreads();
@@ -167,15 +216,47 @@ __global__ __launch_bounds__(kScatterThreads) void kde_scatter_kernel(KdeArgs a)
     const int64_t lo = a.seg_off[g], hi = a.seg_off[g + 1];
     const bool bad = !(lo >= 0 && lo <= hi && hi <= a.n_events && hi - lo <= (int64_t)UINT32_MAX);
     if (!bad) {
-      const uint32_t len = (uint32_t)(hi - lo);
-      uint64_t* out = a.bucket + lo;
-      for (int64_t i = lo + tid; i < hi; i += kScatterThreads) {
-        const int32_t kid = a.kernel_id[i], st = a.stream[i];
-        const int64_t t0 = a.start_ns[i], t1 = a.end_ns[i];
-        if (kid >= 0 && kid < K && st >= 0 && st < a.NS && t0 >= 0 && t1 >= t0) {
-          const uint32_t p = atomicAdd(&cur[kid], 1u);
-          if (p < len) out[p] = (uint64_t)t1 - (uint64_t)t0;
+      const ScatterCtx s{cur, a.bucket + lo, (uint32_t)(hi - lo), K, a.NS};
+      int64_t a4 = hi, b4 = hi;  // aligned body [a4, b4) in groups of four events
+      if (a.vec_ok) {
+        const int64_t up = (lo + 3) & ~(int64_t)3, dn = hi & ~(int64_t)3;
+        a4 = up < hi ? up : hi;
+        b4 = dn > a4 ? dn : a4;
+      }
+      // head [lo, a4) (the whole segment without aligned arrays) and tail [b4, hi)
+      for (int64_t i = lo + tid; i < a4; i += kScatterThreads)
+        scatter_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
+      for (int64_t i = b4 + tid; i < hi; i += kScatterThreads)
+        scatter_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
+      const int64_t qb = b4 >> 2;
+      int64_t q = (a4 >> 2) + tid;
+      v4i nk4 = 0, ns4 = 0;
+      v2l na0 = 0, na1 = 0, nb0 = 0, nb1 = 0;
+      if (q < qb) {
+        nk4 = __builtin_nontemporal_load(K4 + q);
+        ns4 = __builtin_nontemporal_load(S4 + q);
+        na0 = __builtin_nontemporal_load(T0 + 2 * q);
+        na1 = __builtin_nontemporal_load(T0 + 2 * q + 1);
+        nb0 = __builtin_nontemporal_load(T1 + 2 * q);
+        nb1 = __builtin_nontemporal_load(T1 + 2 * q + 1);
+      }
+      while (q < qb) {
+        const v4i k4 = nk4, s4 = ns4;
+        const v2l x0 = na0, x1 = na1, y0 = nb0, y1 = nb1;
+        const int64_t qn = q + kScatterThreads;
+        if (qn < qb) {
+          nk4 = __builtin_nontemporal_load(K4 + qn);
+          ns4 = __builtin_nontemporal_load(S4 + qn);
+          na0 = __builtin_nontemporal_load(T0 + 2 * qn);
+          na1 = __builtin_nontemporal_load(T0 + 2 * qn + 1);
+          nb0 = __builtin_nontemporal_load(T1 + 2 * qn);
+          nb1 = __builtin_nontemporal_load(T1 + 2 * qn + 1);
         }
+        scatter_one(s, k4.x, s4.x, x0.x, y0.x);
+        scatter_one(s, k4.y, s4.y, x0.y, y0.y);
+        scatter_one(s, k4.z, s4.z, x1.x, y1.x);
+        scatter_one(s, k4.w, s4.w, x1.y, y1.y);
+        q = qn;
       }
     }
     __syncthreads();
@@ -187,20 +268,33 @@ __global__ __launch_bounds__(kScatterThreads) void kde_scatter_kernel(KdeArgs a)
 
 // -------------------------------------------------------------------- cells
 
-template <int WORDS, int CAND>
+template <int TIER>
 struct CellLds {
-  uint64_t cval[CAND];  // valley depth f
+  static constexpr int W = Tier<TIER>::kWords, CA = Tier<TIER>::kCand, NZ = Tier<TIER>::kNz;
+  uint64_t cval[CA];    // valley depth f
   uint64_t tlb[kMaxT];  // target bin: smallest duration
   uint64_t tub[kMaxT];  // target bin: one past the largest duration
   uint64_t tpre[kMaxT]; // digits selected so far
   uint64_t trank[kMaxT];
-  uint32_t buf[WORDS];  // grid histogram (then its prefix) | weights; later selection histograms
-  int32_t cpos[CAND];   // valley grid index
+  uint32_t tpop[kMaxT];  // durations in the target bin
+  uint32_t tdone[kMaxT]; // target already resolved
+  uint32_t buf[W];      // grid histogram (then its prefix) | weights; later selection counters
+  uint32_t nzc[NZ];     // occupied grid points: count
+  int32_t cpos[CA];     // valley grid index
+  uint16_t nzb[NZ];     // occupied grid points: index (ascending)
   uint32_t th[64];
 };
 
-template <int WORDS, int CAND>
-__device__ void remove_valley(CellLds<WORDS, CAND>& L, int idx, int m) {
+// One cell's inputs, checked against the bucketed durations.
+struct CellMeta {
+  uint32_t n;
+  int64_t mn, mx;
+  int64_t off;  // first duration in the bucket, or -1 when the summary does not match
+  double pw;    // n^-0.2 from the table (0 when n is outside it)
+};
+
+template <int TIER>
+__device__ void remove_valley(CellLds<TIER>& L, int idx, int m) {
   const int l = lane_id();
   for (int qb = idx; qb < m - 1; qb += kWave) {
     const int q = qb + l;
@@ -232,28 +326,32 @@ __device__ void write_empty(const KdeArgs& a, int64_t c) {
   }
 }
 
-// One cell on one wavefront. vals: the cell's n durations (global memory);
-// when n <= 64 * kRegVals they are also held in registers (rv). Returns false
-// when the cell does not fit this kernel's LDS (only if may_defer).
-template <int WORDS, int CAND>
-__device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t c, uint32_t n, uint64_t mn,
-                             uint64_t mx, const uint64_t* vals, bool may_defer) {
+// Load a small cell's durations into registers (lane l holds l, l + 64, ...).
+__device__ __forceinline__ void load_small(const KdeArgs& a, const CellMeta& m, uint64_t (&rv)[kRegVals]) {
   const int l = lane_id();
+  const bool small = m.off >= 0 && m.n <= (uint32_t)(kWave * kRegVals);
+#pragma unroll
+  for (int r = 0; r < kRegVals; ++r) {
+    const uint32_t i = (uint32_t)(l + r * kWave);
+    rv[r] = small && i < m.n ? __builtin_nontemporal_load(a.bucket + m.off + i) : 0ull;
+  }
+}
+
+// One cell on one wavefront. Returns false when the cell needs a larger
+// tier (only for TIER < 2; nothing has been written for it then).
+template <int TIER>
+__device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, const CellMeta& cm,
+                             const uint64_t (&rv)[kRegVals]) {
+  constexpr int WORDS = CellLds<TIER>::W, CAND = CellLds<TIER>::CA, NZCAP = CellLds<TIER>::NZ;
+  const int l = lane_id();
+  const uint32_t n = cm.n;
+  const uint64_t* vals = a.bucket + cm.off;
   const int sh = 6 - a.sub_bits;
-  const int lo = grid64(mn, L.th) >> sh;
-  const int G = (grid64(mx, L.th) >> sh) - lo + 1;
+  const int lo = grid64((uint64_t)cm.mn, L.th) >> sh;
+  const int G = (grid64((uint64_t)cm.mx, L.th) >> sh) - lo + 1;
+  if (TIER < 2 && G > WORDS) return false;
   uint32_t* cgrid = L.buf;
   const bool in_regs = n <= (uint32_t)(kWave * kRegVals);
-  uint64_t rv[kRegVals];
-#pragma unroll
-  for (int r = 0; r < kRegVals; ++r) rv[r] = 0;
-  if (in_regs) {
-#pragma unroll
-    for (int r = 0; r < kRegVals; ++r) {
-      const uint32_t i = (uint32_t)(l + r * kWave);
-      if (i < n) rv[r] = __builtin_nontemporal_load(vals + i);
-    }
-  }
 
   // 1. grid histogram
   for (int j = l; j < G; j += kWave) cgrid[j] = 0;
@@ -283,20 +381,35 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
     return true;
   }
 
-  // 2. bandwidth
+  // 2. bandwidth; occupied grid points listed for the sparse density
   uint64_t s1 = 0, s2 = 0;
-  for (int j = l; j < G; j += kWave) {
-    const uint64_t k = cgrid[j];
-    s1 += k * (uint64_t)j;
-    s2 += k * (uint64_t)j * (uint64_t)j;
+  int nnz = 0;
+  for (int jb = 0; jb < G; jb += kWave) {
+    const int j = jb + l;
+    const uint32_t k = j < G ? cgrid[j] : 0u;
+    s1 += (uint64_t)k * (uint64_t)j;
+    s2 += (uint64_t)k * (uint64_t)j * (uint64_t)j;
+    const uint64_t occ = __ballot(k != 0);
+    if (k != 0) {
+      const int idx = nnz + __popcll(occ & ((1ull << l) - 1ull));
+      if (idx < NZCAP) {
+        L.nzb[idx] = (uint16_t)j;
+        L.nzc[idx] = k;
+      }
+    }
+    nnz += __popcll(occ);
   }
   s1 = wave_sum_u64(s1);
   s2 = wave_sum_u64(s2);
   int64_t H = 0;
   if (n >= 2) {
-    const unsigned __int128 V = (unsigned __int128)n * s2 - (unsigned __int128)s1 * s1;
-    const double var = u128_to_f64(V) / ((double)n * (double)(n - 1));
-    const double pw = n < (uint32_t)kPowTab ? g_kde_pow[n] : pow((double)n, -0.2);
+    // n * s2 - s1^2 exactly: in 64 bits when it fits (the usual case), else 128
+    uint64_t ns2;
+    double vnum;
+    if (!__builtin_mul_overflow((uint64_t)n, s2, &ns2) && s1 < (1ull << 32)) vnum = (double)(ns2 - s1 * s1);
+    else vnum = u128_to_f64((unsigned __int128)n * s2 - (unsigned __int128)s1 * s1);
+    const double var = vnum / ((double)n * (double)(n - 1));
+    const double pw = n < (uint32_t)kPowTab ? cm.pw : pow((double)n, -0.2);
     const double h = 1.06 * sqrt(var) * pw;
     H = (int64_t)floor(h * 256.0 + 0.5);
   }
@@ -313,24 +426,51 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
       if (t < G) wt = (uint32_t)floor(65536.0 * exp(-(double)(32768ll * t * t) / H2) + 0.5);
       const uint64_t nz = __ballot(wt != 0);
       const int cnt = __popcll(nz);  // weights are non-increasing in t
-      if (G + tb + cnt > WORDS) {
-        if (may_defer) return false;
-      }
+      if (TIER < 2 && G + tb + cnt > WORDS) return false;
       if (wt != 0 && G + t < WORDS) w[t] = wt;
       T = tb + cnt - 1;
       if (cnt < kWave) break;
     }
     __syncthreads();
+    const bool sparse = nnz <= NZCAP && nnz < T;
     int carry_start = -1, carry_drop = 0;
     uint64_t prev_last = 0;
-    bool overflow = false;
     for (int jb = 0; jb < G; jb += kWave) {
       const int j = jb + l;
       const bool valid = j < G;
       uint64_t fj = 0;
-      if (valid) {
-        const int b0 = j - T > 0 ? j - T : 0, b1 = j + T < G - 1 ? j + T : G - 1;
-        for (int b = b0; b <= b1; ++b) fj += (uint64_t)cgrid[b] * w[j > b ? j - b : b - j];
+      if (sparse) {
+        // occupied points within T of this chunk: [k0, k1)
+        const int lo_b = jb - T, hi_b = jb + kWave - 1 + T;
+        int x = 0, y = nnz;
+        while (x < y) {
+          const int mid = (x + y) >> 1;
+          if ((int)L.nzb[mid] < lo_b) x = mid + 1;
+          else y = mid;
+        }
+        const int k0 = x;
+        y = nnz;
+        while (x < y) {
+          const int mid = (x + y) >> 1;
+          if ((int)L.nzb[mid] <= hi_b) x = mid + 1;
+          else y = mid;
+        }
+        const int k1 = x;
+        for (int k = k0; k < k1; ++k) {
+          const int b = L.nzb[k];
+          const int t = j > b ? j - b : b - j;
+          if (valid && t <= T) fj += (uint64_t)L.nzc[k] * w[t];
+        }
+      } else {
+        // f(j) = w(0) c(j) + sum_t w(t) (c(j - t) + c(j + t)), t uniform across lanes
+        const int tmax = T < G - 1 ? T : G - 1;
+        if (valid) fj = (uint64_t)cgrid[j] * w[0];
+        for (int t = 1; t <= tmax; ++t) {
+          const uint32_t wt = w[t];
+          const uint64_t cl = valid && j - t >= 0 ? cgrid[j - t] : 0u;
+          const uint64_t cr = valid && j + t < G ? cgrid[j + t] : 0u;
+          fj += (cl + cr) * wt;
+        }
       }
       uint64_t fl = __shfl_up(fj, 1, kWave);
       if (l == 0) fl = prev_last;
@@ -355,7 +495,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
         }
       }
       m += __popcll(Vb);
-      if (m > CAND) overflow = true;
+      if (TIER < 2 && m > CAND) return false;
       if (S) {
         const int ls = 63 - __builtin_clzll(S);
         carry_start = jb + ls;
@@ -364,11 +504,8 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
       const int last = G - 1 - jb < kWave - 1 ? G - 1 - jb : kWave - 1;
       prev_last = readlane64(fj, last);
     }
+    if (m > CAND) m = CAND;  // cannot happen in tier 2: a grid of G points has < G / 2 valleys
     __syncthreads();
-    if (overflow) {
-      if (may_defer) return false;
-      m = CAND;  // unreachable for the large-LDS instantiation
-    }
   }
 
   // grid histogram -> inclusive prefix counts (in place)
@@ -439,10 +576,9 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
     int best_q = -1;
     for (int qb = 0; qb < m; qb += kWave) {
       const int q = qb + l;
-      uint64_t v = 0;
-      bool on = q < m;
-      if (on) v = L.cval[q];
-      const uint64_t mv = wave_max_u64(on ? v : 0ull);
+      const bool on = q < m;
+      const uint64_t v = on ? L.cval[q] : 0ull;
+      const uint64_t mv = wave_max_u64(v);
       const uint64_t bm = __ballot(on && v == mv);
       if (bm && (best_q < 0 || mv >= best_v)) {
         best_v = mv;
@@ -453,7 +589,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
     --m;
   }
 
-  // 8. counts and selection targets (global ranks in the cell's sorted order)
+  // 8. counts and selection targets (ranks in the cell's sorted order)
   const int ncl = m + 1;
   uint32_t ccount[kMaxC];
 #pragma unroll
@@ -484,6 +620,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
           L.tub[NT] = grid64_lb((lo + lo_j + 1) << sh, L.th);
           L.tpre[NT] = 0;
           L.trank[NT] = r - below;
+          L.tpop[NT] = P[lo_j] - below;
         }
         ++NT;
       }
@@ -492,26 +629,65 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
   }
   __syncthreads();
 
-  // 9. exact selection inside each target bin, 8 bits per pass
+  // 9a. cells held in registers: a target bin with at most 64 durations is
+  // gathered into LDS and its element of the wanted rank found by counting
+  for (int t = 0; t < NT; ++t) {
+    const bool direct = in_regs && L.tpop[t] <= (uint32_t)kWave;
+    if (direct) {
+      uint64_t* list = reinterpret_cast<uint64_t*>(L.buf);
+      const uint64_t lb = L.tlb[t], ub = L.tub[t];
+      int base = 0;
+#pragma unroll
+      for (int r = 0; r < kRegVals; ++r) {
+        const bool in = (uint32_t)(l + r * kWave) < n && rv[r] >= lb && rv[r] < ub;
+        const uint64_t bm = __ballot(in);
+        if (in) list[base + __popcll(bm & ((1ull << l) - 1ull))] = rv[r];
+        base += __popcll(bm);
+      }
+      __syncthreads();
+      const int k = (int)L.tpop[t];
+      const uint64_t e = l < k ? list[l] : 0ull;
+      uint32_t rank = 0;
+      for (int j = 0; j < k; ++j) {
+        const uint64_t ej = list[j];
+        rank += (ej < e || (ej == e && j < l)) ? 1u : 0u;
+      }
+      const uint64_t hit = __ballot(l < k && (uint64_t)rank == L.trank[t]);
+      const uint64_t val = readlane64(e, hit ? __builtin_ctzll(hit) : 0);
+      __syncthreads();
+      if (l == 0) {
+        L.tpre[t] = val - lb;
+        L.tdone[t] = 1;
+      }
+    } else if (l == 0) {
+      L.tdone[t] = 0;
+    }
+    __syncthreads();
+  }
+
+  // 9b. exact selection inside the remaining target bins, kDigit bits per pass
   int nbits = 0;
   for (int t = 0; t < NT; ++t) {
+    if (L.tdone[t]) continue;
     const uint64_t width = L.tub[t] - L.tlb[t];
     const int b = width > 1 ? 64 - __builtin_clzll(width - 1) : 0;
     nbits = b > nbits ? b : nbits;
   }
-  const int npass = (nbits + 7) / 8;
-  uint32_t* hist = L.buf;  // NT x 256 counters; the prefix counts are no longer needed
+  const int npass = (nbits + kDigit - 1) / kDigit;
+  constexpr int R = 1 << kDigit;
+  uint32_t* hist = L.buf;  // NT x R counters; the prefix counts are no longer needed
   for (int p = 0; p < npass; ++p) {
-    const int shift = 8 * (npass - 1 - p);
-    for (int i = l; i < NT * 256; i += kWave) hist[i] = 0;
+    const int shift = kDigit * (npass - 1 - p);
+    for (int i = l; i < NT * R; i += kWave) hist[i] = 0;
     __syncthreads();
     auto consider = [&](uint64_t v) {
       for (int t = 0; t < NT; ++t) {
+        if (L.tdone[t]) continue;
         const uint64_t lb = L.tlb[t];
         if (v >= lb && v < L.tub[t]) {
           const uint64_t u = v - lb;
-          const uint64_t hi_part = shift + 8 >= 64 ? 0 : u >> (shift + 8);
-          if (hi_part == L.tpre[t]) atomicAdd(&hist[t * 256 + (int)((u >> shift) & 255u)], 1u);
+          const uint64_t hi_part = shift + kDigit >= 64 ? 0 : u >> (shift + kDigit);
+          if (hi_part == L.tpre[t]) atomicAdd(&hist[t * R + (int)((u >> shift) & (R - 1))], 1u);
         }
       }
     };
@@ -524,32 +700,17 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
     }
     __syncthreads();
     for (int t = 0; t < NT; ++t) {
-      // digit holding the target rank: 4 counters per lane, then a wave scan
-      const uint32_t* h = hist + t * 256;
-      const uint32_t c0 = h[4 * l], c1 = h[4 * l + 1], c2 = h[4 * l + 2], c3 = h[4 * l + 3];
-      const uint32_t tot = c0 + c1 + c2 + c3;
-      const uint32_t incl = wave_incl_scan(tot);
+      if (L.tdone[t]) continue;
+      // the digit holding the target rank: one counter per lane, a wave scan
+      const uint32_t v = hist[t * R + l];
+      const uint32_t incl = wave_incl_scan(v);
       const uint64_t r = L.trank[t];
-      const bool mine = (uint64_t)(incl - tot) <= r && r < (uint64_t)incl;
-      const uint64_t bm = __ballot(mine);
+      const uint64_t bm = __ballot((uint64_t)(incl - v) <= r && r < (uint64_t)incl);
       const int owner = bm ? __builtin_ctzll(bm) : 0;
-      if (l == owner) {
-        uint64_t rr = r - (incl - tot);
-        int d = 4 * l;
-        if (rr >= c0) {
-          rr -= c0;
-          ++d;
-          if (rr >= c1) {
-            rr -= c1;
-            ++d;
-            if (rr >= c2) {
-              rr -= c2;
-              ++d;
-            }
-          }
-        }
-        L.trank[t] = rr;
-        L.tpre[t] = (L.tpre[t] << 8) | (uint64_t)d;
+      const uint32_t excl = __builtin_amdgcn_readlane(incl - v, owner);
+      if (l == 0) {
+        L.trank[t] = r - excl;
+        L.tpre[t] = (L.tpre[t] << kDigit) | (uint64_t)owner;
       }
       __syncthreads();
     }
@@ -574,74 +735,100 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<WORDS, CAND>& L, int64_t 
   return true;
 }
 
-// Checks of one cell's summary against the bucketed durations; on success
-// returns the cell's durations in *vals.
-__device__ bool cell_source(const KdeArgs& a, int64_t c, uint32_t n, int64_t mn, int64_t mx, uint32_t end,
-                            uint32_t prev_end, const uint64_t** vals) {
+// Summary of cell c checked against the bucketed durations (cell_end chain).
+__device__ CellMeta load_meta(const KdeArgs& a, int64_t c) {
+  CellMeta m{};
+  m.off = -1;
+  m.n = a.count[c];
+  if (m.n == 0) return m;
+  m.mn = a.min_ns[c];
+  m.mx = a.max_ns[c];
+  const uint32_t end = a.cell_end[c];
+  const uint32_t prev = c % a.K ? a.cell_end[c - 1] : 0u;
   const int64_t g = c / a.K;
   const int64_t lo = a.seg_off[g], hi = a.seg_off[g + 1];
   const bool seg_ok = lo >= 0 && lo <= hi && hi <= a.n_events && hi - lo <= (int64_t)UINT32_MAX;
-  const bool ok = seg_ok && end >= n && end - n == prev_end && (int64_t)end <= hi - lo && mn >= 0 && mn <= mx;
-  if (ok) *vals = a.bucket + lo + (end - n);
-  return ok;
+  if (seg_ok && end >= m.n && end - m.n == prev && (int64_t)end <= hi - lo && m.mn >= 0 && m.mn <= m.mx)
+    m.off = lo + (end - m.n);
+  m.pw = m.n < (uint32_t)kPowTab ? g_kde_pow[m.n] : 0.0;
+  return m;
 }
 
-template <int WORDS, int CAND, bool SLOW>
-__global__ __launch_bounds__(kWave) void kde_cell_kernel(KdeArgs a) {
-  __shared__ CellLds<WORDS, CAND> L;
+__device__ CellMeta meta_from_lane(const CellMeta& m, int i) {
+  CellMeta r;
+  r.n = __builtin_amdgcn_readlane(m.n, i);
+  r.mn = (int64_t)readlane64((uint64_t)m.mn, i);
+  r.mx = (int64_t)readlane64((uint64_t)m.mx, i);
+  r.off = (int64_t)readlane64((uint64_t)m.off, i);
+  r.pw = readlane_f64(m.pw, i);
+  return r;
+}
+
+template <int TIER>
+__device__ void finish_or_hand_on(const KdeArgs& a, CellLds<TIER>& L, int64_t c, const CellMeta& m,
+                                  const uint64_t (&rv)[kRegVals]) {
+  const int l = lane_id();
+  if (m.n == 0) {
+    write_empty(a, c);
+    return;
+  }
+  if (m.off < 0) {
+    if (l == 0) flag(a, ARGUS_DEV_KDE_SUMMARY);
+    write_empty(a, c);
+    return;
+  }
+  if (!kde_one_cell<TIER>(a, L, c, m, rv)) {
+    if (TIER == 0 && l == 0) a.list1[atomicAdd(&a.counters[2], 1u)] = (uint32_t)c;
+    if (TIER == 1 && l == 0) a.list2[atomicAdd(&a.counters[4], 1u)] = (uint32_t)c;
+    __syncthreads();
+  }
+}
+
+template <int TIER>
+__global__ __launch_bounds__(kWave, TIER == 0 ? 4 : 1) void kde_cell_kernel(KdeArgs a) {
+  __shared__ CellLds<TIER> L;
   const int l = lane_id();
   L.th[l] = a.theta[l];
   __syncthreads();
   const int64_t C = (int64_t)a.n_seg * a.K;
   while (true) {
     uint32_t claim = 0;
-    if (l == 0) claim = atomicAdd(&a.counters[SLOW ? 3 : 1], 1u);
+    if (l == 0) claim = atomicAdd(&a.counters[TIER == 0 ? 1 : (TIER == 1 ? 3 : 5)], 1u);
     claim = __builtin_amdgcn_readfirstlane(claim);
-    int64_t c0;
-    int ncells;
-    if (SLOW) {
-      const uint32_t nd = __builtin_amdgcn_readfirstlane(__hip_atomic_load(&a.counters[2], __ATOMIC_RELAXED,
-                                                                            __HIP_MEMORY_SCOPE_AGENT));
-      if (claim >= nd) break;
-      c0 = a.deferred[claim];
-      ncells = 1;
-    } else {
-      c0 = (int64_t)claim * kWave;
+    if constexpr (TIER == 0) {
+      const int64_t c0 = (int64_t)claim * kWave;
       if (c0 >= C) break;
-      ncells = C - c0 < kWave ? (int)(C - c0) : kWave;
-    }
-    // per-lane prefetch of the cells' summaries
-    uint32_t n = 0, end = 0, prev = 0;
-    int64_t mn = 0, mx = 0;
-    const int64_t cl = SLOW ? c0 : c0 + l;
-    if ((SLOW && l == 0) || (!SLOW && l < ncells)) {
-      n = a.count[cl];
-      if (n) {
-        mn = a.min_ns[cl];
-        mx = a.max_ns[cl];
-        end = a.cell_end[cl];
-        prev = cl % a.K ? a.cell_end[cl - 1] : 0u;
+      const int ncells = C - c0 < kWave ? (int)(C - c0) : kWave;
+      // every lane fetches one cell's summary; the wave then walks the cells,
+      // loading the next small cell's durations while it works on this one
+      CellMeta mine{};
+      mine.off = -1;
+      if (l < ncells) mine = load_meta(a, c0 + l);
+      uint64_t cur[kRegVals], nxt[kRegVals];
+      CellMeta m = meta_from_lane(mine, 0);
+      load_small(a, m, cur);
+      for (int i = 0; i < ncells; ++i) {
+        CellMeta mn{};
+        mn.off = -1;
+        if (i + 1 < ncells) mn = meta_from_lane(mine, i + 1);
+        load_small(a, mn, nxt);
+        finish_or_hand_on<TIER>(a, L, c0 + i, m, cur);
+#pragma unroll
+        for (int r = 0; r < kRegVals; ++r) cur[r] = nxt[r];
+        m = mn;
       }
-    }
-    for (int i = 0; i < ncells; ++i) {
-      const int64_t c = c0 + i;
-      const uint32_t cn = __builtin_amdgcn_readlane(n, i);
-      if (cn == 0) {
-        write_empty(a, c);
-        continue;
-      }
-      const uint32_t ce = __builtin_amdgcn_readlane(end, i), cp = __builtin_amdgcn_readlane(prev, i);
-      const int64_t cmn = (int64_t)readlane64((uint64_t)mn, i), cmx = (int64_t)readlane64((uint64_t)mx, i);
-      const uint64_t* vals = nullptr;
-      if (!cell_source(a, c, cn, cmn, cmx, ce, cp, &vals)) {
-        if (l == 0) flag(a, ARGUS_DEV_KDE_SUMMARY);
-        write_empty(a, c);
-        continue;
-      }
-      if (!kde_one_cell<WORDS, CAND>(a, L, c, cn, (uint64_t)cmn, (uint64_t)cmx, vals, !SLOW)) {
-        if (l == 0) a.deferred[atomicAdd(&a.counters[2], 1u)] = (uint32_t)c;
-        __syncthreads();
-      }
+    } else {
+      const uint32_t len = __builtin_amdgcn_readfirstlane(
+          __hip_atomic_load(&a.counters[TIER == 1 ? 2 : 4], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      if (claim >= len) break;
+      const int64_t c = (TIER == 1 ? a.list1 : a.list2)[claim];
+      CellMeta mine{};
+      mine.off = -1;
+      if (l == 0) mine = load_meta(a, c);
+      const CellMeta m = meta_from_lane(mine, 0);
+      uint64_t cur[kRegVals];
+      load_small(a, m, cur);
+      finish_or_hand_on<TIER>(a, L, c, m, cur);
     }
   }
 }
@@ -715,21 +902,23 @@ int resident(Kern kern, int threads) {
 }
 
 __global__ void kde_clear_kernel(uint32_t* counters, int32_t* dev_status) {
-  if (threadIdx.x < 4) counters[threadIdx.x] = 0;
+  if (threadIdx.x < 8) counters[threadIdx.x] = 0;
   if (threadIdx.x == 0 && dev_status) *dev_status = 0;
 }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
 size_t kde_workspace_bytes(int64_t n_events, int64_t cells) {
-  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  return 256 + al((size_t)n_events * 8) + al((size_t)cells * 4) + al((size_t)cells * 4);
+  return 256 + al256((size_t)n_events * 8) + 3 * al256((size_t)cells * 4);
 }
 
 hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   hipError_t e = ensure_pow_table();
   if (e != hipSuccess) return e;
-  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const int64_t cells = (int64_t)l.n_seg * l.n_kernels;
   char* ws = static_cast<char*>(l.workspace);
   KdeArgs a{};
@@ -742,6 +931,7 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   a.n_seg = l.n_seg;
   a.K = l.n_kernels;
   a.NS = l.n_streams;
+  a.vec_ok = aligned16(l.kernel_id) && aligned16(l.stream) && aligned16(l.start_ns) && aligned16(l.end_ns);
   a.sub_bits = l.p.sub_bits;
   a.frac_pm = l.p.frac_pm;
   a.min_count = l.p.min_count;
@@ -756,9 +946,14 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   a.bw_q8 = l.o.bw_q8;
   a.dev_status = l.o.dev_status;
   a.counters = reinterpret_cast<uint32_t*>(ws);
-  a.bucket = reinterpret_cast<uint64_t*>(ws + 256);
-  a.cell_end = reinterpret_cast<uint32_t*>(ws + 256 + al((size_t)l.n_events * 8));
-  a.deferred = reinterpret_cast<uint32_t*>(ws + 256 + al((size_t)l.n_events * 8) + al((size_t)cells * 4));
+  size_t off = 256;
+  a.bucket = reinterpret_cast<uint64_t*>(ws + off);
+  off += al256((size_t)l.n_events * 8);
+  a.cell_end = reinterpret_cast<uint32_t*>(ws + off);
+  off += al256((size_t)cells * 4);
+  a.list1 = reinterpret_cast<uint32_t*>(ws + off);
+  off += al256((size_t)cells * 4);
+  a.list2 = reinterpret_cast<uint32_t*>(ws + off);
   const uint32_t* th = thresholds();
   for (int t = 0; t < 64; ++t) a.theta[t] = th[t];
 
@@ -767,23 +962,26 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   if (cells == 0) return hipSuccess;
 
   // resident workgroups per kernel, cached per device
-  static std::atomic<int> grids[64][3];
+  static std::atomic<int> grids[64][4];
   int dev = 0;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  int gs = grids[dev][0].load(), gf = grids[dev][1].load(), gl = grids[dev][2].load();
-  if (gs == 0) grids[dev][0].store(gs = resident(kde_scatter_kernel, kScatterThreads));
-  if (gf == 0) grids[dev][1].store(gf = resident(kde_cell_kernel<kFastWords, kFastCand, false>, kWave));
-  if (gl == 0) grids[dev][2].store(gl = resident(kde_cell_kernel<kSlowWords, kSlowCand, true>, kWave));
-  if (gs <= 0 || gf <= 0 || gl <= 0) return hipErrorInvalidDevice;
-  const int g1 = l.n_seg < gs ? l.n_seg : gs;
-  hipLaunchKernelGGL(kde_scatter_kernel, dim3(g1), dim3(kScatterThreads), 0, st, a);
+  int g[4];
+  for (int i = 0; i < 4; ++i) g[i] = grids[dev][i].load();
+  if (g[0] == 0) grids[dev][0].store(g[0] = resident(kde_scatter_kernel, kScatterThreads));
+  if (g[1] == 0) grids[dev][1].store(g[1] = resident(kde_cell_kernel<0>, kWave));
+  if (g[2] == 0) grids[dev][2].store(g[2] = resident(kde_cell_kernel<1>, kWave));
+  if (g[3] == 0) grids[dev][3].store(g[3] = resident(kde_cell_kernel<2>, kWave));
+  for (int i = 0; i < 4; ++i)
+    if (g[i] <= 0) return hipErrorInvalidDevice;
+  hipLaunchKernelGGL(kde_scatter_kernel, dim3(l.n_seg < g[0] ? l.n_seg : g[0]), dim3(kScatterThreads), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int64_t chunks = (cells + kWave - 1) / kWave;
-  const int g2 = chunks < gf ? (int)chunks : gf;
-  hipLaunchKernelGGL((kde_cell_kernel<kFastWords, kFastCand, false>), dim3(g2), dim3(kWave), 0, st, a);
+  hipLaunchKernelGGL(kde_cell_kernel<0>, dim3(chunks < g[1] ? (int)chunks : g[1]), dim3(kWave), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL((kde_cell_kernel<kSlowWords, kSlowCand, true>), dim3(gl), dim3(kWave), 0, st, a);
+  hipLaunchKernelGGL(kde_cell_kernel<1>, dim3(g[2]), dim3(kWave), 0, st, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(kde_cell_kernel<2>, dim3(g[3]), dim3(kWave), 0, st, a);
   return hipGetLastError();
 }
 

@@ -13,7 +13,8 @@
 //   next group is in flight while the current one is processed.
 // * Per-kernel state is privatised in LDS: 64-bit sum, min and max, and a
 //   WIN-bin window of the octave histogram anchored at the first duration
-//   seen for that kernel (lognormal kernels span two or three octaves). Bins
+//   seen for that kernel (a lognormal mode spans two or three octaves; ten
+//   bins also hold kernels whose positions run at 1x, 3x and 9x). Bins
 //   outside the window go to a small pool of full 32-bin records that a
 //   kernel claims on first need.
 // * Kernel ids map to LDS slots directly when the id space fits (dense), or
@@ -581,9 +582,9 @@ hipError_t launch_summarize(const SummarizeLaunch& l, hipStream_t st) {
          l.n_seg, l.queue, l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist, l.n_valid, l.n_invalid, l.t_first, l.t_last,
          l.step_ns, l.busy_ns, l.stream_busy_ns, l.wire_bytes, l.dev_status};
   if (l.n_seg == 0) return hipSuccess;
-  if (l.n_kernels <= 64) return launch_t<64, 8, false>(a, l.n_seg, st);
-  if (l.n_kernels <= 512) return launch_t<512, 8, false>(a, l.n_seg, st);
-  if (l.n_kernels <= 2048) return launch_t<2048, 8, false>(a, l.n_seg, st);
+  if (l.n_kernels <= 64) return launch_t<64, 10, false>(a, l.n_seg, st);
+  if (l.n_kernels <= 512) return launch_t<512, 10, false>(a, l.n_seg, st);
+  if (l.n_kernels <= 2048) return launch_t<2048, 10, false>(a, l.n_seg, st);
   const int64_t cells = (int64_t)l.n_seg * l.n_kernels;
   hipLaunchKernelGGL(identity_fill_kernel, dim3(4096), dim3(256), 0, st, l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist,
                      cells);
