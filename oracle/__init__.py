@@ -20,6 +20,7 @@ XR_DEFAULTS = dict(min_ranks=3, c_min_pair=8, min_kernels=8, k_mad_pm=5189, rati
                    tau_rank_pm=20)
 L1_DEFAULTS = dict(W=5, theta_pm=1500, beta_pm=1200, rho_pm=1300, cmax_pm=100, min_seg=2)
 KDE_DEFAULTS = dict(sub_bits=6, frac_pm=50, min_count=3, gap=48)
+W1_DEFAULTS = dict(grid=64, min_ranks=3, alpha_pm=1500)
 KDE_MAXC = 4
 
 _lib = None
@@ -46,6 +47,10 @@ def lib():
         L.orc_kde_group.argtypes = [I64, V] + [I32] * 4 + [V] * 8
         L.orc_kde.argtypes = [I64, I32, I32, I64] + [V] * 5 + [I32] * 4 + [V] * 5
         L.orc_kde.restype = I64
+        L.orc_w1.argtypes = [I32, I32, I32] + [V] * 4 + [I32] * 3 + [V] * 9
+        L.orc_w1.restype = ctypes.c_int
+        L.orc_w1_cdf_q.argtypes = [I32, V, V, V, ctypes.c_double]
+        L.orc_w1_cdf_q.restype = ctypes.c_uint32
         _lib = L
     return _lib
 
@@ -192,3 +197,31 @@ def kde(ev: dict, n_kernels: int, n_streams: int, n_events: int | None = None, *
         out[k] = out[k].reshape(C, KDE_MAXC)
     out["bad_segments"] = int(bad)
     return out
+
+
+def w1(n_clusters, count, p50, p99, R: int, S: int, K: int, **params) -> dict:
+    """Cross-rank W1 deviation scores and IQR flags from per-cell clusters
+    ([R][S][K] and [R][S][K][KDE_MAXC] arrays)."""
+    p = dict(W1_DEFAULTS, **params)
+    C = R * S * K
+    ncl = np.ascontiguousarray(n_clusters, dtype=np.uint8).reshape(-1)
+    cnt = np.ascontiguousarray(count, dtype=np.uint32).reshape(-1)
+    a = np.ascontiguousarray(p50, dtype=np.int64).reshape(-1)
+    b = np.ascontiguousarray(p99, dtype=np.int64).reshape(-1)
+    assert ncl.size == C and cnt.size == a.size == b.size == C * KDE_MAXC
+    SK = S * K
+    out = {"n_present": np.empty(SK, np.uint32), "lo_ns": np.empty(SK, np.int64), "hi_ns": np.empty(SK, np.int64),
+           "q1": np.empty(SK, np.float64), "q3": np.empty(SK, np.float64), "fence": np.empty(SK, np.float64),
+           "n_flag": np.empty(SK, np.uint32), "score": np.empty(C, np.float64), "flag": np.empty(C, np.uint8)}
+    lib().orc_w1(R, S, K, _p(ncl), _p(cnt), _p(a), _p(b), p["grid"], p["min_ranks"], p["alpha_pm"],
+                 *[_p(out[k]) for k in ("n_present", "lo_ns", "hi_ns", "q1", "q3", "fence", "n_flag", "score",
+                                        "flag")])
+    return out
+
+
+def w1_cdf_q(count, p50, p99, x: float) -> int:
+    """Fixed-point (16-bit) mixture CDF of one rank's clusters at duration x."""
+    cnt = np.ascontiguousarray(count, dtype=np.uint32)
+    a = np.ascontiguousarray(p50, dtype=np.int64)
+    b = np.ascontiguousarray(p99, dtype=np.int64)
+    return lib().orc_w1_cdf_q(len(cnt), _p(cnt), _p(a), _p(b), x)
