@@ -201,7 +201,8 @@ def kde(ev: dict, n_kernels: int, n_streams: int, n_events: int | None = None, *
 
 def w1(n_clusters, count, p50, p99, R: int, S: int, K: int, **params) -> dict:
     """Cross-rank W1 deviation scores and IQR flags from per-cell clusters
-    ([R][S][K] and [R][S][K][KDE_MAXC] arrays)."""
+    ([R][S][K] and [R][S][K][KDE_MAXC] arrays). 'malformed' counts cells with
+    more than KDE_MAXC clusters or clusters of total count 0 (left out)."""
     p = dict(W1_DEFAULTS, **params)
     C = R * S * K
     ncl = np.ascontiguousarray(n_clusters, dtype=np.uint8).reshape(-1)
@@ -213,9 +214,10 @@ def w1(n_clusters, count, p50, p99, R: int, S: int, K: int, **params) -> dict:
     out = {"n_present": np.empty(SK, np.uint32), "lo_ns": np.empty(SK, np.int64), "hi_ns": np.empty(SK, np.int64),
            "q1": np.empty(SK, np.float64), "q3": np.empty(SK, np.float64), "fence": np.empty(SK, np.float64),
            "n_flag": np.empty(SK, np.uint32), "score": np.empty(C, np.float64), "flag": np.empty(C, np.uint8)}
-    lib().orc_w1(R, S, K, _p(ncl), _p(cnt), _p(a), _p(b), p["grid"], p["min_ranks"], p["alpha_pm"],
-                 *[_p(out[k]) for k in ("n_present", "lo_ns", "hi_ns", "q1", "q3", "fence", "n_flag", "score",
-                                        "flag")])
+    bad = lib().orc_w1(R, S, K, _p(ncl), _p(cnt), _p(a), _p(b), p["grid"], p["min_ranks"], p["alpha_pm"],
+                       *[_p(out[k]) for k in ("n_present", "lo_ns", "hi_ns", "q1", "q3", "fence", "n_flag", "score",
+                                              "flag")])
+    out["malformed"] = int(bad)
     return out
 
 

@@ -35,6 +35,10 @@
  *   - Q1, Q3 = lower nearest-rank quartiles v[(n-1)/4], v[3(n-1)/4] of the
  *     sorted scores (the same rule as the cross-rank step); no scores when
  *     fewer than min_ranks ranks are present.
+ *   - a cell takes part ("is present") iff it has 1 to W1_MAXC clusters whose
+ *     counts sum to at least 1; a cell with more than W1_MAXC clusters, or
+ *     with clusters of total count 0, is a malformed record: it is left out
+ *     like an absent cell and counted in the return value.
  *
  * Parity pins (tests/test_oracle_w1.py): the CDF at p50 and p99 against the
  * normal distribution; W1 of two equal-shape lognormals against the closed
@@ -88,10 +92,19 @@ static uint64_t hi_bound(uint64_t a, uint64_t b) {
   return q > (u128)INT64_MAX ? (uint64_t)INT64_MAX : (uint64_t)q;
 }
 
+/* 1 if the cell's cluster record is usable, 0 if absent, -1 if malformed. */
+static int cell_state(uint8_t ncl, const uint32_t* count) {
+  if (ncl == 0) return 0;
+  if (ncl > W1_MAXC) return -1;
+  uint64_t tot = 0;
+  for (int c = 0; c < ncl; c++) tot += count[c];
+  return tot > 0 ? 1 : -1;
+}
+
 /*
  * Inputs are the per-cell cluster outputs, [R][S][K] and [R][S][K][W1_MAXC].
  * Outputs per (s, k): n_present, lo_ns, hi_ns, q1, q3, fence, n_flag; per
- * cell: score, flag. Returns 0.
+ * cell: score, flag. Returns the number of malformed cells.
  */
 int orc_w1(int32_t R, int32_t S, int32_t K, const uint8_t* n_clusters, const uint32_t* count, const int64_t* p50,
            const int64_t* p99, int32_t G, int32_t min_ranks, int32_t alpha_pm, uint32_t* n_present, int64_t* lo_ns,
@@ -101,6 +114,7 @@ int orc_w1(int32_t R, int32_t S, int32_t K, const uint8_t* n_clusters, const uin
   double* sc = malloc((size_t)R * sizeof(double));
   double* sorted = malloc((size_t)R * sizeof(double));
   double* x = malloc((size_t)G * sizeof(double));
+  int malformed = 0;
   for (int32_t s = 0; s < S; s++)
     for (int32_t k = 0; k < K; k++) {
       int64_t sk = (int64_t)s * K + k;
@@ -109,7 +123,9 @@ int orc_w1(int32_t R, int32_t S, int32_t K, const uint8_t* n_clusters, const uin
         int64_t c = ((int64_t)r * S + s) * K + k;
         score[c] = 0.0;
         flag[c] = 0;
-        if (n_clusters[c] > 0) ranks[n++] = r;
+        int st = cell_state(n_clusters[c], count + c * W1_MAXC);
+        if (st > 0) ranks[n++] = r;
+        if (st < 0) malformed++;
       }
       n_present[sk] = (uint32_t)n;
       lo_ns[sk] = hi_ns[sk] = 0;
@@ -184,7 +200,7 @@ int orc_w1(int32_t R, int32_t S, int32_t K, const uint8_t* n_clusters, const uin
   free(sc);
   free(q);
   free(ranks);
-  return 0;
+  return malformed;
 }
 
 /* The fixed-point mixture CDF of one rank at duration x (tests). */

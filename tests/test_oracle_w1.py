@@ -176,3 +176,22 @@ def test_planted_faults_flagged_from_oracle_clusters():
         assert flag[pr, :, pk].all()
     others = np.setdiff1d(np.arange(R), [strag])
     assert flag[others].sum() <= 0.05 * present[others].sum()
+
+
+def test_malformed_cluster_records_are_left_out():
+    # a cell with more clusters than the record holds, and one whose cluster
+    # counts sum to 0, take no part: the scores equal those of the same
+    # ranks with the two cells absent
+    good = [(20, 1000, 1100)]
+    ranks = [good, [(20, 1300, 1400)], good, [(0, 5000, 6000)], good, [(7, 2000, 2100)]]
+    ncl, cnt, a, b = _cells(ranks)
+    ncl[5] = MAXC + 3
+    r = oracle.w1(ncl, cnt, a, b, 6, 1, 1)
+    assert r["malformed"] == 2 and r["n_present"][0] == 4
+    ncl2 = ncl.copy()
+    ncl2[3] = ncl2[5] = 0
+    r2 = oracle.w1(ncl2, cnt, a, b, 6, 1, 1)
+    assert r2["malformed"] == 0
+    for f in ("score", "flag", "fence", "q1", "q3", "lo_ns", "hi_ns", "n_present"):
+        assert np.array_equal(r[f], r2[f]), f
+    assert r["score"][3] == 0 and r["score"][5] == 0
