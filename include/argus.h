@@ -20,6 +20,10 @@
  *                       kernel id) duration clusters from the valleys of a
  *                       Gaussian KDE over log-duration, each reported as
  *                       (count, p50, p99) (section 5.2, Eq. 1).
+ *   argus_w1            clusters -> per (step, kernel) cross-rank
+ *                       Wasserstein-1 deviation scores of the reconstructed
+ *                       lognormal-mixture CDFs and the IQR upper fence over
+ *                       them (section 6.2, Eq. 2 - 4).
  *
  * Conventions for every entry point:
  *   - All array pointers are DEVICE pointers owned by the caller. The library
@@ -38,7 +42,8 @@
  *   - Calls keep no mutable global state and are safe from several host
  *     threads on different streams.
  *   - Integer outputs are exact and deterministic; float outputs are
- *     computed in double and rounded once to float.
+ *     computed in double and rounded once to float (argus_w1 reports its
+ *     doubles unrounded).
  */
 #ifndef ARGUS_H
 #define ARGUS_H
@@ -59,6 +64,8 @@ extern "C" {
 #define ARGUS_MAX_L1_STEPS 4096  /* argus_iter_windows: n_steps limit */
 #define ARGUS_MAX_KDE_KERNELS 16384 /* argus_kde: n_kernels limit */
 #define ARGUS_KDE_MAXC 4         /* argus_kde: clusters reported per cell */
+#define ARGUS_MAX_W1_RANKS 16384 /* argus_w1: n_ranks limit */
+#define ARGUS_MAX_W1_GRID 2048   /* argus_w1: grid points limit */
 
 enum {
   ARGUS_OK = 0,
@@ -72,8 +79,10 @@ enum {
 enum {
   ARGUS_DEV_BAD_SEGMENT = 1, /* some seg_off range was malformed; that segment was summarized as empty */
   ARGUS_DEV_L1_DOMAIN = 2,   /* some rank had a step time outside [0, 2^40) ns; that rank got class 0x80 */
-  ARGUS_DEV_KDE_SUMMARY = 4  /* argus_kde: the summaries passed in do not match the events (counts, min or
+  ARGUS_DEV_KDE_SUMMARY = 4, /* argus_kde: the summaries passed in do not match the events (counts, min or
                                 max); the affected cells report 0 clusters */
+  ARGUS_DEV_W1_INPUT = 8     /* argus_w1: some cell had more than ARGUS_KDE_MAXC clusters, or clusters of total
+                                count 0; such cells take no part */
 };
 
 int argus_abi_version(void);
@@ -306,6 +315,77 @@ size_t argus_kde_workspace(const argus_events_t* ev);
  * 256-byte aligned. */
 int argus_kde(const argus_events_t* ev, const argus_summary_t* sum, const argus_kde_params_t* params,
               const argus_kde_out_t* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ----------------------------------------------------------------------- W1
+ *
+ * Section 6.2 (Eq. 2 - 4): the same kernel is compared across ranks through
+ * the CDFs reconstructed from each rank's clusters. For every (step s,
+ * kernel k), over the ranks whose cell is present (1 <= n_clusters <=
+ * ARGUS_KDE_MAXC with cluster counts summing to >= 1; a cell with more
+ * clusters, or with total count 0, is malformed: it takes no part and raises
+ * ARGUS_DEV_W1_INPUT), n = number of present ranks:
+ *  1. Eq. 2: per cluster c, with p50' = max(p50, 1), p99' = max(p99, 1, p50'):
+ *     mu_c = ln p50', sigma_c = (ln p99' - mu_c) / 2.326; the rank's CDF is
+ *     F(x) = sum_c (count_c / sum count) Phi((ln x - mu_c) / sigma_c), with
+ *     Phi(z) = erfc(-z / sqrt 2) / 2, and a unit step at p50' when sigma_c
+ *     = 0. All in double, clusters in slot order.
+ *  2. Grid: lo = max(1, min over all present clusters of floor(p50'^2 /
+ *     p99')), hi = max of min(ceil(p99'^2 / p50'), INT64_MAX) (exact
+ *     integers); u_g = ln lo + g (ln hi - ln lo) / (G - 1), x_g = exp(u_g),
+ *     g = 0 .. G-1.
+ *  3. q_r(g) = min(65535, floor(65536 F_r(x_g))), the CDF in 16-bit fixed
+ *     point (F evaluated at u_g directly).
+ *  4. Eq. 3 (trapezoid rule), mean over the other ranks: with S_r(g) =
+ *     sum_b |q_r(g) - q_b(g)| (exact) and w_g = (x_{min(g+1,G-1)} -
+ *     x_{max(g-1,0)}) / 2, score_r = (sum_g w_g S_r(g), added in ascending
+ *     g) / (65536 (n - 1)).
+ *  5. Eq. 4: q1 = v[(n-1)/4], q3 = v[3(n-1)/4] of the sorted scores v (lower
+ *     nearest rank), fence = q3 + alpha_pm (q3 - q1) / 1000, flag = score >
+ *     fence; n_flag counts flags.
+ * If n < max(min_ranks, 2) the kernel is not evaluated: lo = hi = 0, q1 = q3
+ * = fence = 0, n_flag = 0 and its cells get score 0, flag 0. Absent and
+ * malformed cells always get score 0, flag 0. Every floating-point step is a
+ * double operation in the order written (no contraction); the grid, the
+ * 16-bit CDF and the quartile rule are this library's readings: the paper
+ * fixes none of them. The logarithm, exponential and erfc are the device
+ * library's, so a CDF value that lies within rounding of a multiple of
+ * 1/65536 may differ by one unit from another implementation's.
+ */
+typedef struct argus_w1_params {
+  int32_t grid;      /* grid points G, 2 .. ARGUS_MAX_W1_GRID, default 64 */
+  int32_t min_ranks; /* >= 1, default 3 */
+  int32_t alpha_pm;  /* anomaly coefficient of Eq. 4 in permille, >= 0, default 1500 */
+} argus_w1_params_t;
+
+typedef struct argus_w1_out {
+  /* per (step, kernel), [n_steps][n_kernels] */
+  uint32_t* n_present;
+  int64_t* lo_ns;
+  int64_t* hi_ns;
+  double* q1;
+  double* q3;
+  double* fence;
+  uint32_t* n_flag;
+  /* per cell, [n_ranks][n_steps][n_kernels] */
+  double* score;
+  uint8_t* flag;
+  int32_t* dev_status; /* optional (may be NULL) */
+} argus_w1_out_t;
+
+void argus_w1_default(argus_w1_params_t* p);
+
+/* Workspace bytes: 2 * n_steps * n_kernels * grid * n_ranks (the 16-bit CDF
+ * values of every rank at every grid point). */
+size_t argus_w1_workspace(int32_t n_ranks, int32_t n_steps, int32_t n_kernels, int32_t grid);
+
+/* clusters: the n_clusters, count, p50_ns and p99_ns outputs of argus_kde
+ * ([n_ranks][n_steps][n_kernels] and [..][ARGUS_KDE_MAXC]); count, p50_ns and
+ * p99_ns must be 16-byte aligned. n_ranks <= ARGUS_MAX_W1_RANKS. Every output
+ * except dev_status is required; the workspace must be 256-byte aligned and
+ * not shared by calls that may overlap. */
+int argus_w1(const argus_kde_out_t* clusters, int32_t n_ranks, int32_t n_steps, int32_t n_kernels,
+             const argus_w1_params_t* params, const argus_w1_out_t* out, void* workspace, size_t workspace_bytes,
+             void* stream);
 
 #ifdef __cplusplus
 }

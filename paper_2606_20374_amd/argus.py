@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "libargus.so")
 NBINS = 32
 
 OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
-DEV_BAD_SEGMENT, DEV_L1_DOMAIN, DEV_KDE_SUMMARY = 1, 2, 4
+DEV_BAD_SEGMENT, DEV_L1_DOMAIN, DEV_KDE_SUMMARY, DEV_W1_INPUT = 1, 2, 4, 8
 KDE_MAXC = 4
 
 V, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
@@ -66,6 +66,17 @@ class KdeOut(ctypes.Structure):
     _fields_ = [(f, V) for f in KDE_FIELDS]
 
 
+class W1Params(ctypes.Structure):
+    _fields_ = [(f, I32) for f in ("grid", "min_ranks", "alpha_pm")]
+
+
+W1_FIELDS = ["n_present", "lo_ns", "hi_ns", "q1", "q3", "fence", "n_flag", "score", "flag", "dev_status"]
+
+
+class W1Out(ctypes.Structure):
+    _fields_ = [(f, V) for f in W1_FIELDS]
+
+
 class ArgusError(RuntimeError):
     pass
 
@@ -103,6 +114,11 @@ def lib():
         L.argus_kde_workspace.restype = ctypes.c_size_t
         L.argus_kde.argtypes = [P(Events), P(Summary), P(KdeParams), P(KdeOut), V, ctypes.c_size_t, V]
         L.argus_kde.restype = ctypes.c_int
+        L.argus_w1_default.argtypes = [P(W1Params)]
+        L.argus_w1_workspace.argtypes = [I32, I32, I32, I32]
+        L.argus_w1_workspace.restype = ctypes.c_size_t
+        L.argus_w1.argtypes = [P(KdeOut), I32, I32, I32, P(W1Params), P(W1Out), V, ctypes.c_size_t, V]
+        L.argus_w1.restype = ctypes.c_int
         if L.argus_abi_version() != 1:
             raise ArgusError("libargus ABI version mismatch")
         _lib = L
@@ -141,6 +157,12 @@ def kde_defaults() -> dict:
     p = KdeParams()
     lib().argus_kde_default(ctypes.byref(p))
     return {f: getattr(p, f) for f, _ in KdeParams._fields_}
+
+
+def w1_defaults() -> dict:
+    p = W1Params()
+    lib().argus_w1_default(ctypes.byref(p))
+    return {f: getattr(p, f) for f, _ in W1Params._fields_}
 
 
 def _events(ev: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: int) -> Events:
@@ -267,4 +289,35 @@ def kde(ev: dict, summary: dict, n_ranks: int, n_steps: int, n_kernels: int, n_s
     ws = out["_workspace"]
     _check(lib().argus_kde(ctypes.byref(e), ctypes.byref(s), ctypes.byref(p), ctypes.byref(o), _ptr(ws),
                            ws.numel(), _stream(dev)), "argus_kde")
+    return out
+
+
+# ------------------------------------------------------------------------- W1
+def alloc_w1(n_ranks: int, n_steps: int, n_kernels: int, grid: int = 64, device="cuda") -> dict:
+    SK, C = n_steps * n_kernels, n_ranks * n_steps * n_kernels
+    e = lambda n, dt: torch.empty(n, dtype=dt, device=device)  # noqa: E731
+    ws = lib().argus_w1_workspace(n_ranks, n_steps, n_kernels, grid)
+    return {"n_present": e(SK, torch.int32), "lo_ns": e(SK, torch.int64), "hi_ns": e(SK, torch.int64),
+            "q1": e(SK, torch.float64), "q3": e(SK, torch.float64), "fence": e(SK, torch.float64),
+            "n_flag": e(SK, torch.int32), "score": e(C, torch.float64), "flag": e(C, torch.uint8),
+            "dev_status": e(1, torch.int32), "_workspace": e(max(ws, 256), torch.uint8), "_grid": grid}
+
+
+def w1(clusters: dict, n_ranks: int, n_steps: int, n_kernels: int, out: Optional[dict] = None, **params) -> dict:
+    """argus_w1: cross-rank W1 deviation scores and IQR flags per (step,
+    kernel) from per-cell clusters (the n_clusters, count, p50_ns and p99_ns
+    tensors of an argus_kde output)."""
+    dev = clusters["n_clusters"].device
+    p = W1Params()
+    lib().argus_w1_default(ctypes.byref(p))
+    for k, v in params.items():
+        setattr(p, k, v)
+    if out is None:
+        out = alloc_w1(n_ranks, n_steps, n_kernels, p.grid, dev)
+    cl = KdeOut(*[_ptr(clusters.get(f)) if f in ("n_clusters", "count", "p50_ns", "p99_ns") else None
+                  for f in KDE_FIELDS])
+    o = W1Out(*[_ptr(out.get(f)) for f in W1_FIELDS])
+    ws = out["_workspace"]
+    _check(lib().argus_w1(ctypes.byref(cl), n_ranks, n_steps, n_kernels, ctypes.byref(p), ctypes.byref(o), _ptr(ws),
+                          ws.numel(), _stream(dev)), "argus_w1")
     return out

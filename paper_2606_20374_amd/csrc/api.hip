@@ -209,4 +209,44 @@ int argus_kde(const argus_events_t* ev, const argus_summary_t* sum, const argus_
   return status_of(launch_kde(l, (hipStream_t)stream));
 }
 
+void argus_w1_default(argus_w1_params_t* p) {
+  if (!p) return;
+  p->grid = 64;
+  p->min_ranks = 3;
+  p->alpha_pm = 1500;
+}
+
+size_t argus_w1_workspace(int32_t n_ranks, int32_t n_steps, int32_t n_kernels, int32_t grid) {
+  return w1_workspace_bytes(n_ranks, n_steps, n_kernels, grid);
+}
+
+int argus_w1(const argus_kde_out_t* clusters, int32_t n_ranks, int32_t n_steps, int32_t n_kernels,
+             const argus_w1_params_t* params, const argus_w1_out_t* out, void* workspace, size_t workspace_bytes,
+             void* stream) {
+  if (!clusters || !params || !out) return ARGUS_EINVAL;
+  if (n_ranks < 1 || n_ranks > ARGUS_MAX_W1_RANKS || n_steps < 1 || n_kernels < 1) return ARGUS_EINVAL;
+  const int64_t SK = (int64_t)n_steps * n_kernels;
+  if (SK > INT32_MAX || SK * n_ranks > INT32_MAX) return ARGUS_EINVAL;
+  const argus_w1_params_t& p = *params;
+  if (p.grid < 2 || p.grid > ARGUS_MAX_W1_GRID || p.min_ranks < 1 || p.alpha_pm < 0) return ARGUS_EINVAL;
+  if (!clusters->n_clusters || !clusters->count || !clusters->p50_ns || !clusters->p99_ns) return ARGUS_EINVAL;
+  auto misaligned = [](const void* q, uintptr_t m) { return (reinterpret_cast<uintptr_t>(q) & (m - 1)) != 0; };
+  if (misaligned(clusters->count, 16) || misaligned(clusters->p50_ns, 16) || misaligned(clusters->p99_ns, 16))
+    return ARGUS_EINVAL;
+  const argus_w1_out_t& o = *out;
+  if (!o.n_present || !o.lo_ns || !o.hi_ns || !o.q1 || !o.q3 || !o.fence || !o.n_flag || !o.score || !o.flag)
+    return ARGUS_EINVAL;
+  if (!workspace || misaligned(workspace, 256) ||
+      workspace_bytes < argus_w1_workspace(n_ranks, n_steps, n_kernels, p.grid))
+    return ARGUS_EINVAL;
+  int rc = check_device();
+  if (rc != ARGUS_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  rc = status_of(launch_clear(o.dev_status, nullptr, st));
+  if (rc != ARGUS_OK) return rc;
+  W1Launch l{clusters->n_clusters, clusters->count, clusters->p50_ns, clusters->p99_ns, n_ranks, n_steps,
+             n_kernels, p, o, workspace};
+  return status_of(launch_w1(l, st));
+}
+
 }  // extern "C"

@@ -115,6 +115,19 @@ struct KdeLaunch {
 hipError_t launch_kde(const KdeLaunch& a, hipStream_t st);
 size_t kde_workspace_bytes(int64_t n_events, int64_t cells);
 
+struct W1Launch {
+  const uint8_t* n_clusters;
+  const uint32_t* count;
+  const int64_t* p50;
+  const int64_t* p99;
+  int32_t R, S, K;
+  argus_w1_params_t p;
+  argus_w1_out_t o;
+  void* workspace;  // w1_workspace_bytes(R, S, K, grid)
+};
+hipError_t launch_w1(const W1Launch& a, hipStream_t st);
+size_t w1_workspace_bytes(int32_t R, int32_t S, int32_t K, int32_t G);
+
 // Zero the optional device status word and the optional queue counter.
 hipError_t launch_clear(int32_t* dev_status, uint32_t* queue, hipStream_t st);
 

@@ -23,9 +23,9 @@
 // Digit histograms live in LDS; lanes of a wavefront that hit the same bin
 // are counted by one atomic (values of one kernel cluster tightly around
 // the median, so most lanes share a bin in the leading digits).
-#include <type_traits>
 
 #include "argus_internal.h"
+#include "argus_select.h"
 
 namespace argus {
 namespace {
@@ -33,121 +33,9 @@ namespace {
 typedef unsigned __int128 u128;
 typedef __int128 i128;
 
-constexpr int kBins = 256;  // 8-bit digits: the first 256 threads own one bin each
-
 __device__ __forceinline__ int64_t cell_x(uint32_t count, int64_t sum) {
   const uint64_t x = (uint64_t)sum / count;
   return x > (uint64_t)INT64_MAX ? INT64_MAX : (int64_t)x;
-}
-
-// hist[bin] += 1 for every active lane. Two rounds count all active lanes
-// sharing the first remaining lane's bin with one atomic (the bin is read
-// with readlane, no LDS round trip); the rest add individually. Must be
-// reached by every lane of the wavefront.
-__device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool active) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    const unsigned long long act = __ballot(active);
-    if (act == 0) return;
-    const int leader = __ffsll((long long)act) - 1;
-    const uint32_t lb = __builtin_amdgcn_readlane(bin, leader);
-    const bool mine = active && bin == lb;
-    const unsigned long long same = __ballot(mine);
-    if (lane == leader) atomicAdd(&hist[lb], (uint32_t)__popcll(same));
-    if (mine) active = false;
-  }
-  if (active) atomicAdd(&hist[bin], 1u);
-}
-
-template <int T>
-struct SelShared {
-  uint32_t hist[T][256];
-  uint32_t wave_tot[T * 4];
-  uint32_t digit[T], before[T];
-};
-
-// MSD radix select of the ranks k[0..T) among the valid register keys of
-// the whole block of NT >= 256 threads (bit j of vm: key[j] valid), all keys
-// <= range. Every thread of the block must call it.
-template <int NT, int V, int T, typename KeyT>
-__device__ void select_ranks(const KeyT (&key)[V], uint64_t vm, uint64_t range, const uint32_t (&k)[T],
-                             uint64_t (&out)[T], SelShared<T>& sh) {
-  uint64_t prefix[T];
-  uint32_t kk[T];
-#pragma unroll
-  for (int t = 0; t < T; ++t) {
-    prefix[t] = 0;
-    kk[t] = k[t];
-  }
-  if (range != 0) {
-    const int nbits = 64 - __builtin_clzll(range);
-    const int passes = (nbits + 7) >> 3;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    for (int p = passes - 1; p >= 0; --p) {
-      const int shift = p * 8;
-      const bool top = p == passes - 1;
-      if (tid < kBins)
-#pragma unroll
-        for (int t = 0; t < T; ++t) sh.hist[t][tid] = 0;
-      __syncthreads();
-      // targets with equal prefixes share one histogram: rep[t] is the first
-      int rep[T];
-#pragma unroll
-      for (int t = 0; t < T; ++t) {
-        rep[t] = t;
-#pragma unroll
-        for (int q = T - 1; q >= 0; --q)
-          if (q < t && prefix[q] == prefix[t]) rep[t] = q;
-      }
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        const uint64_t kj = (uint64_t)key[j];
-        const bool ok = (vm >> j) & 1u;
-        const uint32_t digit = (uint32_t)(kj >> shift) & 255u;
-        const uint64_t hi = top ? 0 : kj >> (shift + 8);
-#pragma unroll
-        for (int t = 0; t < T; ++t)
-          if (rep[t] == t) hist_add(sh.hist[t], digit, ok && (top || hi == prefix[t]));
-      }
-      __syncthreads();
-      // per-target inclusive scan over 256 bins, one bin per thread
-      uint32_t h[T], v[T];
-      if (tid < kBins) {
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-          h[t] = sh.hist[rep[t]][tid];
-          v[t] = h[t];
-          for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t n = __shfl_up(v[t], o, 64);
-            if (lane >= o) v[t] += n;
-          }
-          if (lane == 63) sh.wave_tot[t * 4 + w] = v[t];
-        }
-      }
-      __syncthreads();
-      if (tid < kBins) {
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-          for (int ww = 0; ww < w; ++ww) v[t] += sh.wave_tot[t * 4 + ww];
-          const uint32_t excl = v[t] - h[t];
-          if (excl <= kk[t] && kk[t] < v[t]) {
-            sh.digit[t] = (uint32_t)tid;
-            sh.before[t] = excl;
-          }
-        }
-      }
-      __syncthreads();
-#pragma unroll
-      for (int q = 0; q < T; ++q) {
-        prefix[q] = (prefix[q] << 8) | sh.digit[q];
-        kk[q] -= sh.before[q];
-      }
-      __syncthreads();
-    }
-  }
-#pragma unroll
-  for (int t = 0; t < T; ++t) out[t] = prefix[t];
 }
 
 // ---------------------------------------------------------------- transpose
@@ -404,30 +292,6 @@ __global__ __launch_bounds__(NT) void xr_rank(RankArgs a) {
     a.o.n_flag_rank[rs] = nf_sh;
     a.o.straggler[rs] = strag ? 1 : 0;
   }
-}
-
-// Call f(std::integral_constant<int, NT>, std::integral_constant<int, V>)
-// with a block size NT and the smallest instantiated per-thread count V such
-// that NT * V >= n (n <= 16384): at most 24 values per thread stay in
-// registers without spilling.
-template <typename F>
-void dispatch_block(int n, F&& f) {
-  using std::integral_constant;
-  auto pick = [&](auto nt) {
-    constexpr int NT = decltype(nt)::value;
-    const int v = (n + NT - 1) / NT;
-    if (v <= 1) return f(nt, integral_constant<int, 1>{});
-    if (v <= 2) return f(nt, integral_constant<int, 2>{});
-    if (v <= 4) return f(nt, integral_constant<int, 4>{});
-    if (v <= 8) return f(nt, integral_constant<int, 8>{});
-    if (v <= 12) return f(nt, integral_constant<int, 12>{});
-    if (v <= 16) return f(nt, integral_constant<int, 16>{});
-    if (v <= 20) return f(nt, integral_constant<int, 20>{});
-    return f(nt, integral_constant<int, 24>{});
-  };
-  if (n <= 24 * 256) return pick(integral_constant<int, 256>{});
-  if (n <= 24 * 512) return pick(integral_constant<int, 512>{});
-  return pick(integral_constant<int, 1024>{});
 }
 
 template <int NT, int V>

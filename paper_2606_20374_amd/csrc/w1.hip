@@ -1,0 +1,520 @@
+// Cross-rank Wasserstein-1 deviation scores over the duration clusters of
+// every (step, kernel) (section 6.2, Eq. 2 - 4; the step-by-step definition
+// is in include/argus.h).
+//
+// Launches, in order:
+//   w1_init     per (step, kernel): n_present = 0 and the identities of the
+//               grid-bound minimum / maximum.
+//   w1_bounds   one lane per kernel id (64 ids x 64 ranks per workgroup, so
+//               the cluster records of neighbouring ids are read together):
+//               present ranks, grid bounds lo / hi by 64-bit atomics,
+//               malformed records.
+//   w1_cdf      one lane per rank (64 ranks of one kernel id per wavefront):
+//               the count-weighted lognormal mixture of Eq. 2 at every grid
+//               point, quantised to 16 bits, into a [S][K][G][R] workspace
+//               (ranks contiguous, so the writes and the next kernel's reads
+//               are coalesced).
+//   w1_score    one workgroup per (step, kernel): for each grid point the
+//               exact sums S_a = sum_b |q_a - q_b| over all present ranks
+//               from a counting sort of the 16-bit values in LDS (a
+//               256-bucket histogram, then the 256 bins of each occupied
+//               bucket, 16-bit counters two to a word) and a prefix sum over
+//               the sorted values: with c the number of values below q_a and
+//               P their sum, S_a = q_a (2 c - n) + T - 2 P. The trapezoid
+//               weights are applied in grid order, then the lower
+//               nearest-rank quartiles of the scores come from a radix
+//               selection on their bit patterns (non-negative doubles order
+//               like their bits), then the upper fence of Eq. 4 and the
+//               flags.
+// The pairwise matrix of the paper is never formed: S_a is the row sum of
+// |F_a - F_b| at one grid point, which is all the mean-W1 score needs.
+#include "argus_internal.h"
+#include "argus_select.h"
+
+namespace argus {
+namespace {
+
+typedef unsigned __int128 u128;
+
+constexpr int kMaxC = ARGUS_KDE_MAXC;
+constexpr double kZ99 = 2.326;                     // standard normal 99th percentile, as printed (Eq. 2)
+constexpr double kSqrt2 = 1.41421356237309504880;  // Phi(z) = erfc(-z / sqrt 2) / 2
+constexpr int kFineWords = 32768;                  // 65536 16-bit bin counters, two per word
+
+struct W1Args {
+  const uint8_t* ncl;
+  const uint32_t* cnt;
+  const int64_t* p50;
+  const int64_t* p99;
+  int32_t R, S, K, G, min_ranks, alpha_pm;
+  argus_w1_out_t o;
+  uint16_t* q;  // workspace [S][K][G][R]
+};
+
+__device__ __forceinline__ int64_t cell_of(const W1Args& a, int r, int s, int k) {
+  return ((int64_t)r * a.S + s) * a.K + k;
+}
+
+// 1: usable cluster record, 0: absent, -1: malformed (more clusters than the
+// record holds, or clusters of total count 0). tot: total count.
+__device__ __forceinline__ int cell_state(const W1Args& a, int64_t c, uint32_t& nc, uint64_t& tot) {
+  nc = a.ncl[c];
+  tot = 0;
+  if (nc == 0) return 0;
+  if (nc > kMaxC) return -1;
+  for (uint32_t cl = 0; cl < nc; ++cl) tot += a.cnt[c * kMaxC + cl];
+  return tot > 0 ? 1 : -1;
+}
+
+// Cluster median and 99th percentile, at least 1 ns, p99 not below p50.
+__device__ __forceinline__ void cluster_ab(const W1Args& a, int64_t c, uint32_t cl, uint64_t& x, uint64_t& y) {
+  const int64_t p = a.p50[c * kMaxC + cl], t = a.p99[c * kMaxC + cl];
+  x = p > 1 ? (uint64_t)p : 1;
+  y = t > 1 ? (uint64_t)t : 1;
+  if (y < x) y = x;
+}
+
+// floor(x^2 / y) and min(ceil(y^2 / x), INT64_MAX), for 1 <= x <= y: the
+// lognormal's mirror of its 99th percentile below the median, and its
+// 99.99th percentile.
+__device__ __forceinline__ uint64_t lo_of(uint64_t x, uint64_t y) {
+  if (x < (1ull << 32)) return (x * x) / y;
+  return (uint64_t)(((u128)x * x) / y);
+}
+__device__ __forceinline__ uint64_t hi_of(uint64_t x, uint64_t y) {
+  u128 q;
+  if (y < (1ull << 32))
+    q = (y * y + (x - 1)) / x;
+  else
+    q = ((u128)y * y + (x - 1)) / x;
+  return q > (u128)INT64_MAX ? (uint64_t)INT64_MAX : (uint64_t)q;
+}
+
+// ------------------------------------------------------------------- init
+__global__ __launch_bounds__(256) void w1_init(W1Args a) {
+  const int64_t sk = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (sk >= (int64_t)a.S * a.K) return;
+  a.o.n_present[sk] = 0;
+  a.o.lo_ns[sk] = -1;  // all ones: identity of the unsigned minimum
+  a.o.hi_ns[sk] = 0;
+}
+
+// ----------------------------------------------------------------- bounds
+__global__ __launch_bounds__(256) void w1_bounds(W1Args a) {
+  __shared__ uint32_t n_sh[4][64];
+  __shared__ unsigned long long lo_sh[4][64], hi_sh[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int k = blockIdx.x * 64 + lane, s = blockIdx.z, r0 = blockIdx.y * 64;
+  uint32_t n = 0;
+  uint64_t lo = ~0ull, hi = 0;
+  bool bad = false;
+  if (k < a.K) {
+    for (int i = w; i < 64; i += 4) {
+      const int r = r0 + i;
+      if (r >= a.R) break;
+      const int64_t c = cell_of(a, r, s, k);
+      uint32_t nc;
+      uint64_t tot;
+      const int st = cell_state(a, c, nc, tot);
+      if (st < 0) bad = true;
+      if (st <= 0) continue;
+      ++n;
+      for (uint32_t cl = 0; cl < nc; ++cl) {
+        uint64_t x, y;
+        cluster_ab(a, c, cl, x, y);
+        const uint64_t l = lo_of(x, y), h = hi_of(x, y);
+        lo = l < lo ? l : lo;
+        hi = h > hi ? h : hi;
+      }
+    }
+  }
+  if (__ballot(bad) != 0 && lane == 0 && a.o.dev_status) atomicOr(a.o.dev_status, (int32_t)ARGUS_DEV_W1_INPUT);
+  n_sh[w][lane] = n;
+  lo_sh[w][lane] = lo;
+  hi_sh[w][lane] = hi;
+  __syncthreads();
+  if (w != 0 || k >= a.K) return;
+#pragma unroll
+  for (int i = 1; i < 4; ++i) {
+    n += n_sh[i][lane];
+    lo = lo_sh[i][lane] < lo ? lo_sh[i][lane] : lo;
+    hi = hi_sh[i][lane] > hi ? hi_sh[i][lane] : hi;
+  }
+  if (n == 0) return;
+  const int64_t sk = (int64_t)s * a.K + k;
+  atomicAdd(&a.o.n_present[sk], n);
+  atomicMin(reinterpret_cast<unsigned long long*>(&a.o.lo_ns[sk]), (unsigned long long)lo);
+  atomicMax(reinterpret_cast<unsigned long long*>(&a.o.hi_ns[sk]), (unsigned long long)hi);
+}
+
+__device__ __forceinline__ bool evaluated(const W1Args& a, uint32_t n) {
+  return n >= (uint32_t)a.min_ranks && n >= 2;
+}
+
+// Grid coordinates of one (step, kernel): u_g = lnlo + g du.
+__device__ __forceinline__ void grid_of(const W1Args& a, int64_t sk, double& lnlo, double& du) {
+  const uint64_t lo = (uint64_t)a.o.lo_ns[sk], hi = (uint64_t)a.o.hi_ns[sk];
+  lnlo = log((double)(lo < 1 ? 1 : lo));
+  const double lnhi = log((double)hi);
+  du = (lnhi - lnlo) / (double)(a.G - 1);
+}
+
+// -------------------------------------------------------------------- CDF
+__global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int k = blockIdx.x * 4 + w, r = blockIdx.y * 64 + lane, s = blockIdx.z;
+  if (k >= a.K || r >= a.R) return;
+  const int64_t sk = (int64_t)s * a.K + k;
+  if (!evaluated(a, a.o.n_present[sk])) return;
+  const int64_t c = cell_of(a, r, s, k);
+  uint32_t nc;
+  uint64_t tot;
+  if (cell_state(a, c, nc, tot) <= 0) return;
+  double mu[kMaxC], den[kMaxC], wt[kMaxC];
+  bool spread[kMaxC];
+#pragma unroll
+  for (int cl = 0; cl < kMaxC; ++cl) {
+    mu[cl] = den[cl] = wt[cl] = 0.0;
+    spread[cl] = false;
+    if ((uint32_t)cl >= nc) continue;
+    const int64_t p = a.p50[c * kMaxC + cl], t = a.p99[c * kMaxC + cl];
+    const double x = p > 1 ? (double)p : 1.0;
+    double y = t > 1 ? (double)t : 1.0;
+    if (y < x) y = x;
+    mu[cl] = log(x);
+    const double sigma = (log(y) - mu[cl]) / kZ99;
+    spread[cl] = sigma > 0.0;
+    den[cl] = sigma * kSqrt2;
+    wt[cl] = (double)a.cnt[c * kMaxC + cl] / (double)tot;
+  }
+  double lnlo, du;
+  grid_of(a, sk, lnlo, du);
+  uint16_t* out = a.q + (sk * a.G) * a.R + r;
+  for (int g = 0; g < a.G; ++g) {
+    const double u = lnlo + (double)g * du;
+    double F = 0.0;
+#pragma unroll
+    for (int cl = 0; cl < kMaxC; ++cl) {
+      if ((uint32_t)cl >= nc) break;
+      const double phi = spread[cl] ? 0.5 * erfc((mu[cl] - u) / den[cl]) : (u >= mu[cl] ? 1.0 : 0.0);
+      F += wt[cl] * phi;
+    }
+    const double v = floor(F * 65536.0);
+    out[(int64_t)g * a.R] = v >= 65535.0 ? (uint16_t)65535 : (uint16_t)(uint32_t)v;
+  }
+}
+
+// ------------------------------------------------------------------ score
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t t = __shfl_up(v, o, 64);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+// Adds one to the 16-bit counter of bin v (two counters per word) for every
+// active lane and returns the counter's value before the lane's own claim,
+// so lanes with equal v get distinct consecutive values. Lanes sharing the
+// first remaining lane's value are served by one atomic (two rounds: at the
+// ends of the grid most ranks share the value 0 or 65535); the rest claim
+// one by one. Must be reached by every lane of the wavefront.
+__device__ __forceinline__ uint32_t claim_bin(uint32_t* fine, uint32_t v, bool active) {
+  const int lane = threadIdx.x & 63;
+  const unsigned long long below = (1ull << lane) - 1ull;
+  uint32_t res = 0;
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const unsigned long long act = __ballot(active);
+    if (act == 0) return res;
+    const int leader = __ffsll((long long)act) - 1;
+    const uint32_t lv = __builtin_amdgcn_readlane(v, leader);
+    const bool mine = active && v == lv;
+    const unsigned long long same = __ballot(mine);
+    const uint32_t sh = (lv & 1u) * 16u;
+    uint32_t old = 0;
+    if (lane == leader) old = atomicAdd(&fine[lv >> 1], (uint32_t)__popcll(same) << sh);
+    old = __builtin_amdgcn_readlane(old, leader);
+    if (mine) {
+      res = ((old >> sh) & 0xFFFFu) + (uint32_t)__popcll(same & below);
+      active = false;
+    }
+  }
+  if (active) {
+    const uint32_t sh = (v & 1u) * 16u;
+    res = (atomicAdd(&fine[v >> 1], 1u << sh) >> sh) & 0xFFFFu;
+  }
+  return res;
+}
+
+template <int NT, int V>
+__global__ __launch_bounds__(NT) void w1_score(W1Args a) {
+  constexpr int NW = NT / 64;
+  __shared__ uint32_t fine[kFineWords];  // bin counters, then the sorted values and their prefix sums
+  __shared__ double wts[ARGUS_MAX_W1_GRID];  // trapezoid weights
+  __shared__ uint32_t bcnt[256], bexcl[256];
+  __shared__ uint32_t wtot[NW];
+  __shared__ SelShared<2> sel;
+  __shared__ unsigned long long mn_sh, mx_sh;
+  __shared__ uint32_t nf_sh;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t sk = blockIdx.x;
+  const int s = (int)(sk / a.K), k = (int)(sk % a.K);
+  const uint32_t n = a.o.n_present[sk];
+
+  if (!evaluated(a, n)) {
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const int r = tid + j * NT;
+      if (r >= a.R) break;
+      const int64_t c = cell_of(a, r, s, k);
+      a.o.score[c] = 0.0;
+      a.o.flag[c] = 0;
+    }
+    if (tid == 0) {
+      a.o.lo_ns[sk] = 0;
+      a.o.hi_ns[sk] = 0;
+      a.o.q1[sk] = a.o.q3[sk] = a.o.fence[sk] = 0.0;
+      a.o.n_flag[sk] = 0;
+    }
+    return;
+  }
+
+  uint32_t pm = 0;  // bit j: slot j (rank tid + j NT) is present
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int r = tid + j * NT;
+    if (r >= a.R) break;
+    uint32_t nc;
+    uint64_t tot;
+    if (cell_state(a, cell_of(a, r, s, k), nc, tot) > 0) pm |= 1u << j;
+  }
+  double lnlo, du;
+  grid_of(a, sk, lnlo, du);
+  const int G = a.G;
+  const uint16_t* qrow = a.q + sk * (int64_t)G * a.R;
+  // w_g = (x_{min(g+1,G-1)} - x_{max(g-1,0)}) / 2, x_i = exp(lnlo + i du)
+  for (int g = tid; g < G; g += NT)
+    wts[g] = (exp(lnlo + (double)(g + 1 < G ? g + 1 : G - 1) * du) - exp(lnlo + (double)(g > 0 ? g - 1 : 0) * du)) /
+             2.0;
+
+  // per slot: acc = weighted sum; qt = q | (rank among equal values) << 16;
+  // cl2 / qn2: values below q / the next grid point's q, 16 bits each, two
+  // slots to a word (keeps the 16-slot variant in registers)
+  constexpr int V2 = (V + 1) / 2;
+  double acc[V];
+  uint32_t qt[V], cl2[V2], qn2[V2];
+  auto present = [&](int j) { return ((pm >> j) & 1u) != 0; };
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    acc[j] = 0.0;
+    qt[j] = present(j) ? qrow[(uint32_t)(tid + j * NT)] : 0u;
+  }
+#pragma unroll
+  for (int j = 0; j < V2; ++j) cl2[j] = qn2[j] = 0;
+  if (tid < 256) bcnt[tid] = 0;
+  if (tid == 0) {
+    mn_sh = ~0ull;
+    mx_sh = 0;
+    nf_sh = 0;
+  }
+  __syncthreads();
+
+  const int E = ((int)n + NT - 1) / NT;  // sorted values per thread in the prefix sum
+  for (int g = 0; g < G; ++g) {
+    if (g + 1 < G) {
+      const uint16_t* nrow = qrow + (int64_t)(g + 1) * a.R;  // uniform row base, 32-bit lane offsets
+#pragma unroll
+      for (int j = 0; j < V; j += 2) {
+        const uint32_t lo = present(j) ? nrow[(uint32_t)(tid + j * NT)] : 0u;
+        const uint32_t hi = j + 1 < V && present(j + 1) ? nrow[(uint32_t)(tid + (j + 1) * NT)] : 0u;
+        qn2[j >> 1] = lo | (hi << 16);
+      }
+    }
+    // 1. bucket (high byte) counts
+#pragma unroll
+    for (int j = 0; j < V; ++j) hist_add(bcnt, (qt[j] & 0xFFFFu) >> 8, present(j));
+    __syncthreads();
+    // 2. bucket scan, first half; clear the bins of the occupied buckets
+    uint32_t bc = 0, binc = 0;
+    if (tid < 256) {
+      bc = bcnt[tid];
+      binc = wave_incl_scan(bc);
+      if (lane == 63) wtot[wv] = binc;
+    }
+    for (int ch = tid; ch < kFineWords / 4; ch += NT)
+      if (bcnt[ch >> 5]) *reinterpret_cast<uint4*>(&fine[ch * 4]) = make_uint4(0, 0, 0, 0);
+    __syncthreads();
+    // 3. bucket exclusive prefix; per-value claims (rank among equal values)
+    if (tid < 256) {
+      uint32_t base = 0;
+      for (int w = 0; w < wv; ++w) base += wtot[w];
+      bexcl[tid] = base + binc - bc;
+    }
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const uint32_t v = qt[j] & 0xFFFFu;
+      qt[j] = v | (claim_bin(fine, v, present(j)) << 16);
+    }
+    __syncthreads();
+    // 4. exclusive prefix over the 256 bins of each occupied bucket
+    for (int h = wv; h < 256; h += NW) {
+      if (bcnt[h] == 0) continue;
+      uint2* p = reinterpret_cast<uint2*>(&fine[h * 128 + 2 * lane]);
+      const uint2 wd = *p;
+      const uint32_t b0 = wd.x & 0xFFFFu, b1 = wd.x >> 16, b2 = wd.y & 0xFFFFu, b3 = wd.y >> 16;
+      const uint32_t t = b0 + b1 + b2 + b3;
+      const uint32_t e0 = wave_incl_scan(t) - t, e1 = e0 + b0, e2 = e1 + b1, e3 = e2 + b2;
+      *p = make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
+    }
+    __syncthreads();
+    // 5. values below q: bucket prefix + bin prefix
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const uint32_t v = qt[j] & 0xFFFFu;
+      const uint32_t clt = present(j) ? bexcl[v >> 8] + ((fine[v >> 1] >> ((v & 1u) * 16u)) & 0xFFFFu) : 0u;
+      cl2[j >> 1] = (j & 1) ? (cl2[j >> 1] & 0xFFFFu) | (clt << 16) : (cl2[j >> 1] & 0xFFFF0000u) | clt;
+    }
+    __syncthreads();
+    // 6. counting-sort scatter to position (values below) + (rank among
+    //    equal values); clear the bucket counts for the next point
+#pragma unroll
+    for (int j = 0; j < V; ++j)
+      if (present(j)) fine[((cl2[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu) + (qt[j] >> 16)] = qt[j] & 0xFFFFu;
+    if (tid < 256) bcnt[tid] = 0;
+    __syncthreads();
+    // 7. exclusive prefix sums of the sorted values, in place
+    const int i0 = tid * E, i1 = i0 + E < (int)n ? i0 + E : (int)n;
+    uint32_t loc = 0;
+    for (int i = i0; i < i1; ++i) loc += fine[i];
+    const uint32_t linc = wave_incl_scan(loc);
+    if (lane == 63) wtot[wv] = linc;
+    __syncthreads();
+    uint32_t run = linc - loc, T = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const uint32_t x = wtot[w];
+      if (w < wv) run += x;
+      T += x;
+    }
+    for (int i = i0; i < i1; ++i) {
+      const uint32_t x = fine[i];
+      fine[i] = run;
+      run += x;
+    }
+    __syncthreads();
+    // 8. S_a = q (2 c - n) + T - 2 P, weighted by the trapezoid rule
+    const double wg = wts[g];
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      if (present(j)) {
+        const int64_t clt = (cl2[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
+        const int64_t S =
+            (int64_t)(qt[j] & 0xFFFFu) * (2 * clt - (int64_t)n) + (int64_t)T - 2 * (int64_t)fine[clt];
+        acc[j] += wg * (double)S;
+      }
+      qt[j] = (qn2[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
+    }
+  }
+
+  // deviation scores; quartiles by radix selection on their bit patterns
+  // (the scores are kept only as their bits, offset by the minimum)
+  const double norm = 65536.0 * (double)(n - 1);
+  uint64_t key[V];
+  unsigned long long mn = ~0ull, mx = 0;
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    key[j] = (uint64_t)__double_as_longlong(acc[j] / norm);
+    if (present(j)) {
+      mn = key[j] < mn ? key[j] : mn;
+      mx = key[j] > mx ? key[j] : mx;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    const unsigned long long x = __shfl_xor(mn, o, 64), y = __shfl_xor(mx, o, 64);
+    mn = x < mn ? x : mn;
+    mx = y > mx ? y : mx;
+  }
+  if (lane == 0) {
+    atomicMin(&mn_sh, mn);
+    atomicMax(&mx_sh, mx);
+  }
+  __syncthreads();
+  const uint64_t kmin = mn_sh, kmax = mx_sh;
+#pragma unroll
+  for (int j = 0; j < V; ++j) key[j] = present(j) ? key[j] - kmin : 0;
+  const uint32_t nm1 = n - 1;
+  const uint32_t ranks[2] = {nm1 / 4, (uint32_t)((3ull * nm1) / 4)};
+  uint64_t qs[2];
+  select_ranks<NT, V, 2>(key, (uint64_t)pm, kmax - kmin, ranks, qs, sel);
+  const double a1 = __longlong_as_double((long long)(kmin + qs[0]));
+  const double a3 = __longlong_as_double((long long)(kmin + qs[1]));
+  const double fence = a3 + (double)a.alpha_pm * (a3 - a1) / 1000.0;
+
+  uint32_t nf = 0;
+#pragma unroll
+  for (int j = 0; j < V; ++j) {
+    const int r = tid + j * NT;
+    if (r >= a.R) break;
+    const bool p = present(j);
+    const double sc = __longlong_as_double((long long)(kmin + key[j]));
+    const bool f = p && sc > fence;
+    nf += f ? 1u : 0u;
+    const int64_t c = cell_of(a, r, s, k);
+    a.o.score[c] = p ? sc : 0.0;
+    a.o.flag[c] = f ? 1 : 0;
+  }
+  for (int o = 32; o > 0; o >>= 1) nf += __shfl_xor(nf, o, 64);
+  if (lane == 0 && nf) atomicAdd(&nf_sh, nf);
+  __syncthreads();
+  if (tid == 0) {
+    a.o.lo_ns[sk] = a.o.lo_ns[sk] < 1 ? 1 : a.o.lo_ns[sk];
+    a.o.q1[sk] = a1;
+    a.o.q3[sk] = a3;
+    a.o.fence[sk] = fence;
+    a.o.n_flag[sk] = nf_sh;
+  }
+}
+
+template <int NT, int V>
+void launch_score(const W1Args& wa, hipStream_t st) {
+  hipLaunchKernelGGL((w1_score<NT, V>), dim3((unsigned)((int64_t)wa.S * wa.K)), dim3(NT), 0, st, wa);
+}
+
+}  // namespace
+
+size_t w1_workspace_bytes(int32_t R, int32_t S, int32_t K, int32_t G) {
+  if (R < 0 || S < 0 || K < 0 || G < 0) return 0;
+  return (size_t)S * (size_t)K * (size_t)G * (size_t)R * sizeof(uint16_t);
+}
+
+hipError_t launch_w1(const W1Launch& l, hipStream_t st) {
+  W1Args wa{l.n_clusters, l.count, l.p50, l.p99, l.R, l.S, l.K, l.p.grid, l.p.min_ranks, l.p.alpha_pm, l.o,
+            static_cast<uint16_t*>(l.workspace)};
+  const int64_t SK = (int64_t)l.S * l.K;
+  hipLaunchKernelGGL(w1_init, dim3((unsigned)((SK + 255) / 256)), dim3(256), 0, st, wa);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(w1_bounds, dim3((l.K + 63) / 64, (l.R + 63) / 64, l.S), dim3(256), 0, st, wa);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(w1_cdf, dim3((l.K + 3) / 4, (l.R + 63) / 64, l.S), dim3(256), 0, st, wa);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // register-resident slots per thread: R <= 1024 with 256 threads, else 1024 threads
+  const int R = l.R;
+  if (R <= 256) launch_score<256, 1>(wa, st);
+  else if (R <= 512) launch_score<256, 2>(wa, st);
+  else if (R <= 1024) launch_score<256, 4>(wa, st);
+  else if (R <= 2048) launch_score<1024, 2>(wa, st);
+  else if (R <= 4096) launch_score<1024, 4>(wa, st);
+  else if (R <= 8192) launch_score<1024, 8>(wa, st);
+  else if (R <= 10240) launch_score<1024, 10>(wa, st);
+  else if (R <= 12288) launch_score<1024, 12>(wa, st);
+  else launch_score<1024, 16>(wa, st);
+  return hipGetLastError();
+}
+
+}  // namespace argus

@@ -114,3 +114,37 @@ def test_kde_rejects_bad_arguments(mutate):
         mutate(e, s, p)
     assert pa.lib().argus_kde(ctypes.byref(e), ctypes.byref(s), ctypes.byref(p), ctypes.byref(o), ws, n,
                               None) == A.EINVAL
+
+
+def test_w1_defaults_and_workspace():
+    assert pa.w1_defaults() == dict(grid=64, min_ranks=3, alpha_pm=1500)
+    assert pa.lib().argus_w1_workspace(10240, 1, 2048, 64) == 2 * 10240 * 2048 * 64
+
+
+@pytest.mark.parametrize("mutate", [
+    lambda c, p, o, d: setattr(p, "grid", 1),
+    lambda c, p, o, d: setattr(p, "grid", 2049),
+    lambda c, p, o, d: setattr(p, "min_ranks", 0),
+    lambda c, p, o, d: setattr(p, "alpha_pm", -1),
+    lambda c, p, o, d: setattr(c, "p99_ns", None),
+    lambda c, p, o, d: setattr(c, "count", 0x1008),  # misaligned cluster counts
+    lambda c, p, o, d: setattr(o, "score", None),
+    lambda c, p, o, d: d.__setitem__("R", 16385),
+    lambda c, p, o, d: d.__setitem__("S", 0),
+    "misaligned", "small",
+])
+def test_w1_rejects_bad_arguments(mutate):
+    c = A.KdeOut(0x1000, 0x1000, 0x1000, 0x1000, None, None)
+    p = A.W1Params()
+    pa.lib().argus_w1_default(ctypes.byref(p))
+    o = A.W1Out(*([0x1000] * 9 + [None]))
+    d = {"R": 8, "S": 2, "K": 4}
+    ws, n = 0x10000, 1 << 20
+    if mutate == "misaligned":
+        ws = 0x10080
+    elif mutate == "small":
+        n = 2 * 8 * 2 * 4 * 64 - 1
+    else:
+        mutate(c, p, o, d)
+    assert pa.lib().argus_w1(ctypes.byref(c), d["R"], d["S"], d["K"], ctypes.byref(p), ctypes.byref(o), ws, n,
+                             None) == A.EINVAL
