@@ -113,7 +113,8 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes (counter calibration)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--kde-reps", type=int, default=5, help="timed argus_kde calls (0: skip the KDE leg)")
+    ap.add_argument("--kde-reps", type=int, default=5, help="timed argus_kde calls (0: skip the KDE and W1 legs)")
+    ap.add_argument("--w1-reps", type=int, default=5, help="timed argus_w1 calls (0: skip the W1 leg)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -270,6 +271,30 @@ def main():
             "summary_bytes_per_rank_step": wire / G,
             "raw_bytes_per_rank_step": 24 * trace.n_events / G,
         }
+        if args.w1_reps > 0:
+            # cross-rank W1 deviation scores over those clusters (section 6.2,
+            # Eq. 2 - 4): 64-point log grid, IQR fence alpha 1.5
+            w1_out = pa.alloc_w1(R, S, K, 64, dev)
+            pa.w1(kde_out, R, S, K, out=w1_out)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(args.w1_reps):
+                pa.w1(kde_out, R, S, K, out=w1_out)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            w1_ms = e0.elapsed_time(e1) / args.w1_reps
+            assert int(w1_out["dev_status"].item()) == 0
+            wf = w1_out["flag"].cpu().numpy().reshape(R, S, K).astype(bool)
+            pres = ncl.reshape(R, S, K) > 0
+            strag = sorted(truth["stragglers"])
+            others = np.setdiff1d(np.arange(R), strag)
+            result["w1"] = {
+                "ms": w1_ms, "ms_per_step": w1_ms / S, "grid": 64,
+                "kernel_steps": S * K, "present_cells": int(pres.sum()),
+                "straggler_cells_flagged_frac": float(wf[strag].sum() / max(1, pres[strag].sum())),
+                "other_cells_flagged_frac": float(wf[others].sum() / max(1, pres[others].sum())),
+            }
+            del w1_out
         del kde_out
         torch.cuda.empty_cache()
 
