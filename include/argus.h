@@ -24,6 +24,11 @@
  *                       Wasserstein-1 deviation scores of the reconstructed
  *                       lognormal-mixture CDFs and the IQR upper fence over
  *                       them (section 6.2, Eq. 2 - 4).
+ *   argus_l2            summaries + a routing table and parallelism groups ->
+ *                       per (step, event, group) mean, sample std, CV class
+ *                       and per-rank z-score straggler flags, every event
+ *                       compared only inside the groups of its dimension
+ *                       (section 6.1, Table "routing"; Appendix B, Eq. 5).
  *
  * Conventions for every entry point:
  *   - All array pointers are DEVICE pointers owned by the caller. The library
@@ -66,6 +71,8 @@ extern "C" {
 #define ARGUS_KDE_MAXC 4         /* argus_kde: clusters reported per cell */
 #define ARGUS_MAX_W1_RANKS 16384 /* argus_w1: n_ranks limit */
 #define ARGUS_MAX_W1_GRID 2048   /* argus_w1: grid points limit */
+#define ARGUS_MAX_L2_RANKS 65536 /* argus_l2: n_ranks limit */
+#define ARGUS_MAX_L2_DIMS 16     /* argus_l2: parallelism dimensions limit */
 
 enum {
   ARGUS_OK = 0,
@@ -81,8 +88,13 @@ enum {
   ARGUS_DEV_L1_DOMAIN = 2,   /* some rank had a step time outside [0, 2^40) ns; that rank got class 0x80 */
   ARGUS_DEV_KDE_SUMMARY = 4, /* argus_kde: the summaries passed in do not match the events (counts, min or
                                 max); the affected cells report 0 clusters */
-  ARGUS_DEV_W1_INPUT = 8     /* argus_w1: some cell had more than ARGUS_KDE_MAXC clusters, or clusters of total
+  ARGUS_DEV_W1_INPUT = 8,    /* argus_w1: some cell had more than ARGUS_KDE_MAXC clusters, or clusters of total
                                 count 0; such cells take no part */
+  ARGUS_DEV_GROUPS_MALFORMED = 16, /* argus_l2: a group range outside [0, n_ranks] or reversed (group skipped), or
+                                      a member id outside [0, n_ranks) (member skipped) */
+  ARGUS_DEV_GROUPS_DUPLICATE = 32, /* argus_l2: a rank listed more than once in one dimension (only its first
+                                      listing counts) */
+  ARGUS_DEV_L2_DOMAIN = 64         /* argus_l2: a mean duration at or above 2^40 ns (that cell is left out) */
 };
 
 int argus_abi_version(void);
@@ -386,6 +398,77 @@ size_t argus_w1_workspace(int32_t n_ranks, int32_t n_steps, int32_t n_kernels, i
 int argus_w1(const argus_kde_out_t* clusters, int32_t n_ranks, int32_t n_steps, int32_t n_kernels,
              const argus_w1_params_t* params, const argus_w1_out_t* out, void* workspace, size_t workspace_bytes,
              void* stream);
+
+/* ----------------------------------------------------------------------- L2
+ *
+ * Section 6.1 (parallelism-group-aware routing, Table "routing") and Appendix
+ * B (Eq. 5): each event is compared only among the ranks of the parallelism
+ * group that its dimension assigns them to. Events are the summaries' kernel
+ * ids; the window is one step.
+ *
+ * Groups: route[e] is the dimension of event e (a value >= n_dims, e.g.
+ * 0xFF, means "not compared"); dimension d has up to max_groups groups, group
+ * g of d lists members[d][group_off[d][g] .. group_off[d][g+1]) (rank ids).
+ * A range that is reversed or leaves [0, n_ranks] is skipped and a member id
+ * outside [0, n_ranks) is skipped (ARGUS_DEV_GROUPS_MALFORMED); a rank listed
+ * more than once in a dimension counts only at its first listing, the lowest
+ * group and then the lowest position (ARGUS_DEV_GROUPS_DUPLICATE).
+ *
+ * For step s, event e routed to d, group g: x_r = floor((uint64)sum / count)
+ * over the listed ranks with count >= 1 and x_r < 2^40 (larger x: left out,
+ * ARGUS_DEV_L2_DOMAIN); n of them. With n >= max(min_group, 2), exact
+ * integers S = sum x, Q = sum x^2, D = n Q - S^2 (= n (n - 1) sigma^2):
+ *   mean = (double)S / n, std = sqrt((double)D / ((double)n (n - 1))),
+ *   cv = mean > 0 ? std / mean : 0 (each a double operation);
+ *   cls = 0 (balanced) if S = 0 or n D 10^6 < cv_mild_pm^2 (n - 1) S^2,
+ *         1 (mild) else if n D 10^6 < cv_severe_pm^2 (n - 1) S^2, else 2;
+ *   per member: z = std > 0 ? (float)(((double)x - mean) / std) : 0,
+ *   flags bit0 (evaluated) and bit1 (straggler: z > z_pm / 1000, decided as
+ *   n x > S and (n x - S)^2 (n - 1) 10^6 > z_pm^2 n D);
+ *   n_strag = number of bit1 members.
+ * Groups that are not evaluated report n (their present ranks), cls = 0xFF
+ * and zeros. Every other cell gets z = 0, flags = 0.
+ */
+typedef struct argus_l2_params {
+  int32_t min_group;    /* >= 2, default 3 */
+  int32_t cv_mild_pm;   /* 0 .. 10^6, default 20 (CV 0.02) */
+  int32_t cv_severe_pm; /* 0 .. 10^6, default 50 (CV 0.05) */
+  int32_t z_pm;         /* 0 .. 10^6, default 3000 (z > 3) */
+} argus_l2_params_t;
+
+typedef struct argus_groups {
+  const uint8_t* route;     /* [n_events] dimension of each event (device) */
+  const int32_t* group_off; /* [n_dims][max_groups + 1] (device) */
+  const int32_t* members;   /* [n_dims][n_ranks] (device) */
+  int32_t n_dims;           /* 1 .. ARGUS_MAX_L2_DIMS */
+  int32_t max_groups;       /* 1 .. 65535, max_groups * n_ranks < 2^32 */
+} argus_groups_t;
+
+typedef struct argus_l2_out {
+  /* per (step, event, group), [n_steps][n_events][max_groups] */
+  uint32_t* n;
+  double* mean_ns;
+  double* std_ns;
+  double* cv;
+  uint8_t* cls;
+  uint32_t* n_strag;
+  /* per cell, [n_ranks][n_steps][n_events] */
+  float* z;
+  uint8_t* flags;
+  int32_t* dev_status; /* optional (may be NULL) */
+} argus_l2_out_t;
+
+void argus_l2_default(argus_l2_params_t* p);
+
+/* Workspace bytes: 4 * n_dims * n_ranks (each rank's first listing). */
+size_t argus_l2_workspace(int32_t n_ranks, int32_t n_dims);
+
+/* count and sum_ns: argus_summarize outputs ([n_ranks][n_steps][n_events]).
+ * n_steps * n_dims <= 65535. The workspace must be 4-byte aligned and not
+ * shared by calls that may overlap. */
+int argus_l2(const uint32_t* count, const int64_t* sum_ns, int32_t n_ranks, int32_t n_steps, int32_t n_events,
+             const argus_groups_t* groups, const argus_l2_params_t* params, const argus_l2_out_t* out,
+             void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -21,6 +21,8 @@ XR_DEFAULTS = dict(min_ranks=3, c_min_pair=8, min_kernels=8, k_mad_pm=5189, rati
 L1_DEFAULTS = dict(W=5, theta_pm=1500, beta_pm=1200, rho_pm=1300, cmax_pm=100, min_seg=2)
 KDE_DEFAULTS = dict(sub_bits=6, frac_pm=50, min_count=3, gap=48)
 W1_DEFAULTS = dict(grid=64, min_ranks=3, alpha_pm=1500)
+L2_DEFAULTS = dict(min_group=3, cv_mild_pm=20, cv_severe_pm=50, z_pm=3000)
+L2_NOT_EVALUATED = 0xFF
 KDE_MAXC = 4
 
 _lib = None
@@ -51,6 +53,8 @@ def lib():
         L.orc_w1.restype = ctypes.c_int
         L.orc_w1_cdf_q.argtypes = [I32, V, V, V, ctypes.c_double]
         L.orc_w1_cdf_q.restype = ctypes.c_uint32
+        L.orc_l2.argtypes = [I32, I32, I32] + [V] * 5 + [I32] * 6 + [V] * 8
+        L.orc_l2.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -227,3 +231,30 @@ def w1_cdf_q(count, p50, p99, x: float) -> int:
     a = np.ascontiguousarray(p50, dtype=np.int64)
     b = np.ascontiguousarray(p99, dtype=np.int64)
     return lib().orc_w1_cdf_q(len(cnt), _p(cnt), _p(a), _p(b), x)
+
+
+def l2(count, sum_ns, R: int, S: int, E: int, route, group_off, members, **params) -> dict:
+    """Group-aware L2 comparison (CV classes, z-scores, straggler flags) of
+    per-(rank, step, event) summaries. route: [E] uint8 dimension per event
+    (0xFF: not compared); group_off: [n_dims][max_groups + 1] int32 offsets
+    into members: [n_dims][R] int32. 'status': bit 1 malformed groups, 2
+    duplicate listings, 4 values out of the 2^40 ns domain."""
+    p = dict(L2_DEFAULTS, **params)
+    cnt = np.ascontiguousarray(count, dtype=np.uint32).reshape(-1)
+    sm = np.ascontiguousarray(sum_ns, dtype=np.int64).reshape(-1)
+    rt = np.ascontiguousarray(route, dtype=np.uint8).reshape(-1)
+    off = np.ascontiguousarray(group_off, dtype=np.int32)
+    mem = np.ascontiguousarray(members, dtype=np.int32)
+    n_dims = off.shape[0] if off.ndim == 2 else 0
+    max_groups = off.shape[1] - 1 if off.ndim == 2 else 0
+    assert cnt.size == sm.size == R * S * E and rt.size == E and mem.size == n_dims * R
+    GO = S * E * max_groups
+    out = {"n": np.empty(GO, np.uint32), "mean_ns": np.empty(GO, np.float64), "std_ns": np.empty(GO, np.float64),
+           "cv": np.empty(GO, np.float64), "cls": np.empty(GO, np.uint8), "n_strag": np.empty(GO, np.uint32),
+           "z": np.empty(R * S * E, np.float32), "flags": np.empty(R * S * E, np.uint8)}
+    st = lib().orc_l2(R, S, E, _p(cnt), _p(sm), _p(rt), _p(off) if off.size else None,
+                      _p(mem) if mem.size else None, n_dims, max_groups, p["min_group"], p["cv_mild_pm"],
+                      p["cv_severe_pm"], p["z_pm"],
+                      *[_p(out[k]) for k in ("n", "mean_ns", "std_ns", "cv", "cls", "n_strag", "z", "flags")])
+    out["status"] = int(st)
+    return out

@@ -10,7 +10,7 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp"
     cmd = ["gcc", "-std=gnu11", "-O2", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
            "-Wall", "-Wextra", "-o", tmp, os.path.join(HERE, "argus_oracle.c"), os.path.join(HERE, "kde_oracle.c"),
-           os.path.join(HERE, "w1_oracle.c"), "-lm"]
+           os.path.join(HERE, "w1_oracle.c"), os.path.join(HERE, "l2_oracle.c"), "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

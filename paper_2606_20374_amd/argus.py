@@ -20,6 +20,7 @@ NBINS = 32
 
 OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
 DEV_BAD_SEGMENT, DEV_L1_DOMAIN, DEV_KDE_SUMMARY, DEV_W1_INPUT = 1, 2, 4, 8
+DEV_GROUPS_MALFORMED, DEV_GROUPS_DUPLICATE, DEV_L2_DOMAIN = 16, 32, 64
 KDE_MAXC = 4
 
 V, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
@@ -77,6 +78,21 @@ class W1Out(ctypes.Structure):
     _fields_ = [(f, V) for f in W1_FIELDS]
 
 
+class L2Params(ctypes.Structure):
+    _fields_ = [(f, I32) for f in ("min_group", "cv_mild_pm", "cv_severe_pm", "z_pm")]
+
+
+class Groups(ctypes.Structure):
+    _fields_ = [("route", V), ("group_off", V), ("members", V), ("n_dims", I32), ("max_groups", I32)]
+
+
+L2_FIELDS = ["n", "mean_ns", "std_ns", "cv", "cls", "n_strag", "z", "flags", "dev_status"]
+
+
+class L2Out(ctypes.Structure):
+    _fields_ = [(f, V) for f in L2_FIELDS]
+
+
 class ArgusError(RuntimeError):
     pass
 
@@ -119,6 +135,11 @@ def lib():
         L.argus_w1_workspace.restype = ctypes.c_size_t
         L.argus_w1.argtypes = [P(KdeOut), I32, I32, I32, P(W1Params), P(W1Out), V, ctypes.c_size_t, V]
         L.argus_w1.restype = ctypes.c_int
+        L.argus_l2_default.argtypes = [P(L2Params)]
+        L.argus_l2_workspace.argtypes = [I32, I32]
+        L.argus_l2_workspace.restype = ctypes.c_size_t
+        L.argus_l2.argtypes = [V, V, I32, I32, I32, P(Groups), P(L2Params), P(L2Out), V, ctypes.c_size_t, V]
+        L.argus_l2.restype = ctypes.c_int
         if L.argus_abi_version() != 1:
             raise ArgusError("libargus ABI version mismatch")
         _lib = L
@@ -163,6 +184,12 @@ def w1_defaults() -> dict:
     p = W1Params()
     lib().argus_w1_default(ctypes.byref(p))
     return {f: getattr(p, f) for f, _ in W1Params._fields_}
+
+
+def l2_defaults() -> dict:
+    p = L2Params()
+    lib().argus_l2_default(ctypes.byref(p))
+    return {f: getattr(p, f) for f, _ in L2Params._fields_}
 
 
 def _events(ev: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: int) -> Events:
@@ -320,4 +347,36 @@ def w1(clusters: dict, n_ranks: int, n_steps: int, n_kernels: int, out: Optional
     ws = out["_workspace"]
     _check(lib().argus_w1(ctypes.byref(cl), n_ranks, n_steps, n_kernels, ctypes.byref(p), ctypes.byref(o), _ptr(ws),
                           ws.numel(), _stream(dev)), "argus_w1")
+    return out
+
+
+# ------------------------------------------------------------------------- L2
+def alloc_l2(n_ranks: int, n_steps: int, n_events: int, n_dims: int, max_groups: int, device="cuda") -> dict:
+    GO, C = n_steps * n_events * max_groups, n_ranks * n_steps * n_events
+    e = lambda n, dt: torch.empty(n, dtype=dt, device=device)  # noqa: E731
+    ws = lib().argus_l2_workspace(n_ranks, n_dims)
+    return {"n": e(GO, torch.int32), "mean_ns": e(GO, torch.float64), "std_ns": e(GO, torch.float64),
+            "cv": e(GO, torch.float64), "cls": e(GO, torch.uint8), "n_strag": e(GO, torch.int32),
+            "z": e(C, torch.float32), "flags": e(C, torch.uint8), "dev_status": e(1, torch.int32),
+            "_workspace": e(max(ws, 4), torch.uint8)}
+
+
+def l2(count: torch.Tensor, sum_ns: torch.Tensor, n_ranks: int, n_steps: int, n_events: int, route: torch.Tensor,
+       group_off: torch.Tensor, members: torch.Tensor, out: Optional[dict] = None, **params) -> dict:
+    """argus_l2: group-aware CV classes and z-score straggler flags. route
+    [n_events] uint8, group_off [n_dims][max_groups + 1] int32, members
+    [n_dims][n_ranks] int32 (device tensors)."""
+    dev = count.device
+    n_dims, max_groups = group_off.shape[0], group_off.shape[1] - 1
+    if out is None:
+        out = alloc_l2(n_ranks, n_steps, n_events, n_dims, max_groups, dev)
+    p = L2Params()
+    lib().argus_l2_default(ctypes.byref(p))
+    for k, v in params.items():
+        setattr(p, k, v)
+    g = Groups(_ptr(route), _ptr(group_off), _ptr(members), n_dims, max_groups)
+    o = L2Out(*[_ptr(out.get(f)) for f in L2_FIELDS])
+    ws = out["_workspace"]
+    _check(lib().argus_l2(_ptr(count), _ptr(sum_ns), n_ranks, n_steps, n_events, ctypes.byref(g), ctypes.byref(p),
+                          ctypes.byref(o), _ptr(ws), ws.numel(), _stream(dev)), "argus_l2")
     return out

@@ -249,4 +249,45 @@ int argus_w1(const argus_kde_out_t* clusters, int32_t n_ranks, int32_t n_steps, 
   return status_of(launch_w1(l, st));
 }
 
+void argus_l2_default(argus_l2_params_t* p) {
+  if (!p) return;
+  p->min_group = 3;
+  p->cv_mild_pm = 20;
+  p->cv_severe_pm = 50;
+  p->z_pm = 3000;
+}
+
+size_t argus_l2_workspace(int32_t n_ranks, int32_t n_dims) { return l2_workspace_bytes(n_ranks, n_dims); }
+
+int argus_l2(const uint32_t* count, const int64_t* sum_ns, int32_t n_ranks, int32_t n_steps, int32_t n_events,
+             const argus_groups_t* groups, const argus_l2_params_t* params, const argus_l2_out_t* out,
+             void* workspace, size_t workspace_bytes, void* stream) {
+  if (!count || !sum_ns || !groups || !params || !out) return ARGUS_EINVAL;
+  if (n_ranks < 1 || n_ranks > ARGUS_MAX_L2_RANKS || n_steps < 1 || n_events < 1) return ARGUS_EINVAL;
+  const argus_groups_t& g = *groups;
+  if (!g.route || !g.group_off || !g.members) return ARGUS_EINVAL;
+  if (g.n_dims < 1 || g.n_dims > ARGUS_MAX_L2_DIMS || g.max_groups < 1 || g.max_groups > 65535) return ARGUS_EINVAL;
+  if ((int64_t)g.max_groups * n_ranks >= ((int64_t)1 << 32)) return ARGUS_EINVAL;
+  if ((int64_t)n_steps * g.n_dims > 65535) return ARGUS_EINVAL;
+  const int64_t cells = (int64_t)n_ranks * n_steps * n_events;
+  if (cells > ((int64_t)1 << 40) || (int64_t)n_steps * n_events * g.max_groups > ((int64_t)1 << 40))
+    return ARGUS_EINVAL;
+  const argus_l2_params_t& p = *params;
+  if (p.min_group < 2 || p.cv_mild_pm < 0 || p.cv_mild_pm > 1000000 || p.cv_severe_pm < 0 ||
+      p.cv_severe_pm > 1000000 || p.z_pm < 0 || p.z_pm > 1000000)
+    return ARGUS_EINVAL;
+  const argus_l2_out_t& o = *out;
+  if (!o.n || !o.mean_ns || !o.std_ns || !o.cv || !o.cls || !o.n_strag || !o.z || !o.flags) return ARGUS_EINVAL;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 3u) != 0 ||
+      workspace_bytes < argus_l2_workspace(n_ranks, g.n_dims))
+    return ARGUS_EINVAL;
+  int rc = check_device();
+  if (rc != ARGUS_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  rc = status_of(launch_clear(o.dev_status, nullptr, st));
+  if (rc != ARGUS_OK) return rc;
+  L2Launch l{count, sum_ns, n_ranks, n_steps, n_events, g, p, o, workspace};
+  return status_of(launch_l2(l, st));
+}
+
 }  // extern "C"

@@ -17,6 +17,17 @@ __device__ __forceinline__ int octave_bin(uint64_t d) {
   return b < NB - 1 ? b : NB - 1;
 }
 
+// Correctly rounded conversion of an unsigned 128-bit integer to double.
+__device__ __forceinline__ double u128_to_f64(unsigned __int128 v) {
+  const uint64_t hi = (uint64_t)(v >> 64);
+  if (hi == 0) return (double)(uint64_t)v;
+  const int sh = 64 - __builtin_clzll(hi);
+  uint64_t top = (uint64_t)(v >> sh);
+  const unsigned __int128 low_mask = (((unsigned __int128)1) << sh) - 1;
+  top |= (v & low_mask) != 0 ? 1ull : 0ull;
+  return ldexp((double)top, sh);
+}
+
 template <typename T>
 __device__ __forceinline__ T lds_load(T* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -127,6 +138,18 @@ struct W1Launch {
 };
 hipError_t launch_w1(const W1Launch& a, hipStream_t st);
 size_t w1_workspace_bytes(int32_t R, int32_t S, int32_t K, int32_t G);
+
+struct L2Launch {
+  const uint32_t* count;
+  const int64_t* sum_ns;
+  int32_t R, S, E;
+  argus_groups_t g;
+  argus_l2_params_t p;
+  argus_l2_out_t o;
+  void* workspace;  // l2_workspace_bytes(R, n_dims)
+};
+hipError_t launch_l2(const L2Launch& a, hipStream_t st);
+size_t l2_workspace_bytes(int32_t R, int32_t n_dims);
 
 // Zero the optional device status word and the optional queue counter.
 hipError_t launch_clear(int32_t* dev_status, uint32_t* queue, hipStream_t st);

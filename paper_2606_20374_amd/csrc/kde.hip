@@ -115,17 +115,6 @@ __device__ __forceinline__ uint64_t grid64_lb(int b, const uint32_t* th) {
   return e >= 23 ? (m << (e - 23)) : ((m + (1ull << (23 - e)) - 1) >> (23 - e));
 }
 
-// Correctly rounded conversion of an unsigned 128-bit integer to double.
-__device__ __forceinline__ double u128_to_f64(unsigned __int128 v) {
-  const uint64_t hi = (uint64_t)(v >> 64);
-  if (hi == 0) return (double)(uint64_t)v;
-  const int sh = 64 - __builtin_clzll(hi);
-  uint64_t top = (uint64_t)(v >> sh);
-  const unsigned __int128 low_mask = (((unsigned __int128)1) << sh) - 1;
-  top |= (v & low_mask) != 0 ? 1ull : 0ull;
-  return ldexp((double)top, sh);
-}
-
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 
 __device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {

@@ -20,6 +20,8 @@ XR_INT_FIELDS = ["n_present", "med_ns", "mad_ns", "q1_ns", "q3_ns", "n_flag", "n
                  "n_eval", "n_flag_rank", "straggler"]
 XR_FLOAT_FIELDS = ["xmean_ns", "z", "mean_ns"]
 L1_INT_FIELDS = ["flags", "cls", "eff_width", "cp"]
+L2_INT_FIELDS = ["n", "cls", "n_strag", "flags"]
+L2_FLOAT_FIELDS = ["mean_ns", "std_ns", "cv", "z"]
 RTOL = 1e-5  # float32 outputs: relative tolerance
 
 

@@ -148,3 +148,39 @@ def test_w1_rejects_bad_arguments(mutate):
         mutate(c, p, o, d)
     assert pa.lib().argus_w1(ctypes.byref(c), d["R"], d["S"], d["K"], ctypes.byref(p), ctypes.byref(o), ws, n,
                              None) == A.EINVAL
+
+
+def test_l2_defaults_and_workspace():
+    assert pa.l2_defaults() == dict(min_group=3, cv_mild_pm=20, cv_severe_pm=50, z_pm=3000)
+    assert pa.lib().argus_l2_workspace(10240, 4) == 4 * 10240 * 4
+
+
+@pytest.mark.parametrize("mutate", [
+    lambda g, p, o, d: setattr(g, "n_dims", 0),
+    lambda g, p, o, d: setattr(g, "n_dims", 17),
+    lambda g, p, o, d: setattr(g, "max_groups", 0),
+    lambda g, p, o, d: setattr(g, "max_groups", 65536),
+    lambda g, p, o, d: setattr(g, "members", None),
+    lambda g, p, o, d: setattr(p, "min_group", 1),
+    lambda g, p, o, d: setattr(p, "z_pm", 1000001),
+    lambda g, p, o, d: setattr(p, "cv_mild_pm", -1),
+    lambda g, p, o, d: setattr(o, "cls", None),
+    lambda g, p, o, d: d.__setitem__("R", 65537),
+    lambda g, p, o, d: d.__setitem__("S", 65535),  # S * n_dims over the launch limit
+    "misaligned", "small",
+])
+def test_l2_rejects_bad_arguments(mutate):
+    g = A.Groups(0x1000, 0x1000, 0x1000, 2, 4)
+    p = A.L2Params()
+    pa.lib().argus_l2_default(ctypes.byref(p))
+    o = A.L2Out(*([0x1000] * 8 + [None]))
+    d = {"R": 8, "S": 2, "K": 4}
+    ws, n = 0x10000, 1 << 20
+    if mutate == "misaligned":
+        ws = 0x10002
+    elif mutate == "small":
+        n = 4 * 8 * 2 - 1
+    else:
+        mutate(g, p, o, d)
+    assert pa.lib().argus_l2(0x1000, 0x1000, d["R"], d["S"], d["K"], ctypes.byref(g), ctypes.byref(p),
+                             ctypes.byref(o), ws, n, None) == A.EINVAL

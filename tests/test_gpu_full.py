@@ -6,7 +6,8 @@ The oracle regenerates every segment on the host and summarizes it with the
 unmodified single-threaded code on disjoint chunks in parallel; its
 summaries (never the GPU's) feed the oracle's cross-rank and L1 steps.
 Everything is compared element by element; float32 fields within 1e-5
-relative. Planted faults must be recovered exactly.
+relative. Planted faults must be recovered exactly. The group-aware L2 step
+runs over the same summaries with the workload's parallel layout.
 """
 import gc
 
@@ -74,6 +75,18 @@ def _full_parity(name: str, chunk_segments: int = 512):
         assert {(int(r), int(k)) for r, k in zip(*np.nonzero(flags[:, t, :] & 8))} == truth["pairs"]
     l1 = w["flags"].cpu().numpy().reshape(R, S)
     assert {(int(r), int(t)) for r, t in zip(*np.nonzero(l1 & 2))} == truth["anomalous"]
+
+    # group-aware L2 over the workload's parallel layout, same summaries
+    route, off, mem = tracegen.workload_groups(name, R, K)
+    t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a.astype(dt))).to(DEV)  # noqa: E731
+    g2 = pa.l2(s["count"], s["sum_ns"], R, S, K, t(route, np.uint8), t(off, np.int32), t(mem, np.int32))
+    torch.cuda.synchronize()
+    assert int(g2["dev_status"].item()) == 0
+    o2 = oracle.l2(so["count"], so["sum_ns"], R, S, K, route, off, mem)
+    assert o2["status"] == 0
+    P.assert_int_equal(g2, o2, P.L2_INT_FIELDS, name + " l2")
+    P.assert_float_close(g2, o2, P.L2_FLOAT_FIELDS, name + " l2")
+    del g2, o2
     del s, x, w
     gc.collect()
     torch.cuda.empty_cache()

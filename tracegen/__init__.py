@@ -390,3 +390,56 @@ class Trace:
 
 def make(name: str, seg_lengths=None, **overrides) -> Trace:
     return Trace(config(name, **overrides), seg_lengths=seg_lengths)
+
+
+# ---------------------------------------------------------------------------
+# Parallelism groups and the event routing table (inputs of the L2 step).
+# Ranks follow the usual tensor-major layout r = t + TP (p + PP d) with
+# tensor index t, pipeline stage p and data-parallel index d; expert-parallel
+# groups split each data-parallel group into chunks of EP consecutive d.
+DIMS = ("tp", "pp", "dp", "ep")
+
+
+def parallel_groups(n_ranks: int, tp: int, pp: int, ep: int = 1):
+    """Group lists of the four parallelism dimensions: (group_off
+    [4][max_groups + 1] int32, members [4][n_ranks] int32, n_groups [4])."""
+    assert n_ranks % (tp * pp) == 0
+    dp = n_ranks // (tp * pp)
+    assert dp % ep == 0
+    r = np.arange(n_ranks)
+    t, p, d = r % tp, (r // tp) % pp, r // (tp * pp)
+    keys = [d * pp + p,                      # TP group: ranks sharing (p, d)
+            d * tp + t,                      # PP group: ranks sharing (t, d)
+            p * tp + t,                      # DP group: ranks sharing (t, p)
+            ((d // ep) * pp + p) * tp + t]   # EP group: (t, p) and a chunk of ep consecutive d
+    n_groups = [n_ranks // tp, n_ranks // pp, tp * pp, n_ranks // ep]
+    G = max(n_groups)
+    off = np.zeros((4, G + 1), np.int32)
+    mem = np.zeros((4, n_ranks), np.int32)
+    for i, key in enumerate(keys):
+        order = np.argsort(key, kind="stable")
+        mem[i] = order
+        cnt = np.bincount(key, minlength=G)
+        off[i, 1:] = np.cumsum(cnt)
+    return off, mem, n_groups
+
+
+def event_routes(n_events: int, seed: int = 0, shares=(150, 100, 500, 250)) -> np.ndarray:
+    """A seeded routing table: each event id is compared in one dimension
+    (TP, PP, DP, EP), drawn with the given permille shares."""
+    rng = np.random.default_rng([seed, 0x12A7])
+    w = np.asarray(shares, np.float64)
+    return rng.choice(4, size=n_events, p=w / w.sum()).astype(np.uint8)
+
+
+# Parallel layout (tensor, pipeline, expert degrees) of each workload; the
+# data-parallel degree is what remains of the rank count.
+LAYOUTS = {"tiny": (2, 2, 2), "medium": (2, 4, 4), "production": (8, 4, 8), "cluster": (8, 8, 8),
+           "skew": (8, 4, 8)}
+
+
+def workload_groups(name: str, n_ranks: int, n_events: int, seed: int = 0):
+    """(route, group_off, members) of a workload's parallel layout."""
+    tp, pp, ep = LAYOUTS[name]
+    off, mem, _ = parallel_groups(n_ranks, tp, pp, ep)
+    return event_routes(n_events, seed), off, mem
