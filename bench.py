@@ -115,6 +115,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kde-reps", type=int, default=5, help="timed argus_kde calls (0: skip the KDE and W1 legs)")
     ap.add_argument("--w1-reps", type=int, default=5, help="timed argus_w1 calls (0: skip the W1 leg)")
+    ap.add_argument("--l2-reps", type=int, default=5, help="timed argus_l2 calls (0: skip the L2 leg)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -241,6 +242,37 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     result["iter_windows_10240x1000_ms"] = e0.elapsed_time(e1) / 5
+
+    if args.l2_reps > 0:
+        # group-aware L2 (section 6.1 routing, Appendix B) over the step's
+        # summaries, with the workload's TP / PP / DP / EP layout
+        route, goff, gmem = tracegen.workload_groups(args.config, R, K)
+        tt = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a.astype(dt))).to(dev)  # noqa: E731
+        route_d, goff_d, gmem_d = tt(route, np.uint8), tt(goff, np.int32), tt(gmem, np.int32)
+        l2_out = pa.alloc_l2(R, S, K, goff.shape[0], goff.shape[1] - 1, dev)
+        pa.l2(s["count"], s["sum_ns"], R, S, K, route_d, goff_d, gmem_d, out=l2_out)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.l2_reps):
+            pa.l2(s["count"], s["sum_ns"], R, S, K, route_d, goff_d, gmem_d, out=l2_out)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        l2_ms = e0.elapsed_time(e1) / args.l2_reps
+        assert int(l2_out["dev_status"].item()) == 0
+        lf = l2_out["flags"].cpu().numpy().reshape(R, S, K)
+        cls = l2_out["cls"].cpu().numpy()
+        strag = sorted(truth["stragglers"])
+        others = np.setdiff1d(np.arange(R), strag)
+        ev_cells = (lf & 1) > 0
+        result["l2"] = {
+            "ms": l2_ms, "ms_per_step": l2_ms / S, "layout_tp_pp_ep": list(tracegen.LAYOUTS[args.config]),
+            "groups_evaluated": int((cls != 0xFF).sum()),
+            "groups_by_class": [int((cls == c).sum()) for c in (0, 1, 2)],
+            "straggler_cells_flagged_frac": float(((lf[strag] & 2) > 0).sum() / max(1, ev_cells[strag].sum())),
+            "other_cells_flagged_frac": float(((lf[others] & 2) > 0).sum() / max(1, ev_cells[others].sum())),
+        }
+        del l2_out
+        torch.cuda.empty_cache()
 
     if args.kde_reps > 0:
         # KDE valley clustering of every (rank, step, kernel) group (section
