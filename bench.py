@@ -116,6 +116,7 @@ def main():
     ap.add_argument("--kde-reps", type=int, default=5, help="timed argus_kde calls (0: skip the KDE and W1 legs)")
     ap.add_argument("--w1-reps", type=int, default=5, help="timed argus_w1 calls (0: skip the W1 leg)")
     ap.add_argument("--l2-reps", type=int, default=5, help="timed argus_l2 calls (0: skip the L2 leg)")
+    ap.add_argument("--compact-reps", type=int, default=5, help="timed argus_compact calls (0: skip that leg)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -242,6 +243,33 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     result["iter_windows_10240x1000_ms"] = e0.elapsed_time(e1) / 5
+
+    if args.compact_reps > 0:
+        # the uploaded record stream of the step's summaries (section 5.2,
+        # sizes of section 8.3): sized once, then timed into a preallocated
+        # buffer
+        comp = pa.compact(s, R, S, K, 0)
+        total = int(comp["seg_byte_off"][-1].item())
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.compact_reps):
+            pa.compact(s, R, S, K, 0, out=comp["bytes"])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        c_ms = e0.elapsed_time(e1) / args.compact_reps
+        assert int(comp["dev_status"].item()) == 0
+        # read: count of every cell, hist of the present ones, sum / min /
+        # max of the present ones (twice: sizing and writing); written: the
+        # records and the segment offsets
+        c_bytes = 4 * G * K * 2 + present * (128 * 2 + 24) + total + 16 * G
+        result["compact"] = {
+            "ms": c_ms, "bytes": total, "bytes_per_rank_step": total / G,
+            "raw_bytes_per_rank_step": 24 * trace.n_events / G,
+            "compression_ratio": 24 * trace.n_events / max(1, total),
+            "algorithmic_bytes": c_bytes, "achieved_GBps": c_bytes / (c_ms * 1e-3) / 1e9,
+        }
+        del comp
+        torch.cuda.empty_cache()
 
     if args.l2_reps > 0:
         # group-aware L2 (section 6.1 routing, Appendix B) over the step's

@@ -94,7 +94,8 @@ enum {
                                       a member id outside [0, n_ranks) (member skipped) */
   ARGUS_DEV_GROUPS_DUPLICATE = 32, /* argus_l2: a rank listed more than once in one dimension (only its first
                                       listing counts) */
-  ARGUS_DEV_L2_DOMAIN = 64         /* argus_l2: a mean duration at or above 2^40 ns (that cell is left out) */
+  ARGUS_DEV_L2_DOMAIN = 64,        /* argus_l2: a mean duration at or above 2^40 ns (that cell is left out) */
+  ARGUS_DEV_COMPACT_CAPACITY = 128 /* argus_compact: the records did not all fit in the caller's buffer */
 };
 
 int argus_abi_version(void);
@@ -155,6 +156,41 @@ size_t argus_summarize_workspace(const argus_events_t* ev);
  * must be 16-byte aligned. workspace: see argus_summarize_workspace. */
 int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* workspace, size_t workspace_bytes,
                     void* stream);
+
+/* As argus_summarize, but cells are keyed by (kernel id, stream), the
+ * grouping key of section 5.2: cells are [n_ranks][n_steps][n_kernels]
+ * [n_streams] (cell index (g * n_kernels + kernel_id) * n_streams + stream),
+ * n_kernels * n_streams <= ARGUS_MAX_KERNELS. Per-segment outputs and
+ * wire_bytes are as for argus_summarize. */
+int argus_summarize_keyed(const argus_events_t* ev, const argus_summary_t* out, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------ compact
+ *
+ * The uploaded summary (section 5.2: only compact statistics leave the host;
+ * section 8.3 compares their size with the raw trace): the present cells
+ * (count >= 1) of dense summaries, every segment in order and every cell in
+ * key order, as little-endian records
+ *   key u32    the kernel id; with (kernel, stream) keys kid | stream << 24
+ *   count u32, sum i64, min i64, max i64
+ *   nnz u8     number of nonzero octave bins
+ *   nnz x (bin u8, count u32) in ascending bin order
+ * i.e. 33 + 5 nnz bytes (the wire_bytes of argus_summarize, per segment).
+ * seg_byte_off[g] is the first byte of segment g and seg_byte_off[n_seg]
+ * the total, whatever the capacity; a record is written only if it lies
+ * entirely inside out[0, capacity) (else ARGUS_DEV_COMPACT_CAPACITY), so a
+ * call with capacity 0 only sizes the stream. Placement is deterministic.
+ */
+size_t argus_compact_workspace(int32_t n_ranks, int32_t n_steps);
+
+/* sum: count, sum_ns, min_ns, max_ns and hist (16-byte aligned) of an
+ * argus_summarize (n_streams = 0, n_cells = n_kernels) or
+ * argus_summarize_keyed (n_streams = NS, n_cells = n_kernels * NS) output.
+ * seg_byte_off: [n_ranks * n_steps + 1]. out may be NULL when capacity = 0.
+ * The workspace must be 8-byte aligned. */
+int argus_compact(const argus_summary_t* sum, int32_t n_ranks, int32_t n_steps, int32_t n_cells, int32_t n_streams,
+                  uint8_t* out, int64_t capacity, int64_t* seg_byte_off, int32_t* dev_status, void* workspace,
+                  size_t workspace_bytes, void* stream);
 
 /* --------------------------------------------------------------- cross-rank
  *

@@ -39,6 +39,10 @@ def lib():
         L.orc_bin.restype = ctypes.c_int
         L.orc_summarize.argtypes = [I64, I32, I32, I64] + [V] * 5 + [V] * 5 + [V] * 8
         L.orc_summarize.restype = I64
+        L.orc_summarize_keyed.argtypes = [I64, I32, I32, I64] + [V] * 5 + [V] * 5 + [V] * 8
+        L.orc_summarize_keyed.restype = I64
+        L.orc_compact.argtypes = [I64, I64, I32] + [V] * 5 + [V, I64, V]
+        L.orc_compact.restype = I64
         L.orc_cross_rank.argtypes = [I32, I32, I32, V, V] + [I32] * 7 + [V] * 8 + [V] * 3 + [V] * 4
         L.orc_cross_rank.restype = ctypes.c_int
         L.orc_iter_windows.argtypes = [I32, I32, V] + [I32] * 6 + [V] * 5
@@ -68,10 +72,11 @@ def bin_of(d: int) -> int:
     return lib().orc_bin(d)
 
 
-def summarize(ev: dict, n_kernels: int, n_streams: int, n_events: int | None = None) -> dict:
-    """Exact per-(segment, kernel) group-by. ev: kernel_id, stream, start_ns,
-    end_ns, seg_off (numpy). Returns dict of numpy outputs; 'bad_segments'
-    counts malformed segments."""
+def summarize(ev: dict, n_kernels: int, n_streams: int, n_events: int | None = None, keyed: bool = False) -> dict:
+    """Exact per-(segment, kernel) group-by (keyed: per (segment, kernel,
+    stream), cells [G][K][NS]). ev: kernel_id, stream, start_ns, end_ns,
+    seg_off (numpy). Returns dict of numpy outputs; 'bad_segments' counts
+    malformed segments."""
     kid = np.ascontiguousarray(ev["kernel_id"], dtype=np.int32)
     st = np.ascontiguousarray(ev["stream"], dtype=np.int32)
     t0 = np.ascontiguousarray(ev["start_ns"], dtype=np.int64)
@@ -79,24 +84,41 @@ def summarize(ev: dict, n_kernels: int, n_streams: int, n_events: int | None = N
     off = np.ascontiguousarray(ev["seg_off"], dtype=np.int64)
     G = len(off) - 1
     K, NS = n_kernels, n_streams
+    KC = K * NS if keyed else K
     n = len(kid) if n_events is None else n_events
     out = {
-        "count": np.empty(G * K, np.uint32), "sum_ns": np.empty(G * K, np.int64),
-        "min_ns": np.empty(G * K, np.int64), "max_ns": np.empty(G * K, np.int64),
-        "hist": np.empty(G * K * NB, np.uint32),
+        "count": np.empty(G * KC, np.uint32), "sum_ns": np.empty(G * KC, np.int64),
+        "min_ns": np.empty(G * KC, np.int64), "max_ns": np.empty(G * KC, np.int64),
+        "hist": np.empty(G * KC * NB, np.uint32),
         "n_valid": np.empty(G, np.uint32), "n_invalid": np.empty(G, np.uint32),
         "t_first": np.empty(G, np.int64), "t_last": np.empty(G, np.int64), "step_ns": np.empty(G, np.int64),
         "busy_ns": np.empty(G, np.int64), "stream_busy_ns": np.empty(G * NS, np.int64),
         "wire_bytes": np.empty(G, np.int64),
     }
-    bad = lib().orc_summarize(G, K, NS, n, _p(kid), _p(st), _p(t0), _p(t1), _p(off),
+    fn = lib().orc_summarize_keyed if keyed else lib().orc_summarize
+    bad = fn(G, K, NS, n, _p(kid), _p(st), _p(t0), _p(t1), _p(off),
                               *[_p(out[k]) for k in ("count", "sum_ns", "min_ns", "max_ns", "hist", "n_valid",
                                                      "n_invalid", "t_first", "t_last", "step_ns", "busy_ns",
                                                      "stream_busy_ns", "wire_bytes")])
-    out["hist"] = out["hist"].reshape(G * K, NB)
+    out["hist"] = out["hist"].reshape(G * KC, NB)
     out["stream_busy_ns"] = out["stream_busy_ns"].reshape(G, NS)
     out["bad_segments"] = int(bad)
     return out
+
+
+def compact(summary: dict, n_seg: int, n_cells: int, n_streams: int = 0, cap: int | None = None):
+    """Record stream of dense summaries ([n_seg][n_cells] arrays): (bytes,
+    seg_byte_off [n_seg + 1]). n_streams = 0 for kernel-id keys, else the
+    stream count of (kernel, stream) keys."""
+    f = {k: np.ascontiguousarray(summary[k]).reshape(-1) for k in ("count", "sum_ns", "min_ns", "max_ns", "hist")}
+    ptrs = [_p(f[k]) for k in ("count", "sum_ns", "min_ns", "max_ns", "hist")]
+    off = np.empty(n_seg + 1, np.int64)
+    if cap is None:
+        lib().orc_compact(n_seg, n_cells, n_streams, *ptrs, None, 0, _p(off))
+        cap = int(off[-1])
+    buf = np.zeros(max(cap, 1), np.uint8)
+    total = lib().orc_compact(n_seg, n_cells, n_streams, *ptrs, _p(buf), cap, _p(off))
+    return buf[:min(total, cap)], off
 
 
 def cross_rank(count: np.ndarray, sum_ns: np.ndarray, R: int, S: int, K: int, **params) -> dict:

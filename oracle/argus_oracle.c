@@ -16,6 +16,10 @@
  *                       transform evaluated on an equally spaced grid,
  *                       per-group count and order statistics). Plain
  *                       definition: an exact group-by.
+ *   orc_summarize_keyed - the same group-by keyed by (kernel, stream).
+ *   orc_compact       - the uploaded record stream of the summaries
+ *                       (section 5.2, section 8.3 sizes). Plain definition:
+ *                       fields written out in order.
  *   orc_cross_rank    - section 6.2 (the same kernel compared across ranks,
  *                       an anomalous rank shows as an elevated row, mean
  *                       distance to the other ranks as the deviation score,
@@ -65,20 +69,21 @@ int orc_bin(uint64_t d) {
 
 /* ------------------------------------------------------------- summarize */
 
-/* Returns the number of malformed segments (treated as empty). */
-int64_t orc_summarize(int64_t n_seg, int32_t K, int32_t NS, int64_t n_events, const int32_t* kid,
-                      const int32_t* stream, const int64_t* start, const int64_t* end, const int64_t* seg_off,
-                      /* per cell [n_seg][K] */
-                      uint32_t* count, int64_t* sum_ns, int64_t* min_ns, int64_t* max_ns,
-                      uint32_t* hist /* [n_seg][K][NB] */,
-                      /* per segment [n_seg] */
-                      uint32_t* n_valid, uint32_t* n_invalid, int64_t* t_first, int64_t* t_last, int64_t* step_ns,
-                      int64_t* busy_ns, int64_t* stream_busy_ns /* [n_seg][NS] */, int64_t* wire_bytes) {
+/* The group-by of both keyings: key = kernel id (KC = K cells per segment),
+ * or key = (kernel id, stream) as kid * NS + stream (KC = K * NS, section
+ * 5.2 groups per (kernel, stream, rank)). Returns the number of malformed
+ * segments (treated as empty). */
+static int64_t summarize_impl(int keyed, int64_t n_seg, int32_t K, int32_t NS, int64_t n_events, const int32_t* kid,
+                              const int32_t* stream, const int64_t* start, const int64_t* end, const int64_t* seg_off,
+                              uint32_t* count, int64_t* sum_ns, int64_t* min_ns, int64_t* max_ns, uint32_t* hist,
+                              uint32_t* n_valid, uint32_t* n_invalid, int64_t* t_first, int64_t* t_last,
+                              int64_t* step_ns, int64_t* busy_ns, int64_t* stream_busy_ns, int64_t* wire_bytes) {
+  const int64_t KC = keyed ? (int64_t)K * NS : K;
   int64_t bad = 0;
   for (int64_t g = 0; g < n_seg; g++) {
     /* identity values for every cell and segment */
-    for (int32_t k = 0; k < K; k++) {
-      int64_t c = g * K + k;
+    for (int64_t k = 0; k < KC; k++) {
+      int64_t c = g * KC + k;
       count[c] = 0;
       sum_ns[c] = 0;
       min_ns[c] = INT64_MAX;
@@ -108,7 +113,7 @@ int64_t orc_summarize(int64_t n_seg, int32_t K, int32_t NS, int64_t n_events, co
         continue;
       }
       uint64_t d = (uint64_t)end[i] - (uint64_t)start[i];
-      int64_t c = g * K + kid[i];
+      int64_t c = g * KC + (keyed ? (int64_t)kid[i] * NS + stream[i] : kid[i]);
       count[c] += 1;
       sum_ns[c] = (int64_t)((uint64_t)sum_ns[c] + d); /* modulo 2^64 */
       if ((int64_t)d < min_ns[c]) min_ns[c] = (int64_t)d;
@@ -122,11 +127,11 @@ int64_t orc_summarize(int64_t n_seg, int32_t K, int32_t NS, int64_t n_events, co
     }
     step_ns[g] = n_valid[g] ? t_last[g] - t_first[g] : 0;
 
-    /* uploaded record size: kid 4, count 4, sum 8, min 8, max 8, nnz 1,
+    /* uploaded record size: key 4, count 4, sum 8, min 8, max 8, nnz 1,
      * then (bin u8, count u32) per nonzero bin */
     int64_t wb = 0;
-    for (int32_t k = 0; k < K; k++) {
-      int64_t c = g * K + k;
+    for (int64_t k = 0; k < KC; k++) {
+      int64_t c = g * KC + k;
       if (count[c] == 0) continue;
       int nnz = 0;
       for (int b = 0; b < NB; b++) nnz += hist[c * NB + b] != 0;
@@ -135,6 +140,77 @@ int64_t orc_summarize(int64_t n_seg, int32_t K, int32_t NS, int64_t n_events, co
     wire_bytes[g] = wb;
   }
   return bad;
+}
+
+/* Per-(rank, step, kernel id) cells [n_seg][K]. */
+int64_t orc_summarize(int64_t n_seg, int32_t K, int32_t NS, int64_t n_events, const int32_t* kid,
+                      const int32_t* stream, const int64_t* start, const int64_t* end, const int64_t* seg_off,
+                      uint32_t* count, int64_t* sum_ns, int64_t* min_ns, int64_t* max_ns, uint32_t* hist,
+                      uint32_t* n_valid, uint32_t* n_invalid, int64_t* t_first, int64_t* t_last, int64_t* step_ns,
+                      int64_t* busy_ns, int64_t* stream_busy_ns, int64_t* wire_bytes) {
+  return summarize_impl(0, n_seg, K, NS, n_events, kid, stream, start, end, seg_off, count, sum_ns, min_ns, max_ns,
+                        hist, n_valid, n_invalid, t_first, t_last, step_ns, busy_ns, stream_busy_ns, wire_bytes);
+}
+
+/* Per-(rank, step, kernel id, stream) cells [n_seg][K][NS]. */
+int64_t orc_summarize_keyed(int64_t n_seg, int32_t K, int32_t NS, int64_t n_events, const int32_t* kid,
+                            const int32_t* stream, const int64_t* start, const int64_t* end, const int64_t* seg_off,
+                            uint32_t* count, int64_t* sum_ns, int64_t* min_ns, int64_t* max_ns, uint32_t* hist,
+                            uint32_t* n_valid, uint32_t* n_invalid, int64_t* t_first, int64_t* t_last,
+                            int64_t* step_ns, int64_t* busy_ns, int64_t* stream_busy_ns, int64_t* wire_bytes) {
+  return summarize_impl(1, n_seg, K, NS, n_events, kid, stream, start, end, seg_off, count, sum_ns, min_ns, max_ns,
+                        hist, n_valid, n_invalid, t_first, t_last, step_ns, busy_ns, stream_busy_ns, wire_bytes);
+}
+
+/* -------------------------------------------------------------- compact */
+
+static uint8_t* put_le(uint8_t* p, uint64_t v, int n) {
+  for (int i = 0; i < n; i++) p[i] = (uint8_t)(v >> (8 * i));
+  return p + n;
+}
+
+/* The uploaded summary (section 5.2: only compact statistics leave the
+ * host; section 8.3 compares their size with the raw trace): for every
+ * segment in order, every present cell (count >= 1) in key order becomes one
+ * little-endian record: key u32 (the kernel id; with (kernel, stream) keys
+ * kid | stream << 24), count u32, sum i64, min i64, max i64, nnz u8, then
+ * (bin u8, count u32) for each nonzero octave bin in ascending order.
+ * KC cells per segment; NS = 0 for kernel-id keys, else the stream count of
+ * (kernel, stream) keys (KC = K NS). seg_byte_off[g] is the first byte of
+ * segment g, seg_byte_off[n_seg] the total; bytes are written only while
+ * they fit in cap. Returns the total. */
+int64_t orc_compact(int64_t n_seg, int64_t KC, int32_t NS, const uint32_t* count, const int64_t* sum_ns,
+                    const int64_t* min_ns, const int64_t* max_ns, const uint32_t* hist, uint8_t* out, int64_t cap,
+                    int64_t* seg_byte_off) {
+  int64_t pos = 0;
+  uint8_t rec[33 + 5 * NB];
+  for (int64_t g = 0; g < n_seg; g++) {
+    seg_byte_off[g] = pos;
+    for (int64_t k = 0; k < KC; k++) {
+      int64_t c = g * KC + k;
+      if (count[c] == 0) continue;
+      uint32_t key = NS > 0 ? (uint32_t)(k / NS) | ((uint32_t)(k % NS) << 24) : (uint32_t)k;
+      uint8_t* p = rec;
+      p = put_le(p, key, 4);
+      p = put_le(p, count[c], 4);
+      p = put_le(p, (uint64_t)sum_ns[c], 8);
+      p = put_le(p, (uint64_t)min_ns[c], 8);
+      p = put_le(p, (uint64_t)max_ns[c], 8);
+      uint8_t* nnz = p++;
+      *nnz = 0;
+      for (int b = 0; b < NB; b++) {
+        if (hist[c * NB + b] == 0) continue;
+        p = put_le(p, (uint64_t)b, 1);
+        p = put_le(p, hist[c * NB + b], 4);
+        (*nnz)++;
+      }
+      int64_t len = p - rec;
+      if (pos + len <= cap) memcpy(out + pos, rec, (size_t)len);
+      pos += len;
+    }
+  }
+  seg_byte_off[n_seg] = pos;
+  return pos;
 }
 
 /* ------------------------------------------------------------ cross-rank */

@@ -20,7 +20,7 @@ NBINS = 32
 
 OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
 DEV_BAD_SEGMENT, DEV_L1_DOMAIN, DEV_KDE_SUMMARY, DEV_W1_INPUT = 1, 2, 4, 8
-DEV_GROUPS_MALFORMED, DEV_GROUPS_DUPLICATE, DEV_L2_DOMAIN = 16, 32, 64
+DEV_GROUPS_MALFORMED, DEV_GROUPS_DUPLICATE, DEV_L2_DOMAIN, DEV_COMPACT_CAPACITY = 16, 32, 64, 128
 KDE_MAXC = 4
 
 V, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
@@ -115,6 +115,12 @@ def lib():
         L.argus_summarize_workspace.restype = ctypes.c_size_t
         L.argus_summarize.argtypes = [P(Events), P(Summary), V, ctypes.c_size_t, V]
         L.argus_summarize.restype = ctypes.c_int
+        L.argus_summarize_keyed.argtypes = [P(Events), P(Summary), V, ctypes.c_size_t, V]
+        L.argus_summarize_keyed.restype = ctypes.c_int
+        L.argus_compact_workspace.argtypes = [I32, I32]
+        L.argus_compact_workspace.restype = ctypes.c_size_t
+        L.argus_compact.argtypes = [P(Summary), I32, I32, I32, I32, V, I64, V, V, V, ctypes.c_size_t, V]
+        L.argus_compact.restype = ctypes.c_int
         L.argus_xr_default.argtypes = [P(XrParams)]
         L.argus_cross_rank_workspace.argtypes = [I32, I32, I32]
         L.argus_cross_rank_workspace.restype = ctypes.c_size_t
@@ -212,20 +218,49 @@ def alloc_summary(n_ranks: int, n_steps: int, n_kernels: int, n_streams: int, de
 
 
 def summarize(ev: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: int,
-              out: Optional[dict] = None) -> dict:
-    """argus_summarize over SoA device tensors ev = {kernel_id, stream,
-    start_ns, end_ns, seg_off}. Unsigned outputs are returned in signed
-    torch dtypes of the same width (reinterpret with .view on the host)."""
+              out: Optional[dict] = None, keyed: bool = False) -> dict:
+    """argus_summarize (keyed: argus_summarize_keyed, cells per (kernel,
+    stream)) over SoA device tensors ev = {kernel_id, stream, start_ns,
+    end_ns, seg_off}. Unsigned outputs are returned in signed torch dtypes of
+    the same width (reinterpret with .view on the host)."""
     dev = ev["kernel_id"].device
     if out is None:
-        out = alloc_summary(n_ranks, n_steps, n_kernels, n_streams, dev)
+        out = alloc_summary(n_ranks, n_steps, n_kernels * (n_streams if keyed else 1), n_streams, dev)
     e = _events(ev, n_ranks, n_steps, n_kernels, n_streams)
     s = Summary(*[_ptr(out.get(f)) for f in SUMMARY_FIELDS])
     ws = out["_workspace"]
     assert ws.numel() >= lib().argus_summarize_workspace(ctypes.byref(e))
-    _check(lib().argus_summarize(ctypes.byref(e), ctypes.byref(s), _ptr(ws), ws.numel(), _stream(dev)),
-           "argus_summarize")
+    fn = lib().argus_summarize_keyed if keyed else lib().argus_summarize
+    _check(fn(ctypes.byref(e), ctypes.byref(s), _ptr(ws), ws.numel(), _stream(dev)), "argus_summarize")
     return out
+
+
+def compact(summary: dict, n_ranks: int, n_steps: int, n_cells: int, n_streams: int = 0,
+            capacity: Optional[int] = None, out: Optional[torch.Tensor] = None) -> dict:
+    """argus_compact: the record stream of a dense summary (n_streams = 0 for
+    kernel-id keys, else the stream count of (kernel, stream) keys). With no
+    capacity the stream is sized by a first call (one host synchronisation)."""
+    dev = summary["count"].device
+    G = n_ranks * n_steps
+    seg = torch.empty(G + 1, dtype=torch.int64, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(lib().argus_compact_workspace(n_ranks, n_steps), 8), dtype=torch.uint8, device=dev)
+    sm = Summary(*[_ptr(summary.get(f)) if f in ("count", "sum_ns", "min_ns", "max_ns", "hist") else None
+                   for f in SUMMARY_FIELDS])
+
+    def call(buf, cap):
+        _check(lib().argus_compact(ctypes.byref(sm), n_ranks, n_steps, n_cells, n_streams,
+                                   None if buf is None else _ptr(buf), cap, _ptr(seg), _ptr(status), _ptr(ws),
+                                   ws.numel(), _stream(dev)), "argus_compact")
+
+    if out is None:
+        if capacity is None:
+            call(None, 0)
+            capacity = int(seg[-1].item())
+        out = torch.empty(max(capacity, 1), dtype=torch.uint8, device=dev)
+    cap = out.numel() if capacity is None else capacity
+    call(out, cap)
+    return {"bytes": out, "seg_byte_off": seg, "dev_status": status, "capacity": cap}
 
 
 # ----------------------------------------------------------------- cross-rank

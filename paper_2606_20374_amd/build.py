@@ -7,7 +7,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libargus.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["api.hip", "summarize.hip", "cross_rank.hip", "iter_windows.hip", "kde.hip", "w1.hip", "l2.hip"]
+SOURCES = ["api.hip", "summarize.hip", "cross_rank.hip", "iter_windows.hip", "kde.hip", "w1.hip", "l2.hip", "compact.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HIP_FLAGS = [

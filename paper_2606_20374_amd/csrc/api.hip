@@ -64,14 +64,15 @@ size_t argus_summarize_workspace(const argus_events_t* ev) {
   return kSummarizeWorkspace;
 }
 
-int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* workspace, size_t workspace_bytes,
-                    void* stream) {
+static int summarize_impl(const argus_events_t* ev, const argus_summary_t* out, void* workspace, size_t workspace_bytes,
+                   void* stream, bool keyed) {
   if (!ev || !out) return ARGUS_EINVAL;
   if (!workspace || workspace_bytes < kSummarizeWorkspace) return ARGUS_EINVAL;
   if ((reinterpret_cast<uintptr_t>(workspace) & 3u) != 0) return ARGUS_EINVAL;
   if (ev->n_ranks < 0 || ev->n_steps < 0 || ev->n_events < 0) return ARGUS_EINVAL;
   if (ev->n_kernels < 1 || ev->n_kernels > ARGUS_MAX_KERNELS) return ARGUS_EINVAL;
   if (ev->n_streams < 1 || ev->n_streams > ARGUS_MAX_STREAMS) return ARGUS_EINVAL;
+  if (keyed && (int64_t)ev->n_kernels * ev->n_streams > ARGUS_MAX_KERNELS) return ARGUS_EINVAL;
   const int64_t n_seg = (int64_t)ev->n_ranks * ev->n_steps;
   if (n_seg > INT32_MAX) return ARGUS_EINVAL;
   if (!ev->seg_off) return ARGUS_EINVAL;
@@ -87,10 +88,20 @@ int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* 
   rc = status_of(launch_clear(out->dev_status, queue, st));
   if (rc != ARGUS_OK) return rc;
   SummarizeLaunch l{ev->kernel_id, ev->stream, ev->start_ns, ev->end_ns, ev->seg_off, ev->n_events, (int32_t)n_seg,
-                    ev->n_kernels, ev->n_streams, out->count, out->sum_ns, out->min_ns, out->max_ns, out->hist,
-                    out->n_valid, out->n_invalid, out->t_first, out->t_last, out->step_ns, out->busy_ns,
+                    ev->n_kernels, ev->n_streams, keyed ? 1 : 0, out->count, out->sum_ns, out->min_ns, out->max_ns,
+                    out->hist, out->n_valid, out->n_invalid, out->t_first, out->t_last, out->step_ns, out->busy_ns,
                     out->stream_busy_ns, out->wire_bytes, out->dev_status, queue};
   return status_of(launch_summarize(l, st));
+}
+
+int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* workspace, size_t workspace_bytes,
+                    void* stream) {
+  return summarize_impl(ev, out, workspace, workspace_bytes, stream, false);
+}
+
+int argus_summarize_keyed(const argus_events_t* ev, const argus_summary_t* out, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  return summarize_impl(ev, out, workspace, workspace_bytes, stream, true);
 }
 
 void argus_xr_default(argus_xr_params_t* p) {
@@ -288,6 +299,36 @@ int argus_l2(const uint32_t* count, const int64_t* sum_ns, int32_t n_ranks, int3
   if (rc != ARGUS_OK) return rc;
   L2Launch l{count, sum_ns, n_ranks, n_steps, n_events, g, p, o, workspace};
   return status_of(launch_l2(l, st));
+}
+
+size_t argus_compact_workspace(int32_t n_ranks, int32_t n_steps) {
+  if (n_ranks < 0 || n_steps < 0) return 0;
+  return (size_t)n_ranks * (size_t)n_steps * sizeof(int64_t);
+}
+
+int argus_compact(const argus_summary_t* sum, int32_t n_ranks, int32_t n_steps, int32_t n_cells, int32_t n_streams,
+                  uint8_t* out, int64_t capacity, int64_t* seg_byte_off, int32_t* dev_status, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  if (!sum || !seg_byte_off) return ARGUS_EINVAL;
+  if (n_ranks < 0 || n_steps < 0 || n_cells < 1 || n_streams < 0 || n_streams > ARGUS_MAX_STREAMS) return ARGUS_EINVAL;
+  if (n_streams > 0 && (n_cells % n_streams != 0 || n_cells / n_streams > (1 << 24))) return ARGUS_EINVAL;
+  if (n_streams == 0 && n_cells > (1 << 24)) return ARGUS_EINVAL;
+  const int64_t n_seg = (int64_t)n_ranks * n_steps;
+  if (n_seg > INT32_MAX) return ARGUS_EINVAL;
+  if (capacity < 0 || (capacity > 0 && !out)) return ARGUS_EINVAL;
+  if (n_seg > 0 && (!sum->count || !sum->sum_ns || !sum->min_ns || !sum->max_ns || !sum->hist)) return ARGUS_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(sum->hist) & 15u) != 0) return ARGUS_EINVAL;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 7u) != 0 ||
+      workspace_bytes < argus_compact_workspace(n_ranks, n_steps))
+    return ARGUS_EINVAL;
+  int rc = check_device();
+  if (rc != ARGUS_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  rc = status_of(launch_clear(dev_status, nullptr, st));
+  if (rc != ARGUS_OK) return rc;
+  CompactLaunch l{sum->count, sum->sum_ns, sum->min_ns, sum->max_ns, sum->hist, (int32_t)n_seg, n_cells, n_streams,
+                  out, capacity, seg_byte_off, dev_status, static_cast<int64_t*>(workspace)};
+  return status_of(launch_compact(l, st));
 }
 
 }  // extern "C"

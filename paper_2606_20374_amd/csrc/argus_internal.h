@@ -67,6 +67,7 @@ struct SummarizeLaunch {
   const int64_t* seg_off;
   int64_t n_events;
   int32_t n_seg, n_kernels, n_streams;
+  int32_t keyed;  // cells keyed by (kernel id, stream): [n_seg][n_kernels][n_streams]
   uint32_t* count;
   int64_t* sum_ns;
   int64_t* min_ns;
@@ -150,6 +151,21 @@ struct L2Launch {
 };
 hipError_t launch_l2(const L2Launch& a, hipStream_t st);
 size_t l2_workspace_bytes(int32_t R, int32_t n_dims);
+
+struct CompactLaunch {
+  const uint32_t* count;
+  const int64_t* sum_ns;
+  const int64_t* min_ns;
+  const int64_t* max_ns;
+  const uint32_t* hist;
+  int32_t n_seg, n_cells, n_streams;
+  uint8_t* out;
+  int64_t capacity;
+  int64_t* seg_byte_off;
+  int32_t* dev_status;
+  int64_t* sizes;  // workspace [n_seg]
+};
+hipError_t launch_compact(const CompactLaunch& a, hipStream_t st);
 
 // Zero the optional device status word and the optional queue counter.
 hipError_t launch_clear(int32_t* dev_status, uint32_t* queue, hipStream_t st);

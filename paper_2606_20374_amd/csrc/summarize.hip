@@ -17,9 +17,11 @@
 //   bins also hold kernels whose positions run at 1x, 3x and 9x). Bins
 //   outside the window go to a small pool of full 32-bin records that a
 //   kernel claims on first need.
-// * Kernel ids map to LDS slots directly when the id space fits (dense), or
-//   through an LDS id->slot map that hands out slots on first sight
-//   (mapped), so a large, sparse id space still takes one pass.
+// * Keys (kernel ids, or (kernel id, stream) pairs as id * n_streams +
+//   stream: section 5.2 groups per kernel and stream) map to LDS slots
+//   directly when the key space fits (dense), or through an LDS key->slot
+//   map that hands out slots on first sight (mapped), so a large, sparse key
+//   space takes one pass per 16,384 keys.
 // * Whenever the pool or the slots run out, the kernels concerned are
 //   marked and redone exactly in another pass over the segment: the result
 //   is exact for every input; typical traces need one pass.
@@ -77,6 +79,8 @@ struct Args {
   const int64_t* seg_off;
   int64_t n_events;
   int32_t n_kernels, n_streams;
+  int32_t key_ns;  // 0: cells keyed by kernel id; else n_streams: keyed by (kernel id, stream)
+  int32_t n_keys;  // cells per segment: n_kernels, or n_kernels * n_streams
   int32_t vec_ok;  // event arrays 16-byte aligned: vector loads allowed
   int32_t n_seg;
   uint32_t* queue;  // next segment to take (zeroed before the launch)
@@ -247,7 +251,8 @@ __device__ __forceinline__ void process4(Seg<NSLOT, WIN, MAPPED>& sg, const Args
         ni++;
       }
     }
-    lk[j] = valid && (unsigned)(kid[j] - kb) < (unsigned)nk ? kid[j] - kb : -1;
+    const uint32_t key = a.key_ns ? (uint32_t)kid[j] * (uint32_t)a.key_ns + (uint32_t)st[j] : (uint32_t)kid[j];
+    lk[j] = valid && key - (uint32_t)kb < (uint32_t)nk ? (int)(key - (uint32_t)kb) : -1;
   }
   // per-kernel updates two events at a time: their LDS lookups are issued
   // together, and the live register set stays small enough that nothing
@@ -288,7 +293,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
   __shared__ int64_t g_next;
   Seg<NSLOT, WIN, MAPPED> sg{sm};
   const int tid = threadIdx.x;
-  const int32_t K = a.n_kernels, NS = a.n_streams;
+  const int32_t K = a.n_keys, NS = a.n_streams;
 
   // Persistent workgroups pull segments from a queue, so the output stores
   // of one segment drain while the loads of the next are already in flight.
@@ -578,14 +583,15 @@ __global__ __launch_bounds__(256) void identity_fill_kernel(uint32_t* count, int
 hipError_t launch_summarize(const SummarizeLaunch& l, hipStream_t st) {
   const int32_t vec_ok =
       aligned16(l.kernel_id) && aligned16(l.stream) && aligned16(l.start_ns) && aligned16(l.end_ns) ? 1 : 0;
-  Args a{l.kernel_id, l.stream, l.start_ns, l.end_ns, l.seg_off, l.n_events, l.n_kernels, l.n_streams, vec_ok,
-         l.n_seg, l.queue, l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist, l.n_valid, l.n_invalid, l.t_first, l.t_last,
+  const int32_t n_keys = l.keyed ? l.n_kernels * l.n_streams : l.n_kernels;
+  Args a{l.kernel_id, l.stream, l.start_ns, l.end_ns, l.seg_off, l.n_events, l.n_kernels, l.n_streams,
+         l.keyed ? l.n_streams : 0, n_keys, vec_ok, l.n_seg, l.queue, l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist, l.n_valid, l.n_invalid, l.t_first, l.t_last,
          l.step_ns, l.busy_ns, l.stream_busy_ns, l.wire_bytes, l.dev_status};
   if (l.n_seg == 0) return hipSuccess;
-  if (l.n_kernels <= 64) return launch_t<64, 10, false>(a, l.n_seg, st);
-  if (l.n_kernels <= 512) return launch_t<512, 10, false>(a, l.n_seg, st);
-  if (l.n_kernels <= 2048) return launch_t<2048, 10, false>(a, l.n_seg, st);
-  const int64_t cells = (int64_t)l.n_seg * l.n_kernels;
+  if (n_keys <= 64) return launch_t<64, 10, false>(a, l.n_seg, st);
+  if (n_keys <= 512) return launch_t<512, 10, false>(a, l.n_seg, st);
+  if (n_keys <= 2048) return launch_t<2048, 10, false>(a, l.n_seg, st);
+  const int64_t cells = (int64_t)l.n_seg * n_keys;
   hipLaunchKernelGGL(identity_fill_kernel, dim3(4096), dim3(256), 0, st, l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist,
                      cells);
   const hipError_t e = hipGetLastError();

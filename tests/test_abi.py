@@ -184,3 +184,24 @@ def test_l2_rejects_bad_arguments(mutate):
         mutate(g, p, o, d)
     assert pa.lib().argus_l2(0x1000, 0x1000, d["R"], d["S"], d["K"], ctypes.byref(g), ctypes.byref(p),
                              ctypes.byref(o), ws, n, None) == A.EINVAL
+
+
+def test_compact_workspace_and_bad_arguments():
+    L = pa.lib()
+    assert L.argus_compact_workspace(10240, 1) == 8 * 10240
+    s = A.Summary(*([0x1000] * 12 + [None, None]))
+    ok = dict(R=4, S=2, C=6, NS=0, out=0x1000, cap=100, seg=0x2000, ws=0x3000, n=1 << 10)
+    bad = [dict(C=0), dict(NS=-1), dict(NS=65), dict(C=7, NS=2), dict(cap=-1), dict(out=None),
+           dict(seg=None), dict(ws=0x3004), dict(n=63), dict(R=-1)]
+    for b in bad:
+        a = dict(ok, **b)
+        assert L.argus_compact(ctypes.byref(s), a["R"], a["S"], a["C"], a["NS"], a["out"], a["cap"], a["seg"], None,
+                               a["ws"], a["n"], None) == A.EINVAL, b
+    s2 = A.Summary(*([0x1000] * 4 + [0x1008] + [0x1000] * 7 + [None, None]))  # misaligned histogram
+    assert L.argus_compact(ctypes.byref(s2), 4, 2, 6, 0, 0x1000, 100, 0x2000, None, 0x3000, 1 << 10, None) == A.EINVAL
+
+
+def test_summarize_keyed_rejects_large_key_space():
+    e = A.Events(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 10, 2, 2, 4097, 16)  # 4097 x 16 > 65536 keys
+    s = A.Summary(*([0x1000] * 12 + [None, None]))
+    assert pa.lib().argus_summarize_keyed(ctypes.byref(e), ctypes.byref(s), 0x2000, 256, None) == A.EINVAL
