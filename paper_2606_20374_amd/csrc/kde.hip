@@ -152,6 +152,18 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
   return v;
 }
 
+// Ordering point of the single-wavefront cell kernels. One wavefront's LDS
+// operations are performed in order, so LDS data written by some lanes is
+// visible to later reads of other lanes without waiting; the wavefront-scope
+// fences only stop the compiler from moving memory operations across this
+// point. Unlike a workgroup barrier they do not wait for outstanding global
+// loads (the next cell's prefetched durations) or stores (outputs).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 __device__ __forceinline__ void flag(const KdeArgs& a, int bit) {
   if (a.dev_status) atomicOr(a.dev_status, bit);
 }
@@ -293,12 +305,12 @@ __device__ void remove_valley(CellLds<TIER>& L, int idx, int m) {
       p = L.cpos[q + 1];
       v = L.cval[q + 1];
     }
-    __syncthreads();
+    wave_sync();
     if (q < m - 1) {
       L.cpos[q] = p;
       L.cval[q] = v;
     }
-    __syncthreads();
+    wave_sync();
   }
 }
 
@@ -344,7 +356,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
 
   // 1. grid histogram
   for (int j = l; j < G; j += kWave) cgrid[j] = 0;
-  __syncthreads();
+  wave_sync();
   bool out_of_range = false;
   if (in_regs) {
 #pragma unroll
@@ -363,7 +375,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       else out_of_range = true;
     }
   }
-  __syncthreads();
+  wave_sync();
   if (__any(out_of_range)) {  // durations outside the summarized [min, max]
     if (l == 0) flag(a, ARGUS_DEV_KDE_SUMMARY);
     write_empty(a, c);
@@ -420,7 +432,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       T = tb + cnt - 1;
       if (cnt < kWave) break;
     }
-    __syncthreads();
+    wave_sync();
     const bool sparse = nnz <= NZCAP && nnz < T;
     int carry_start = -1, carry_drop = 0;
     uint64_t prev_last = 0;
@@ -494,7 +506,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       prev_last = readlane64(fj, last);
     }
     if (m > CAND) m = CAND;  // cannot happen in tier 2: a grid of G points has < G / 2 valleys
-    __syncthreads();
+    wave_sync();
   }
 
   // grid histogram -> inclusive prefix counts (in place)
@@ -507,7 +519,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       if (j < G) cgrid[j] = incl;
       carry = __builtin_amdgcn_readlane(incl, kWave - 1);
     }
-    __syncthreads();
+    wave_sync();
   }
   const uint32_t* P = cgrid;
   auto bound = [&](int q, int mm) -> int { return q < mm ? L.cpos[q] : G - 1; };
@@ -616,7 +628,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       before = hiP;
     }
   }
-  __syncthreads();
+  wave_sync();
 
   // 9a. cells held in registers: a target bin with at most 64 durations is
   // gathered into LDS and its element of the wanted rank found by counting
@@ -633,7 +645,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
         if (in) list[base + __popcll(bm & ((1ull << l) - 1ull))] = rv[r];
         base += __popcll(bm);
       }
-      __syncthreads();
+      wave_sync();
       const int k = (int)L.tpop[t];
       const uint64_t e = l < k ? list[l] : 0ull;
       uint32_t rank = 0;
@@ -643,7 +655,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       }
       const uint64_t hit = __ballot(l < k && (uint64_t)rank == L.trank[t]);
       const uint64_t val = readlane64(e, hit ? __builtin_ctzll(hit) : 0);
-      __syncthreads();
+      wave_sync();
       if (l == 0) {
         L.tpre[t] = val - lb;
         L.tdone[t] = 1;
@@ -651,7 +663,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
     } else if (l == 0) {
       L.tdone[t] = 0;
     }
-    __syncthreads();
+    wave_sync();
   }
 
   // 9b. exact selection inside the remaining target bins, kDigit bits per pass
@@ -668,7 +680,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
   for (int p = 0; p < npass; ++p) {
     const int shift = kDigit * (npass - 1 - p);
     for (int i = l; i < NT * R; i += kWave) hist[i] = 0;
-    __syncthreads();
+    wave_sync();
     auto consider = [&](uint64_t v) {
       for (int t = 0; t < NT; ++t) {
         if (L.tdone[t]) continue;
@@ -687,7 +699,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
     } else {
       for (uint32_t i = l; i < n; i += kWave) consider(vals[i]);
     }
-    __syncthreads();
+    wave_sync();
     for (int t = 0; t < NT; ++t) {
       if (L.tdone[t]) continue;
       // the digit holding the target rank: one counter per lane, a wave scan
@@ -701,7 +713,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
         L.trank[t] = r - excl;
         L.tpre[t] = (L.tpre[t] << kDigit) | (uint64_t)owner;
       }
-      __syncthreads();
+      wave_sync();
     }
   }
 
@@ -720,7 +732,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
     a.n_clusters[c] = (uint8_t)ncl;
     if (a.bw_q8) a.bw_q8[c] = (int32_t)H;
   }
-  __syncthreads();
+  wave_sync();
   return true;
 }
 
@@ -769,7 +781,7 @@ __device__ void finish_or_hand_on(const KdeArgs& a, CellLds<TIER>& L, int64_t c,
   if (!kde_one_cell<TIER>(a, L, c, m, rv)) {
     if (TIER == 0 && l == 0) a.list1[atomicAdd(&a.counters[2], 1u)] = (uint32_t)c;
     if (TIER == 1 && l == 0) a.list2[atomicAdd(&a.counters[4], 1u)] = (uint32_t)c;
-    __syncthreads();
+    wave_sync();
   }
 }
 
@@ -778,7 +790,7 @@ __global__ __launch_bounds__(kWave, TIER == 0 ? 4 : 1) void kde_cell_kernel(KdeA
   __shared__ CellLds<TIER> L;
   const int l = lane_id();
   L.th[l] = a.theta[l];
-  __syncthreads();
+  wave_sync();
   const int64_t C = (int64_t)a.n_seg * a.K;
   while (true) {
     uint32_t claim = 0;
@@ -793,18 +805,23 @@ __global__ __launch_bounds__(kWave, TIER == 0 ? 4 : 1) void kde_cell_kernel(KdeA
       CellMeta mine{};
       mine.off = -1;
       if (l < ncells) mine = load_meta(a, c0 + l);
+      // cur is only ever a copy of nxt, taken once its loads are complete,
+      // and the first cell's loads are waited for right away: at the loop
+      // head no load is pending into cur on either path, so the next cell's
+      // loads stay in flight while this one is processed
       uint64_t cur[kRegVals], nxt[kRegVals];
-      CellMeta m = meta_from_lane(mine, 0);
-      load_small(a, m, cur);
+      CellMeta mn = meta_from_lane(mine, 0);
+      load_small(a, mn, nxt);
+      __builtin_amdgcn_s_waitcnt(0);
       for (int i = 0; i < ncells; ++i) {
-        CellMeta mn{};
+        const CellMeta m = mn;
+#pragma unroll
+        for (int r = 0; r < kRegVals; ++r) cur[r] = nxt[r];
+        mn = CellMeta{};
         mn.off = -1;
         if (i + 1 < ncells) mn = meta_from_lane(mine, i + 1);
         load_small(a, mn, nxt);
         finish_or_hand_on<TIER>(a, L, c0 + i, m, cur);
-#pragma unroll
-        for (int r = 0; r < kRegVals; ++r) cur[r] = nxt[r];
-        m = mn;
       }
     } else {
       const uint32_t len = __builtin_amdgcn_readfirstlane(
