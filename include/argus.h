@@ -359,8 +359,8 @@ void argus_kde_default(argus_kde_params_t* p);
 size_t argus_kde_workspace(const argus_events_t* ev);
 
 /* ev: as for argus_summarize, n_kernels <= ARGUS_MAX_KDE_KERNELS.
- * sum: only count, min_ns and max_ns are read. The workspace must be
- * 256-byte aligned. */
+ * sum: only count, min_ns and max_ns are read. out->count, p50_ns and p99_ns
+ * must be 16-byte aligned. The workspace must be 256-byte aligned. */
 int argus_kde(const argus_events_t* ev, const argus_summary_t* sum, const argus_kde_params_t* params,
               const argus_kde_out_t* out, void* workspace, size_t workspace_bytes, void* stream);
 

@@ -207,6 +207,9 @@ int argus_kde(const argus_events_t* ev, const argus_summary_t* sum, const argus_
   if (ev->n_events > 0 && (!ev->kernel_id || !ev->stream || !ev->start_ns || !ev->end_ns)) return ARGUS_EINVAL;
   if (!sum->count || !sum->min_ns || !sum->max_ns) return ARGUS_EINVAL;
   if (!out->n_clusters || !out->count || !out->p50_ns || !out->p99_ns) return ARGUS_EINVAL;
+  if (((reinterpret_cast<uintptr_t>(out->count) | reinterpret_cast<uintptr_t>(out->p50_ns) |
+        reinterpret_cast<uintptr_t>(out->p99_ns)) & 15u) != 0)
+    return ARGUS_EINVAL;  // per-cell records are written with 16-byte stores
   const argus_kde_params_t& p = *params;
   if (p.sub_bits < 1 || p.sub_bits > 6 || p.frac_pm < 0 || p.frac_pm > 1000 || p.min_count < 1 || p.gap < 0)
     return ARGUS_EINVAL;

@@ -82,12 +82,15 @@ struct KdeArgs {
   int32_t* bw_q8;
   int32_t* dev_status;
   // [0] scatter queue, [1] tier-0 queue, [2] list-1 length, [3] list-1 queue,
-  // [4] list-2 length, [5] list-2 queue
+  // [4] list-2 length, [5] list-2 queue, [6] first lane pass queue, [7] list-0 length,
+  // [8] wide lane pass queue, [9] wide list length
   uint32_t* counters;
   uint64_t* bucket;    // [n_events]: segment g's durations at seg_off[g] + local position
   uint32_t* cell_end;  // [cells]: local end offset of each cell's durations
-  uint32_t* list1;     // [cells]: cells handed from tier 0 to tier 1
-  uint32_t* list2;     // [cells]: cells handed from tier 1 to tier 2
+  uint32_t* list1;     // [cells]: wide cells for the second lane pass, later cells handed from tier 0 to
+                       // tier 1 (the wide list is consumed before tier 0 starts)
+  uint32_t* list2;     // [cells]: cells handed from the lane tier to tier 0 (list 0), later from tier 1 to
+                       // tier 2 (list 0 is consumed before tier 1 starts)
   uint32_t theta[64];  // ceil(2^(23 + t/64))
 };
 
@@ -279,6 +282,7 @@ struct CellLds {
   uint64_t trank[kMaxT];
   uint32_t tpop[kMaxT];  // durations in the target bin
   uint32_t tdone[kMaxT]; // target already resolved
+  uint32_t tcnt[kMaxT];  // durations gathered for the target so far
   uint32_t buf[W];      // grid histogram (then its prefix) | weights; later selection counters
   uint32_t nzc[NZ];     // occupied grid points: count
   int32_t cpos[CA];     // valley grid index
@@ -369,10 +373,18 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       }
     }
   } else {
-    for (uint32_t i = l; i < n; i += kWave) {
-      const int x = (grid64(vals[i], L.th) >> sh) - lo;
-      if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
-      else out_of_range = true;
+    // four loads in flight per lane
+    for (uint32_t i0 = l; i0 < n; i0 += 4 * kWave) {
+      uint64_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (i0 + u * kWave >= n) break;
+        const int x = (grid64(v[u], L.th) >> sh) - lo;
+        if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
+        else out_of_range = true;
+      }
     }
   }
   wave_sync();
@@ -630,40 +642,62 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
   }
   wave_sync();
 
-  // 9a. cells held in registers: a target bin with at most 64 durations is
-  // gathered into LDS and its element of the wanted rank found by counting
-  for (int t = 0; t < NT; ++t) {
-    const bool direct = in_regs && L.tpop[t] <= (uint32_t)kWave;
-    if (direct) {
-      uint64_t* list = reinterpret_cast<uint64_t*>(L.buf);
-      const uint64_t lb = L.tlb[t], ub = L.tub[t];
-      int base = 0;
-#pragma unroll
-      for (int r = 0; r < kRegVals; ++r) {
-        const bool in = (uint32_t)(l + r * kWave) < n && rv[r] >= lb && rv[r] < ub;
-        const uint64_t bm = __ballot(in);
-        if (in) list[base + __popcll(bm & ((1ull << l) - 1ull))] = rv[r];
-        base += __popcll(bm);
-      }
-      wave_sync();
-      const int k = (int)L.tpop[t];
-      const uint64_t e = l < k ? list[l] : 0ull;
-      uint32_t rank = 0;
-      for (int j = 0; j < k; ++j) {
-        const uint64_t ej = list[j];
-        rank += (ej < e || (ej == e && j < l)) ? 1u : 0u;
-      }
-      const uint64_t hit = __ballot(l < k && (uint64_t)rank == L.trank[t]);
-      const uint64_t val = readlane64(e, hit ? __builtin_ctzll(hit) : 0);
-      wave_sync();
-      if (l == 0) {
-        L.tpre[t] = val - lb;
-        L.tdone[t] = 1;
-      }
-    } else if (l == 0) {
-      L.tdone[t] = 0;
+  // 9a. a target bin with at most 64 durations is gathered into LDS (from
+  // registers, or in one pass over the cell's durations for all such targets
+  // at once) and its element of the wanted rank found by counting
+  {
+    int ndirect = 0;
+    for (int t = 0; t < NT; ++t) ndirect += L.tpop[t] <= (uint32_t)kWave ? 1 : 0;
+    if (l < kMaxT) {
+      L.tdone[l] = 0;
+      L.tcnt[l] = 0;
     }
     wave_sync();
+    if (ndirect > 0) {
+      uint64_t* lists = reinterpret_cast<uint64_t*>(L.buf);  // kMaxT lists of kWave durations
+      auto gather = [&](uint64_t v) {
+        for (int t = 0; t < NT; ++t) {
+          if (L.tpop[t] > (uint32_t)kWave) continue;
+          if (v >= L.tlb[t] && v < L.tub[t]) {
+            const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
+            if (slot < (uint32_t)kWave) lists[t * kWave + slot] = v;
+          }
+        }
+      };
+      if (in_regs) {
+#pragma unroll
+        for (int r = 0; r < kRegVals; ++r)
+          if ((uint32_t)(l + r * kWave) < n) gather(rv[r]);
+      } else {
+        for (uint32_t i0 = l; i0 < n; i0 += 4 * kWave) {
+          uint64_t v[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (i0 + u * kWave < n) gather(v[u]);
+        }
+      }
+      wave_sync();
+      for (int t = 0; t < NT; ++t) {
+        if (L.tpop[t] > (uint32_t)kWave) continue;
+        const int k = (int)L.tpop[t];
+        const uint64_t* list = lists + t * kWave;
+        const uint64_t e = l < k ? list[l] : 0ull;
+        uint32_t rank = 0;
+        for (int j = 0; j < k; ++j) {
+          const uint64_t ej = list[j];
+          rank += (ej < e || (ej == e && j < l)) ? 1u : 0u;
+        }
+        const uint64_t hit = __ballot(l < k && (uint64_t)rank == L.trank[t]);
+        const uint64_t val = readlane64(e, hit ? __builtin_ctzll(hit) : 0);
+        if (l == 0) {
+          L.tpre[t] = val - L.tlb[t];
+          L.tdone[t] = 1;
+        }
+      }
+      wave_sync();
+    }
   }
 
   // 9b. exact selection inside the remaining target bins, kDigit bits per pass
@@ -697,7 +731,14 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       for (int r = 0; r < kRegVals; ++r)
         if ((uint32_t)(l + r * kWave) < n) consider(rv[r]);
     } else {
-      for (uint32_t i = l; i < n; i += kWave) consider(vals[i]);
+      for (uint32_t i0 = l; i0 < n; i0 += 4 * kWave) {
+        uint64_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (i0 + u * kWave < n) consider(v[u]);
+      }
     }
     wave_sync();
     for (int t = 0; t < NT; ++t) {
@@ -791,20 +832,25 @@ __global__ __launch_bounds__(kWave, TIER == 0 ? 4 : 1) void kde_cell_kernel(KdeA
   const int l = lane_id();
   L.th[l] = a.theta[l];
   wave_sync();
-  const int64_t C = (int64_t)a.n_seg * a.K;
   while (true) {
     uint32_t claim = 0;
     if (l == 0) claim = atomicAdd(&a.counters[TIER == 0 ? 1 : (TIER == 1 ? 3 : 5)], 1u);
     claim = __builtin_amdgcn_readfirstlane(claim);
     if constexpr (TIER == 0) {
-      const int64_t c0 = (int64_t)claim * kWave;
-      if (c0 >= C) break;
-      const int ncells = C - c0 < kWave ? (int)(C - c0) : kWave;
-      // every lane fetches one cell's summary; the wave then walks the cells,
-      // loading the next small cell's durations while it works on this one
+      const uint32_t len0 = __builtin_amdgcn_readfirstlane(
+          __hip_atomic_load(&a.counters[7], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+      const int64_t i0 = (int64_t)claim * kWave;
+      if (i0 >= (int64_t)len0) break;
+      const int ncells = (int64_t)len0 - i0 < kWave ? (int)((int64_t)len0 - i0) : kWave;
+      // every lane fetches one listed cell's summary; the wave then walks the
+      // cells, loading the next small cell's durations while it works on this one
       CellMeta mine{};
       mine.off = -1;
-      if (l < ncells) mine = load_meta(a, c0 + l);
+      int64_t cell = 0;
+      if (l < ncells) {
+        cell = a.list2[i0 + l];
+        mine = load_meta(a, cell);
+      }
       // cur is only ever a copy of nxt, taken once its loads are complete,
       // and the first cell's loads are waited for right away: at the loop
       // head no load is pending into cur on either path, so the next cell's
@@ -821,7 +867,7 @@ __global__ __launch_bounds__(kWave, TIER == 0 ? 4 : 1) void kde_cell_kernel(KdeA
         mn.off = -1;
         if (i + 1 < ncells) mn = meta_from_lane(mine, i + 1);
         load_small(a, mn, nxt);
-        finish_or_hand_on<TIER>(a, L, c0 + i, m, cur);
+        finish_or_hand_on<TIER>(a, L, (int64_t)readlane64((uint64_t)cell, i), m, cur);
       }
     } else {
       const uint32_t len = __builtin_amdgcn_readfirstlane(
@@ -835,6 +881,292 @@ __global__ __launch_bounds__(kWave, TIER == 0 ? 4 : 1) void kde_cell_kernel(KdeA
       uint64_t cur[kRegVals];
       load_small(a, m, cur);
       finish_or_hand_on<TIER>(a, L, c, m, cur);
+    }
+  }
+}
+
+// -------------------------------------------------------------- lane tier
+// Cells of at most kLaneN durations whose grid has at most kLaneG points
+// (nine cells in ten in the benchmark workloads; the median holds 40
+// durations) are processed one per lane, 64 cells per wavefront, each lane
+// running every step of the definition on its own cell: a wavefront per
+// such cell would spend most of its instructions on per-cell fixed costs.
+// Per-lane arrays live in LDS with the lane as the fastest index, so lanes
+// at the same step touch consecutive words. A lane that finds more valleys
+// than kLaneCand, or more durations in a target grid bin than kLaneList,
+// writes nothing and hands its cell to the wavefront tiers, like every cell
+// outside these limits.
+constexpr int kLaneN = 255;     // durations per cell (counts fit in 8 bits, densities in 24)
+constexpr int kLaneG = 64;      // grid points per cell, first lane pass (over every cell)
+constexpr int kLaneGW = 256;    // grid points per cell, second lane pass (listed wide cells)
+constexpr int kLaneT = 32;      // kernel weights (t < 32)
+constexpr int kLaneCand = 8;    // valleys before filtering
+constexpr int kLaneList = 16;   // durations of one target grid bin
+
+template <int GC>
+struct LaneLds {
+  uint32_t cp[GC / 4][kWave];      // grid counts, then inclusive prefix counts: four 8-bit values per word
+  uint32_t w[kLaneT][kWave];       // kernel weights; later the durations of one target bin (lo, hi words)
+  uint32_t cand[kLaneCand][kWave]; // valleys: density << 8 | grid index
+  uint32_t th[64];
+};
+
+template <int GC>
+__device__ __forceinline__ uint32_t lane_cnt(const LaneLds<GC>& L, int j, int l) {
+  return (L.cp[j >> 2][l] >> ((j & 3) * 8)) & 0xFFu;
+}
+
+template <int GC>
+__device__ __forceinline__ void lane_drop(LaneLds<GC>& L, int i, int& m, int l) {
+  for (int q = i; q + 1 < m; ++q) L.cand[q][l] = L.cand[q + 1][l];
+  --m;
+}
+
+// Per-lane empty record (count 0, or a summary that does not match).
+__device__ __forceinline__ void lane_write(const KdeArgs& a, int64_t c, int ncl, const uint32_t (&cnt)[kMaxC],
+                                           const uint64_t (&p50)[kMaxC], const uint64_t (&p99)[kMaxC], int64_t H) {
+  *reinterpret_cast<uint4*>(a.cl_count + c * kMaxC) = make_uint4(cnt[0], cnt[1], cnt[2], cnt[3]);
+  v2l* q50 = reinterpret_cast<v2l*>(a.p50 + c * kMaxC);
+  v2l* q99 = reinterpret_cast<v2l*>(a.p99 + c * kMaxC);
+  q50[0] = v2l{(long long)p50[0], (long long)p50[1]};
+  q50[1] = v2l{(long long)p50[2], (long long)p50[3]};
+  q99[0] = v2l{(long long)p99[0], (long long)p99[1]};
+  q99[1] = v2l{(long long)p99[2], (long long)p99[3]};
+  a.n_clusters[c] = (uint8_t)ncl;
+  if (a.bw_q8) a.bw_q8[c] = (int32_t)H;
+}
+
+// One cell on one lane. Returns false (nothing written) when the cell does
+// not fit the lane limits found on the way.
+template <int GC>
+__device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const CellMeta& cm) {
+  const int l = lane_id();
+  const uint32_t n = cm.n;
+  const uint64_t* vals = a.bucket + cm.off;
+  const int sh = 6 - a.sub_bits;
+  const int lo = grid64((uint64_t)cm.mn, L.th) >> sh;
+  const int G = (grid64((uint64_t)cm.mx, L.th) >> sh) - lo + 1;
+
+  // 1. grid histogram; eight loads in flight per lane, and LDS adds that
+  // return nothing, so no iteration waits on the previous one
+  for (int j = 0; j < (G + 3) / 4; ++j) L.cp[j][l] = 0;
+  bool out_of_range = false;
+  for (uint32_t i0 = 0; i0 < n; i0 += 8) {
+    uint64_t d[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) d[u] = i0 + u < n ? vals[i0 + u] : 0ull;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (i0 + u >= n) break;
+      const int x = (grid64(d[u], L.th) >> sh) - lo;
+      if (x >= 0 && x < G) atomicAdd(&L.cp[x >> 2][l], 1u << ((x & 3) * 8));
+      else out_of_range = true;
+    }
+  }
+  uint32_t cnt[kMaxC] = {0, 0, 0, 0};
+  uint64_t p50[kMaxC] = {0, 0, 0, 0}, p99[kMaxC] = {0, 0, 0, 0};
+  if (out_of_range) {  // durations outside the summarized [min, max]
+    flag(a, ARGUS_DEV_KDE_SUMMARY);
+    lane_write(a, c, 0, cnt, p50, p99, 0);
+    return true;
+  }
+
+  // 2. bandwidth (exact integer moments: n <= 255, x < 64)
+  int64_t H = 0;
+  if (n >= 2) {
+    uint64_t s1 = 0, s2 = 0;
+    for (int j = 0; j < G; ++j) {
+      const uint64_t k = lane_cnt(L, j, l);
+      s1 += k * (uint64_t)j;
+      s2 += k * (uint64_t)j * (uint64_t)j;
+    }
+    const double var = (double)(n * s2 - s1 * s1) / ((double)n * (double)(n - 1));
+    const double h = 1.06 * sqrt(var) * cm.pw;
+    H = (int64_t)floor(h * 256.0 + 0.5);
+  }
+
+  // 3-4. weights, then the density in one pass with its valleys: a run of
+  // equal values entered from above and left upwards is a valley, placed at
+  // the middle of the run
+  int m = 0;
+  if (H > 0 && G >= 3) {
+    const double H2 = (double)(H * H);
+    int T = -1;
+    for (int t = 0; t < G; ++t) {
+      const uint32_t wt = (uint32_t)floor(65536.0 * exp(-(double)(32768ll * t * t) / H2) + 0.5);
+      if (wt == 0) break;
+      if (t == kLaneT) return false;  // kernel wider than the lane's weight table
+      L.w[t][l] = wt;
+      T = t;
+    }
+    uint32_t v = 0, pv = 0;
+    int r0 = 0;
+    for (int j = 0; j < G; ++j) {
+      const int b0 = j - T > 0 ? j - T : 0, b1 = j + T < G - 1 ? j + T : G - 1;
+      uint32_t f = 0;
+#pragma unroll 4
+      for (int b = b0; b <= b1; ++b) f += lane_cnt(L, b, l) * L.w[j > b ? j - b : b - j][l];
+      if (j == 0) {
+        v = f;
+      } else if (f != v) {
+        if (r0 >= 1 && pv > v && f > v) {
+          if (m == kLaneCand) return false;
+          L.cand[m][l] = (v << 8) | (uint32_t)((r0 + j - 1) / 2);
+          ++m;
+        }
+        pv = v;
+        v = f;
+        r0 = j;
+      }
+    }
+  }
+
+  // grid counts -> inclusive prefix counts (at most n <= 255), in place
+  {
+    uint32_t run = 0;
+    for (int j = 0; j < (G + 3) / 4; ++j) {
+      const uint32_t wd = L.cp[j][l];
+      uint32_t out = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        run += (wd >> (8 * b)) & 0xFFu;
+        out |= run << (8 * b);
+      }
+      L.cp[j][l] = out;
+    }
+  }
+  auto P = [&](int j) -> uint32_t { return j < 0 ? 0u : lane_cnt(L, j, l); };
+  auto pos = [&](int q) -> int { return (int)(L.cand[q][l] & 0xFFu); };
+  auto val = [&](int q) -> uint32_t { return L.cand[q][l] >> 8; };
+  auto hi_of = [&](int q, int mm) -> int { return q < mm ? pos(q) : G - 1; };
+
+  // 5. cluster-level filter
+  uint32_t need = (uint32_t)(((uint64_t)a.frac_pm * n + 999u) / 1000u);
+  if (need < (uint32_t)a.min_count) need = (uint32_t)a.min_count;
+  while (m > 0) {
+    int best = 0;
+    uint32_t best_size = 0;
+    for (int q = 0; q <= m; ++q) {
+      const uint32_t sz = P(hi_of(q, m)) - (q > 0 ? P(pos(q - 1)) : 0u);
+      if (q == 0 || sz < best_size) {
+        best = q;
+        best_size = sz;
+      }
+    }
+    if (best_size >= need) break;
+    lane_drop(L, best == 0 ? 0 : (best == m ? m - 1 : (val(best - 1) > val(best) ? best - 1 : best)), m, l);
+  }
+
+  // 6. spacing filter over [0, valleys..., G - 1]
+  while (m > 0) {
+    int hit = -1;
+    for (int q = 0; q <= m && hit < 0; ++q)
+      if (hi_of(q, m) - (q > 0 ? pos(q - 1) : 0) < a.gap) hit = q;
+    if (hit < 0) break;
+    lane_drop(L, hit == 0 ? 0 : (hit == m ? m - 1 : (val(hit - 1) > val(hit) ? hit - 1 : hit)), m, l);
+  }
+
+  // 7. cluster cap: drop the largest-density valley (the upper one on ties)
+  while (m > kMaxC - 1) {
+    int s = 0;
+    for (int q = 1; q < m; ++q)
+      if (val(q) >= val(s)) s = q;
+    lane_drop(L, s, m, l);
+  }
+
+  // 8. per cluster: count, then p50 / p99 as the element of the wanted rank
+  // inside its grid bin, found among the bin's durations gathered in LDS
+  const int ncl = m + 1;
+  uint32_t before = 0;
+  for (int q = 0; q < ncl; ++q) {
+    const uint32_t hiP = P(hi_of(q, m)), size = hiP - before;
+    for (int qq = 0; qq < kMaxC; ++qq)
+      if (qq == q) cnt[qq] = size;
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const uint32_t r = t2 == 0 ? before + (size - 1) / 2 : before + (99 * size + 99) / 100 - 1;
+      int j = 0;
+      while (P(j) <= r) ++j;  // smallest grid index whose prefix count passes r
+      const uint32_t below = P(j - 1), k = P(j) - below;
+      if (k > (uint32_t)kLaneList) return false;
+      const uint64_t lb = grid64_lb((lo + j) << sh, L.th), ub = grid64_lb((lo + j + 1) << sh, L.th);
+      uint32_t got = 0;
+      for (uint32_t i0 = 0; i0 < n && got < k; i0 += 8) {
+        uint64_t d[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) d[u] = i0 + u < n ? vals[i0 + u] : ~0ull;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          if (d[u] >= lb && d[u] < ub && got < k) {
+            L.w[2 * got][l] = (uint32_t)d[u];
+            L.w[2 * got + 1][l] = (uint32_t)(d[u] >> 32);
+            ++got;
+          }
+        }
+      }
+      const uint32_t rr = r - below;
+      uint64_t pick = 0;
+      for (uint32_t i = 0; i < k; ++i) {
+        const uint64_t e = ((uint64_t)L.w[2 * i + 1][l] << 32) | L.w[2 * i][l];
+        uint32_t rank = 0;
+        for (uint32_t x = 0; x < k; ++x) {
+          const uint64_t y = ((uint64_t)L.w[2 * x + 1][l] << 32) | L.w[2 * x][l];
+          rank += (y < e || (y == e && x < i)) ? 1u : 0u;
+        }
+        if (rank == rr) pick = e;
+      }
+      for (int qq = 0; qq < kMaxC; ++qq) {
+        if (qq != q) continue;
+        if (t2 == 0) p50[qq] = pick;
+        else p99[qq] = pick;
+      }
+    }
+    before = hiP;
+  }
+  lane_write(a, c, ncl, cnt, p50, p99, H);
+  return true;
+}
+
+// Lane passes. GC = kLaneG: every cell, 64 consecutive cells per claim;
+// cells of up to kLaneN durations whose grid has 65 .. kLaneGW points go to
+// the wide list, the rest that does not fit to list 0. GC = kLaneGW: the
+// wide list, 64 entries per claim; what does not fit goes to list 0.
+template <int GC>
+__global__ __launch_bounds__(kWave) void kde_lane_kernel(KdeArgs a) {
+  constexpr bool kFirst = GC == kLaneG;
+  __shared__ LaneLds<GC> L;
+  const int l = lane_id();
+  L.th[l] = a.theta[l];
+  wave_sync();
+  const int64_t C = kFirst ? (int64_t)a.n_seg * a.K
+                           : (int64_t)__builtin_amdgcn_readfirstlane(
+                                 __hip_atomic_load(&a.counters[9], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  const int sh = 6 - a.sub_bits;
+  while (true) {
+    uint32_t claim = 0;
+    if (l == 0) claim = atomicAdd(&a.counters[kFirst ? 6 : 8], 1u);
+    claim = __builtin_amdgcn_readfirstlane(claim);
+    if ((int64_t)claim * kWave >= C) break;
+    const int64_t i = (int64_t)claim * kWave + l;
+    if (i < C) {
+      const int64_t c = kFirst ? i : (int64_t)a.list1[i];
+      const CellMeta m = load_meta(a, c);
+      bool done = false;
+      if (kFirst && (m.n == 0 || m.off < 0)) {
+        if (m.n != 0) flag(a, ARGUS_DEV_KDE_SUMMARY);
+        const uint32_t z[kMaxC] = {0, 0, 0, 0};
+        const uint64_t zz[kMaxC] = {0, 0, 0, 0};
+        lane_write(a, c, 0, z, zz, zz, 0);
+        done = true;
+      } else if (m.n <= (uint32_t)kLaneN) {
+        const int G = (grid64((uint64_t)m.mx, L.th) >> sh) - (grid64((uint64_t)m.mn, L.th) >> sh) + 1;
+        if (G <= GC) {
+          done = lane_cell<GC>(a, L, c, m);
+        } else if (kFirst && G <= kLaneGW) {
+          a.list1[atomicAdd(&a.counters[9], 1u)] = (uint32_t)c;
+          done = true;
+        }
+      }
+      if (!done) a.list2[atomicAdd(&a.counters[7], 1u)] = (uint32_t)c;
     }
   }
 }
@@ -908,7 +1240,7 @@ int resident(Kern kern, int threads) {
 }
 
 __global__ void kde_clear_kernel(uint32_t* counters, int32_t* dev_status) {
-  if (threadIdx.x < 8) counters[threadIdx.x] = 0;
+  if (threadIdx.x < 16) counters[threadIdx.x] = 0;
   if (threadIdx.x == 0 && dev_status) *dev_status = 0;
 }
 
@@ -968,22 +1300,28 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   if (cells == 0) return hipSuccess;
 
   // resident workgroups per kernel, cached per device
-  static std::atomic<int> grids[64][4];
+  static std::atomic<int> grids[64][6];
   int dev = 0;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  int g[4];
-  for (int i = 0; i < 4; ++i) g[i] = grids[dev][i].load();
+  int g[6];
+  for (int i = 0; i < 6; ++i) g[i] = grids[dev][i].load();
   if (g[0] == 0) grids[dev][0].store(g[0] = resident(kde_scatter_kernel, kScatterThreads));
   if (g[1] == 0) grids[dev][1].store(g[1] = resident(kde_cell_kernel<0>, kWave));
   if (g[2] == 0) grids[dev][2].store(g[2] = resident(kde_cell_kernel<1>, kWave));
   if (g[3] == 0) grids[dev][3].store(g[3] = resident(kde_cell_kernel<2>, kWave));
-  for (int i = 0; i < 4; ++i)
+  if (g[4] == 0) grids[dev][4].store(g[4] = resident(kde_lane_kernel<kLaneG>, kWave));
+  if (g[5] == 0) grids[dev][5].store(g[5] = resident(kde_lane_kernel<kLaneGW>, kWave));
+  for (int i = 0; i < 6; ++i)
     if (g[i] <= 0) return hipErrorInvalidDevice;
   hipLaunchKernelGGL(kde_scatter_kernel, dim3(l.n_seg < g[0] ? l.n_seg : g[0]), dim3(kScatterThreads), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int64_t chunks = (cells + kWave - 1) / kWave;
-  hipLaunchKernelGGL(kde_cell_kernel<0>, dim3(chunks < g[1] ? (int)chunks : g[1]), dim3(kWave), 0, st, a);
+  hipLaunchKernelGGL(kde_lane_kernel<kLaneG>, dim3(chunks < g[4] ? (int)chunks : g[4]), dim3(kWave), 0, st, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(kde_lane_kernel<kLaneGW>, dim3(g[5]), dim3(kWave), 0, st, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(kde_cell_kernel<0>, dim3(g[1]), dim3(kWave), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(kde_cell_kernel<1>, dim3(g[2]), dim3(kWave), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;

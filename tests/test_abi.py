@@ -97,7 +97,7 @@ def test_cross_rank_and_l1_reject_bad_arguments():
     lambda e, s, p: setattr(p, "frac_pm", 1001),
     lambda e, s, p: setattr(p, "min_count", 0),
     lambda e, s, p: setattr(p, "gap", -1),
-    "misaligned", "small",
+    "misaligned", "small", "misaligned_out",
 ])
 def test_kde_rejects_bad_arguments(mutate):
     e = A.Events(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 10, 2, 2, 4, 2)
@@ -110,6 +110,8 @@ def test_kde_rejects_bad_arguments(mutate):
         ws = 0x10080
     elif mutate == "small":
         n = 256
+    elif mutate == "misaligned_out":
+        o.p50_ns = 0x1008
     else:
         mutate(e, s, p)
     assert pa.lib().argus_kde(ctypes.byref(e), ctypes.byref(s), ctypes.byref(p), ctypes.byref(o), ws, n,
