@@ -43,21 +43,23 @@ constexpr int kPowTab = 65536;    // n^-0.2 for n below this, from the host libm
 constexpr int kRegVals = 4;       // cells of up to 256 durations stay in registers
 constexpr int kDigit = 6;         // radix-selection digit width (64 counters per target)
 
-// LDS per tier: grid words (histogram + weights), valley capacity, capacity
-// of the occupied-grid-point list used by the sparse density.
+// LDS per tier: grid words (histogram, chunk offsets, occupied-point list
+// and symmetric zero-padded weight table: at most 3 G + 2 T + 337 words; the
+// selection lists of the wavefront tiers take 1,024) and valley capacity.
+// Tier 2 holds any grid of the duration range (at most 4,032 points, T < G).
 template <int TIER>
 struct Tier;
 template <>
 struct Tier<0> {
-  static constexpr int kWords = 1024, kCand = 64, kNz = 128;
+  static constexpr int kWords = 1536, kCand = 64;
 };
 template <>
 struct Tier<1> {
-  static constexpr int kWords = 4096, kCand = 256, kNz = 512;
+  static constexpr int kWords = 4096, kCand = 256;
 };
 template <>
 struct Tier<2> {
-  static constexpr int kWords = 8192, kCand = 2047, kNz = 1;  // 4,032-point grids at most
+  static constexpr int kWords = 20512, kCand = 2047;
 };
 
 // n^-0.2 for small n, filled once per device from the host's pow().
@@ -83,14 +85,15 @@ struct KdeArgs {
   int32_t* dev_status;
   // [0] scatter queue, [1] tier-0 queue, [2] list-1 length, [3] list-1 queue,
   // [4] list-2 length, [5] list-2 queue, [6] first lane pass queue, [7] list-0 length,
-  // [8] wide lane pass queue, [9] wide list length
+  // [8] wide lane pass queue, [9] wide list length, [10] workgroup tier queue, [11] heavy list length
   uint32_t* counters;
   uint64_t* bucket;    // [n_events]: segment g's durations at seg_off[g] + local position
   uint32_t* cell_end;  // [cells]: local end offset of each cell's durations
-  uint32_t* list1;     // [cells]: wide cells for the second lane pass, later cells handed from tier 0 to
-                       // tier 1 (the wide list is consumed before tier 0 starts)
-  uint32_t* list2;     // [cells]: cells handed from the lane tier to tier 0 (list 0), later from tier 1 to
-                       // tier 2 (list 0 is consumed before tier 1 starts)
+  uint32_t* list1;     // [cells]: wide cells for the second lane pass, later cells handed from the
+                       // workgroup tier and tier 0 to tier 1 (the wide list is consumed first)
+  uint32_t* list2;     // [cells]: cells handed from the lane tier to tier 0 (list 0, from the bottom) and
+                       // to the workgroup tier (heavy list, from the top), later from tier 1 to tier 2
+                       // (both are consumed before tier 1 starts)
   uint32_t theta[64];  // ceil(2^(23 + t/64))
 };
 
@@ -274,7 +277,7 @@ __global__ __launch_bounds__(kScatterThreads) void kde_scatter_kernel(KdeArgs a)
 
 template <int TIER>
 struct CellLds {
-  static constexpr int W = Tier<TIER>::kWords, CA = Tier<TIER>::kCand, NZ = Tier<TIER>::kNz;
+  static constexpr int W = Tier<TIER>::kWords, CA = Tier<TIER>::kCand;
   uint64_t cval[CA];    // valley depth f
   uint64_t tlb[kMaxT];  // target bin: smallest duration
   uint64_t tub[kMaxT];  // target bin: one past the largest duration
@@ -283,10 +286,8 @@ struct CellLds {
   uint32_t tpop[kMaxT];  // durations in the target bin
   uint32_t tdone[kMaxT]; // target already resolved
   uint32_t tcnt[kMaxT];  // durations gathered for the target so far
-  uint32_t buf[W];      // grid histogram (then its prefix) | weights; later selection counters
-  uint32_t nzc[NZ];     // occupied grid points: count
+  alignas(16) uint32_t buf[W];  // grid histogram (then its prefix) | analysis data; later selection data
   int32_t cpos[CA];     // valley grid index
-  uint16_t nzb[NZ];     // occupied grid points: index (ascending)
   uint32_t th[64];
 };
 
@@ -342,76 +343,99 @@ __device__ __forceinline__ void load_small(const KdeArgs& a, const CellMeta& m, 
   }
 }
 
-// One cell on one wavefront. Returns false when the cell needs a larger
-// tier (only for TIER < 2; nothing has been written for it then).
+// Zero padding of the symmetric weight table beyond T: the density loop
+// takes occupied grid points by whole histogram chunks of 64, so it meets
+// distances up to T + 126.
+constexpr int kWPad = 127;
+
+// f(j) = sum_b c(b) w(|j - b|) for this lane's grid point j = jb + lane, in
+// registers, over the occupied grid points list[k0, k1) (pairs (b, c(b)),
+// read with wavefront-uniform addresses). ws is the symmetric weight table,
+// ws[d] = w(|d|), zero from T + 1 to T + kWPad. Eight points per step, so
+// eight weight reads are in flight; the list holds eight readable pairs past
+// its end. Acc = uint32_t is exact while the cell has fewer than 65,536
+// durations (f <= 65536 n) and multiplies in 24 bits (c < 2^24, w <= 2^16).
+template <typename Acc>
+__device__ __forceinline__ Acc density_list(const uint32_t* ws, const uint2* list, int k0, int k1, int jb) {
+  const int j = jb + lane_id();
+  const uint32_t* wj = ws + j;
+  Acc fj = 0;
+  for (int k = k0; k < k1; k += 8) {
+    uint32_t cb[8], wv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint2 e = list[k + u];
+      const bool in = k + u < k1;
+      cb[u] = in ? e.y : 0u;
+      wv[u] = wj[-(in ? (int)e.x : j)];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if constexpr (sizeof(Acc) == 4) fj += __umul24(cb[u], wv[u]);
+      else fj += (uint64_t)cb[u] * wv[u];
+    }
+  }
+  return fj;
+}
+
+// Rank of this lane's element e (lane < k) among list[0, k) in ascending
+// order, ties broken by position; list has 64 readable slots.
+__device__ __forceinline__ uint32_t rank_in_list(const uint64_t* list, int k, uint64_t e) {
+  const int l = lane_id();
+  uint32_t rank = 0;
+  for (int j0 = 0; j0 < k; j0 += 8) {
+    uint64_t ej[8];  // eight reads in flight
+#pragma unroll
+    for (int u = 0; u < 8; ++u) ej[u] = list[j0 + u];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) rank += (j0 + u < k && (ej[u] < e || (ej[u] == e && j0 + u < l))) ? 1u : 0u;
+  }
+  return rank;
+}
+
+// Steps 2 - 8 on one wavefront, the grid histogram of the cell being in
+// L.buf[0, G): bandwidth, density, valleys, filters, cap, per-cluster counts
+// and the selection targets (L.tlb / tub / trank / tpop, L.tpre = 0).
+// Returns false when the cell needs a larger tier (only for TIER < 2).
+struct Analysis {
+  int ncl, NT;
+  int64_t H;
+  uint32_t ccount[kMaxC];
+};
+
 template <int TIER>
-__device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, const CellMeta& cm,
-                             const uint64_t (&rv)[kRegVals]) {
-  constexpr int WORDS = CellLds<TIER>::W, CAND = CellLds<TIER>::CA, NZCAP = CellLds<TIER>::NZ;
+__device__ bool kde_analyze(const KdeArgs& a, CellLds<TIER>& L, const CellMeta& cm, int lo, int G, Analysis& res) {
+  constexpr int WORDS = CellLds<TIER>::W, CAND = CellLds<TIER>::CA;
   const int l = lane_id();
   const uint32_t n = cm.n;
-  const uint64_t* vals = a.bucket + cm.off;
   const int sh = 6 - a.sub_bits;
-  const int lo = grid64((uint64_t)cm.mn, L.th) >> sh;
-  const int G = (grid64((uint64_t)cm.mx, L.th) >> sh) - lo + 1;
-  if (TIER < 2 && G > WORDS) return false;
   uint32_t* cgrid = L.buf;
-  const bool in_regs = n <= (uint32_t)(kWave * kRegVals);
-
-  // 1. grid histogram
-  for (int j = l; j < G; j += kWave) cgrid[j] = 0;
-  wave_sync();
-  bool out_of_range = false;
-  if (in_regs) {
-#pragma unroll
-    for (int r = 0; r < kRegVals; ++r) {
-      const uint32_t i = (uint32_t)(l + r * kWave);
-      if (i < n) {
-        const int x = (grid64(rv[r], L.th) >> sh) - lo;
-        if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
-        else out_of_range = true;
-      }
-    }
-  } else {
-    // four loads in flight per lane
-    for (uint32_t i0 = l; i0 < n; i0 += 4 * kWave) {
-      uint64_t v[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (i0 + u * kWave >= n) break;
-        const int x = (grid64(v[u], L.th) >> sh) - lo;
-        if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
-        else out_of_range = true;
-      }
-    }
-  }
-  wave_sync();
-  if (__any(out_of_range)) {  // durations outside the summarized [min, max]
-    if (l == 0) flag(a, ARGUS_DEV_KDE_SUMMARY);
-    write_empty(a, c);
-    return true;
-  }
-
-  // 2. bandwidth; occupied grid points listed for the sparse density
+  // 2. bandwidth from the exact first and second moments of the grid index;
+  // the occupied grid points are listed on the way, in ascending order, as
+  // (b, c(b)) pairs, with cs[i] = pairs before histogram chunk i. LDS words:
+  // [0, G) histogram | cs | list (+ 8 pairs) | weight table
+  const int NCH = (G + kWave - 1) / kWave + 1;
+  uint32_t* cs = L.buf + G;
+  const int lofs = (G + NCH + 1) & ~1;
+  uint2* list = reinterpret_cast<uint2*>(L.buf + lofs);
   uint64_t s1 = 0, s2 = 0;
   int nnz = 0;
-  for (int jb = 0; jb < G; jb += kWave) {
+  for (int jb = 0, ch = 0; jb < G; jb += kWave, ++ch) {
     const int j = jb + l;
     const uint32_t k = j < G ? cgrid[j] : 0u;
     s1 += (uint64_t)k * (uint64_t)j;
     s2 += (uint64_t)k * (uint64_t)j * (uint64_t)j;
     const uint64_t occ = __ballot(k != 0);
+    if (l == 0) cs[ch] = (uint32_t)nnz;
     if (k != 0) {
       const int idx = nnz + __popcll(occ & ((1ull << l) - 1ull));
-      if (idx < NZCAP) {
-        L.nzb[idx] = (uint16_t)j;
-        L.nzc[idx] = k;
-      }
+      if (TIER == 2 || lofs + 2 * idx + 1 < WORDS) list[idx] = make_uint2((uint32_t)j, k);
     }
     nnz += __popcll(occ);
   }
+  if (l == 0) cs[NCH - 1] = (uint32_t)nnz;
+  const int tofs = lofs + 2 * (nnz + 8);
+  if (TIER < 2 && tofs > WORDS) return false;
   s1 = wave_sum_u64(s1);
   s2 = wave_sum_u64(s2);
   int64_t H = 0;
@@ -430,61 +454,40 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
   // 3-4. weights, density and valleys
   int m = 0;
   if (H > 0 && G >= 3) {
-    uint32_t* w = L.buf + G;
+    // weights straight into the symmetric table ws[-C .. C]: w(t) rounds to
+    // 0 once 32768 t^2 / H^2 > ln(131072), i.e. t > 0.018963 H, so every
+    // nonzero weight has t <= Tb = floor(0.019 H) + 2 (and t < G)
+    const int64_t Tb = (H * 19) / 1000 + 2;
+    const int C = (Tb < (int64_t)G - 1 ? (int)Tb : G - 1) + kWPad;
+    if (TIER < 2 && tofs + 2 * C + 1 > WORDS) return false;
+    uint32_t* ws = L.buf + tofs + C;
     const double H2 = (double)(H * H);
     int T = -1;
-    for (int tb = 0; tb < G; tb += kWave) {
+    bool past = false;  // a chunk with a zero weight has been seen: the rest are zero
+    for (int tb = 0; tb <= C; tb += kWave) {
       const int t = tb + l;
       uint32_t wt = 0;
-      if (t < G) wt = (uint32_t)floor(65536.0 * exp(-(double)(32768ll * t * t) / H2) + 0.5);
-      const uint64_t nz = __ballot(wt != 0);
-      const int cnt = __popcll(nz);  // weights are non-increasing in t
-      if (TIER < 2 && G + tb + cnt > WORDS) return false;
-      if (wt != 0 && G + t < WORDS) w[t] = wt;
-      T = tb + cnt - 1;
-      if (cnt < kWave) break;
+      if (!past && t < G) wt = (uint32_t)floor(65536.0 * exp(-(double)(32768ll * t * t) / H2) + 0.5);
+      const int cnt = __popcll(__ballot(wt != 0));  // weights are non-increasing in t
+      if (!past) T = tb + cnt - 1;
+      past = past || cnt < kWave;
+      if (t <= C) {
+        ws[t] = wt;
+        ws[-t] = wt;
+      }
     }
     wave_sync();
-    const bool sparse = nnz <= NZCAP && nnz < T;
     int carry_start = -1, carry_drop = 0;
     uint64_t prev_last = 0;
     for (int jb = 0; jb < G; jb += kWave) {
       const int j = jb + l;
       const bool valid = j < G;
-      uint64_t fj = 0;
-      if (sparse) {
-        // occupied points within T of this chunk: [k0, k1)
-        const int lo_b = jb - T, hi_b = jb + kWave - 1 + T;
-        int x = 0, y = nnz;
-        while (x < y) {
-          const int mid = (x + y) >> 1;
-          if ((int)L.nzb[mid] < lo_b) x = mid + 1;
-          else y = mid;
-        }
-        const int k0 = x;
-        y = nnz;
-        while (x < y) {
-          const int mid = (x + y) >> 1;
-          if ((int)L.nzb[mid] <= hi_b) x = mid + 1;
-          else y = mid;
-        }
-        const int k1 = x;
-        for (int k = k0; k < k1; ++k) {
-          const int b = L.nzb[k];
-          const int t = j > b ? j - b : b - j;
-          if (valid && t <= T) fj += (uint64_t)L.nzc[k] * w[t];
-        }
-      } else {
-        // f(j) = w(0) c(j) + sum_t w(t) (c(j - t) + c(j + t)), t uniform across lanes
-        const int tmax = T < G - 1 ? T : G - 1;
-        if (valid) fj = (uint64_t)cgrid[j] * w[0];
-        for (int t = 1; t <= tmax; ++t) {
-          const uint32_t wt = w[t];
-          const uint64_t cl = valid && j - t >= 0 ? cgrid[j - t] : 0u;
-          const uint64_t cr = valid && j + t < G ? cgrid[j + t] : 0u;
-          fj += (cl + cr) * wt;
-        }
-      }
+      const int kb0 = (jb - T > 0 ? jb - T : 0) / kWave;
+      const int kb1 = (jb + kWave - 1 + T < G - 1 ? jb + kWave - 1 + T : G - 1) / kWave;
+      const int k0 = (int)cs[kb0], k1 = (int)cs[kb1 + 1];
+      uint64_t fj = n < 65536u ? (uint64_t)density_list<uint32_t>(ws, list, k0, k1, jb)
+                               : density_list<uint64_t>(ws, list, k0, k1, jb);
+      if (!valid) fj = 0;
       uint64_t fl = __shfl_up(fj, 1, kWave);
       if (l == 0) fl = prev_last;
       const bool start = valid && (j == 0 || fj != fl);
@@ -602,45 +605,128 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
     --m;
   }
 
-  // 8. counts and selection targets (ranks in the cell's sorted order)
-  const int ncl = m + 1;
+  // 8. counts and selection targets (ranks in the cell's sorted order):
+  // cluster q holds the ranks [hiP(q - 1), hiP(q)) of the sorted durations
+  const int ncl = m + 1, NT = 2 * ncl;
+  uint64_t hiP[kMaxC], tr[kMaxT];
   uint32_t ccount[kMaxC];
 #pragma unroll
-  for (int q = 0; q < kMaxC; ++q) ccount[q] = 0;
-  int NT = 0;
-  {
-    uint64_t before = 0;
-    for (int q = 0; q < ncl; ++q) {
-      const uint64_t hiP = P[bound(q, m)];
-      const uint64_t size = hiP - before;
+  for (int q = 0; q < kMaxC; ++q) hiP[q] = q < ncl ? (uint64_t)P[bound(q, m)] : 0ull;
 #pragma unroll
-      for (int qq = 0; qq < kMaxC; ++qq)
-        if (qq == q) ccount[qq] = (uint32_t)size;
-      const uint64_t r50 = before + (size - 1) / 2;
-      const uint64_t r99 = before + (99 * size + 99) / 100 - 1;
-      for (int t2 = 0; t2 < 2; ++t2) {
-        const uint64_t r = t2 == 0 ? r50 : r99;
-        // smallest grid index j with P[j] > r
-        int lo_j = 0, hi_j = G - 1;
-        while (lo_j < hi_j) {
-          const int mid = (lo_j + hi_j) >> 1;
-          if ((uint64_t)P[mid] > r) hi_j = mid;
-          else lo_j = mid + 1;
+  for (int q = 0; q < kMaxC; ++q) {
+    const uint64_t before = q > 0 ? hiP[q - 1] : 0ull;
+    const uint64_t size = q < ncl ? hiP[q] - before : 1ull;  // >= 1 for a kept cluster (min_count >= 1)
+    ccount[q] = q < ncl ? (uint32_t)size : 0u;
+    tr[2 * q] = before + (size - 1) / 2;
+    tr[2 * q + 1] = before + (99 * size + 99) / 100 - 1;
+  }
+  // target grid bin: the smallest j with P[j] > rank (P is non-decreasing
+  // and P[G - 1] = n exceeds every rank), one ballot per target and chunk
+  int tj[kMaxT];
+#pragma unroll
+  for (int t = 0; t < kMaxT; ++t) tj[t] = G - 1;
+  uint32_t open = (1u << NT) - 1u;
+  for (int jb = 0; jb < G && open; jb += kWave) {
+    const int j = jb + l;
+    const uint64_t pj = j < G ? (uint64_t)P[j] : ~0ull;
+#pragma unroll
+    for (int t = 0; t < kMaxT; ++t) {
+      if ((open >> t) & 1u) {
+        const uint64_t bm = __ballot(pj > tr[t]);
+        if (bm) {
+          tj[t] = jb + __builtin_ctzll(bm);
+          open &= ~(1u << t);
         }
-        const uint64_t below = lo_j > 0 ? P[lo_j - 1] : 0;
-        if (l == 0) {
-          L.tlb[NT] = grid64_lb((lo + lo_j) << sh, L.th);
-          L.tub[NT] = grid64_lb((lo + lo_j + 1) << sh, L.th);
-          L.tpre[NT] = 0;
-          L.trank[NT] = r - below;
-          L.tpop[NT] = P[lo_j] - below;
-        }
-        ++NT;
       }
-      before = hiP;
+    }
+  }
+  {
+    int j = 0;
+    uint64_t r = 0;
+#pragma unroll
+    for (int t = 0; t < kMaxT; ++t)
+      if (t == l) {
+        j = tj[t];
+        r = tr[t];
+      }
+    if (l < NT) {
+      const uint64_t below = j > 0 ? P[j - 1] : 0;
+      L.tlb[l] = grid64_lb((lo + j) << sh, L.th);
+      L.tub[l] = grid64_lb((lo + j + 1) << sh, L.th);
+      L.tpre[l] = 0;
+      L.trank[l] = r - below;
+      L.tpop[l] = P[j] - below;
     }
   }
   wave_sync();
+
+  res.ncl = ncl;
+  res.NT = NT;
+  res.H = H;
+#pragma unroll
+  for (int q = 0; q < kMaxC; ++q) res.ccount[q] = ccount[q];
+  return true;
+}
+
+// One cell on one wavefront. Returns false when the cell needs a larger
+// tier (only for TIER < 2; nothing has been written for it then).
+template <int TIER>
+__device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, const CellMeta& cm,
+                             const uint64_t (&rv)[kRegVals]) {
+  constexpr int WORDS = CellLds<TIER>::W;
+  const int l = lane_id();
+  const uint32_t n = cm.n;
+  const uint64_t* vals = a.bucket + cm.off;
+  const int sh = 6 - a.sub_bits;
+  const int lo = grid64((uint64_t)cm.mn, L.th) >> sh;
+  const int G = (grid64((uint64_t)cm.mx, L.th) >> sh) - lo + 1;
+  if (TIER < 2 && G > WORDS) return false;
+  uint32_t* cgrid = L.buf;
+  const bool in_regs = n <= (uint32_t)(kWave * kRegVals);
+
+  // 1. grid histogram
+  for (int j = l; j < G; j += kWave) cgrid[j] = 0;
+  wave_sync();
+  bool out_of_range = false;
+  if (in_regs) {
+#pragma unroll
+    for (int r = 0; r < kRegVals; ++r) {
+      const uint32_t i = (uint32_t)(l + r * kWave);
+      if (i < n) {
+        const int x = (grid64(rv[r], L.th) >> sh) - lo;
+        if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
+        else out_of_range = true;
+      }
+    }
+  } else {
+    // four loads in flight per lane
+    for (uint64_t i0 = l; i0 < n; i0 += 4 * kWave) {
+      uint64_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (i0 + u * kWave >= n) break;
+        const int x = (grid64(v[u], L.th) >> sh) - lo;
+        if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
+        else out_of_range = true;
+      }
+    }
+  }
+  wave_sync();
+  if (__any(out_of_range)) {  // durations outside the summarized [min, max]
+    if (l == 0) flag(a, ARGUS_DEV_KDE_SUMMARY);
+    write_empty(a, c);
+    return true;
+  }
+
+  Analysis an;
+  if (!kde_analyze<TIER>(a, L, cm, lo, G, an)) return false;
+  const int ncl = an.ncl, NT = an.NT;
+  const int64_t H = an.H;
+  uint32_t ccount[kMaxC];
+#pragma unroll
+  for (int q = 0; q < kMaxC; ++q) ccount[q] = an.ccount[q];
 
   // 9a. a target bin with at most 64 durations is gathered into LDS (from
   // registers, or in one pass over the cell's durations for all such targets
@@ -669,7 +755,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
         for (int r = 0; r < kRegVals; ++r)
           if ((uint32_t)(l + r * kWave) < n) gather(rv[r]);
       } else {
-        for (uint32_t i0 = l; i0 < n; i0 += 4 * kWave) {
+        for (uint64_t i0 = l; i0 < n; i0 += 4 * kWave) {
           uint64_t v[4];
 #pragma unroll
           for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
@@ -684,11 +770,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
         const int k = (int)L.tpop[t];
         const uint64_t* list = lists + t * kWave;
         const uint64_t e = l < k ? list[l] : 0ull;
-        uint32_t rank = 0;
-        for (int j = 0; j < k; ++j) {
-          const uint64_t ej = list[j];
-          rank += (ej < e || (ej == e && j < l)) ? 1u : 0u;
-        }
+        const uint32_t rank = rank_in_list(list, k, e);
         const uint64_t hit = __ballot(l < k && (uint64_t)rank == L.trank[t]);
         const uint64_t val = readlane64(e, hit ? __builtin_ctzll(hit) : 0);
         if (l == 0) {
@@ -731,7 +813,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       for (int r = 0; r < kRegVals; ++r)
         if ((uint32_t)(l + r * kWave) < n) consider(rv[r]);
     } else {
-      for (uint32_t i0 = l; i0 < n; i0 += 4 * kWave) {
+      for (uint64_t i0 = l; i0 < n; i0 += 4 * kWave) {
         uint64_t v[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
@@ -882,6 +964,240 @@ __global__ __launch_bounds__(kWave, TIER == 0 ? 4 : 1) void kde_cell_kernel(KdeA
       load_small(a, m, cur);
       finish_or_hand_on<TIER>(a, L, c, m, cur);
     }
+  }
+}
+
+// --------------------------------------------------------- workgroup tier
+// Cells of at least kBlockMin durations, one 512-thread workgroup per cell:
+// every wavefront streams a share of the durations (four loads in flight per
+// lane) into the LDS grid histogram, wavefront 0 runs the analysis, and the
+// p50 / p99 targets are then resolved by selection passes in which all
+// threads stream the durations once more. Each target owns a region of
+// kSelRegion LDS words per pass: a histogram of the next kSelDigit bits of
+// its candidate range while more than kSelCap durations remain in it, else
+// the list of those durations, whose element of the wanted rank is found by
+// counting. Wavefront w resolves target w after each pass. Cells whose grid
+// or valleys do not fit go to tier 1 unchanged.
+constexpr int kBlockThreads = 512;
+constexpr uint32_t kBlockMin = 2048;
+constexpr int kSelRegion = Tier<1>::kWords / kMaxT;  // 512 words per target
+constexpr int kSelDigit = 9;                         // log2(kSelRegion)
+constexpr int kSelCap = 64;
+static_assert(kBlockThreads / kWave == kMaxT, "one wavefront per selection target");
+static_assert((1 << kSelDigit) == kSelRegion && 2 * kSelCap <= kSelRegion, "selection regions");
+
+__global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) {
+  __shared__ CellLds<1> L;
+  __shared__ uint32_t s_claim, s_nt, s_ok, s_bad;
+  const int tid = threadIdx.x, l = lane_id(), wv = tid / kWave;
+  if (tid < 64) L.th[tid] = a.theta[tid];
+  const int64_t cells = (int64_t)a.n_seg * a.K;
+  const uint32_t n_heavy = __hip_atomic_load(&a.counters[11], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int sh = 6 - a.sub_bits;
+  uint32_t* cgrid = L.buf;
+  while (true) {
+    if (tid == 0) {
+      s_claim = atomicAdd(&a.counters[10], 1u);
+      s_bad = 0;
+    }
+    __syncthreads();
+    const uint32_t claim = __builtin_amdgcn_readfirstlane(s_claim);
+    if (claim >= n_heavy) break;
+    const int64_t c = (int64_t)__builtin_amdgcn_readfirstlane(a.list2[cells - 1 - (int64_t)claim]);
+    const CellMeta cm = load_meta(a, c);  // checked when the cell was listed: off >= 0, n >= kBlockMin
+    const uint64_t n = cm.n;
+    const uint64_t* vals = a.bucket + cm.off;
+    const int lo = grid64((uint64_t)cm.mn, L.th) >> sh;
+    const int G = (grid64((uint64_t)cm.mx, L.th) >> sh) - lo + 1;
+    if (G > Tier<1>::kWords) {
+      if (tid == 0) a.list1[atomicAdd(&a.counters[2], 1u)] = (uint32_t)c;
+      __syncthreads();
+      continue;
+    }
+
+    // 1. grid histogram, all wavefronts
+    for (int j = tid; j < G; j += kBlockThreads) cgrid[j] = 0;
+    __syncthreads();
+    bool out_of_range = false;
+    for (uint64_t i0 = tid; i0 < n; i0 += 4 * kBlockThreads) {
+      uint64_t v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = i0 + u * kBlockThreads < n ? vals[i0 + u * kBlockThreads] : 0ull;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        if (i0 + u * kBlockThreads >= n) break;
+        const int x = (grid64(v[u], L.th) >> sh) - lo;
+        if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
+        else out_of_range = true;
+      }
+    }
+    if (out_of_range) s_bad = 1;
+    __syncthreads();
+    if (s_bad) {  // durations outside the summarized [min, max]
+      if (wv == 0) {
+        if (l == 0) flag(a, ARGUS_DEV_KDE_SUMMARY);
+        write_empty(a, c);
+      }
+      __syncthreads();
+      continue;
+    }
+
+    // 2-8. analysis on wavefront 0
+    Analysis an{};
+    if (wv == 0) {
+      const bool ok = kde_analyze<1>(a, L, cm, lo, G, an);
+      if (l == 0) {
+        s_ok = ok ? 1u : 0u;
+        s_nt = (uint32_t)an.NT;
+      }
+    }
+    __syncthreads();
+    if (!s_ok) {
+      if (tid == 0) a.list1[atomicAdd(&a.counters[2], 1u)] = (uint32_t)c;
+      __syncthreads();
+      continue;
+    }
+    const int NT = (int)__builtin_amdgcn_readfirstlane(s_nt);
+
+    // 9. selection passes: target t's candidates are the durations in
+    // [tlb, tub), of which tpop are there and the one of rank trank is wanted
+    if (tid < kMaxT) L.tdone[tid] = tid < NT && L.tub[tid] - L.tlb[tid] <= 1 ? 1u : 0u;
+    __syncthreads();
+    while (true) {
+      // per target, uniform: range start, width (0 once resolved), digit shift (-1: gather)
+      uint64_t tlo[kMaxT], twd[kMaxT];
+      int tsh[kMaxT];
+      uint32_t live = 0;
+#pragma unroll
+      for (int t = 0; t < kMaxT; ++t) {
+        tlo[t] = 0;
+        twd[t] = 0;
+        tsh[t] = -1;
+        if (t < NT && !L.tdone[t]) {
+          tlo[t] = readlane64(L.tlb[t], 0);
+          twd[t] = readlane64(L.tub[t] - L.tlb[t], 0);
+          const int bits = 64 - __builtin_clzll(twd[t] - 1);  // width >= 2
+          tsh[t] = (int)__builtin_amdgcn_readfirstlane(
+              L.tpop[t] <= (uint32_t)kSelCap ? -1 : (bits > kSelDigit ? bits - kSelDigit : 0));
+          live |= 1u << t;
+        }
+      }
+      live = __builtin_amdgcn_readfirstlane(live);
+      if (live == 0) break;
+      for (int i = tid; i < kMaxT * kSelRegion; i += kBlockThreads) L.buf[i] = 0;
+      if (tid < kMaxT) L.tcnt[tid] = 0;
+      __syncthreads();
+      auto consider = [&](uint64_t v) {
+#pragma unroll
+        for (int t = 0; t < kMaxT; ++t) {
+          const uint64_t u = v - tlo[t];
+          if (u < twd[t]) {
+            if (tsh[t] < 0) {
+              const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
+              if (slot < (uint32_t)kSelCap)
+                reinterpret_cast<uint64_t*>(L.buf + t * kSelRegion)[slot] = v;
+            } else {
+              atomicAdd(&L.buf[t * kSelRegion + (int)(u >> tsh[t])], 1u);
+            }
+          }
+        }
+      };
+      for (uint64_t i0 = tid; i0 < n; i0 += 4 * kBlockThreads) {
+        uint64_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = i0 + u * kBlockThreads < n ? vals[i0 + u * kBlockThreads] : 0ull;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (i0 + u * kBlockThreads < n) consider(v[u]);
+      }
+      __syncthreads();
+      // wavefront wv resolves target wv
+      if ((live >> wv) & 1u) {
+        const int t = wv;
+        const uint64_t r = readlane64(L.trank[t], 0);
+        const uint64_t base = readlane64(L.tlb[t], 0);
+        if (tsh[t] < 0) {
+          // counting rank among the gathered durations
+          const uint64_t* list = reinterpret_cast<const uint64_t*>(L.buf + t * kSelRegion);
+          const uint32_t got = L.tcnt[t];
+          const int k = got < (uint32_t)kSelCap ? (int)got : kSelCap;
+          const uint64_t e = l < k ? list[l] : 0ull;
+          const uint32_t rank = rank_in_list(list, k, e);
+          const uint64_t hit = __ballot(l < k && (uint64_t)rank == r);
+          const uint64_t val = readlane64(e, hit ? __builtin_ctzll(hit) : 0);
+          if (l == 0) {
+            L.tlb[t] = hit ? val : base;
+            L.tdone[t] = 1;
+          }
+        } else {
+          // the digit holding rank r: 8 counters per lane, a wave scan
+          constexpr int PER = kSelRegion / kWave;
+          const uint32_t* h = L.buf + t * kSelRegion + l * PER;
+          uint32_t cnt[PER], sum = 0;
+#pragma unroll
+          for (int k = 0; k < PER; ++k) {
+            cnt[k] = h[k];
+            sum += cnt[k];
+          }
+          const uint32_t incl = wave_incl_scan(sum);
+          const bool mine = (uint64_t)(incl - sum) <= r && r < (uint64_t)incl;
+          const uint64_t bm = __ballot(mine);
+          const int owner = bm ? __builtin_ctzll(bm) : 0;
+          uint32_t sub = 0, pop = 0;
+          uint64_t rr = 0;
+          if (l == owner) {
+            rr = bm ? r - (incl - sum) : 0;
+            int k = 0;
+#pragma unroll
+            for (int q = 0; q < PER - 1; ++q)
+              if (k == q && rr >= cnt[q]) {
+                rr -= cnt[q];
+                k = q + 1;
+              }
+            uint32_t pk = 0;
+#pragma unroll
+            for (int q = 0; q < PER; ++q)
+              if (q == k) pk = cnt[q];
+            sub = (uint32_t)(owner * PER + k);
+            pop = pk;
+          }
+          sub = __builtin_amdgcn_readlane(sub, owner);
+          pop = __builtin_amdgcn_readlane(pop, owner);
+          rr = readlane64(rr, owner);
+          const uint64_t nlo = base + ((uint64_t)sub << tsh[t]);
+          const uint64_t span = 1ull << tsh[t];
+          const uint64_t end = base + twd[t];
+          const uint64_t nhi = end - nlo < span ? end : nlo + span;
+          if (l == 0) {
+            L.tlb[t] = nlo;
+            L.tub[t] = nhi;
+            L.trank[t] = rr;
+            L.tpop[t] = pop;
+            L.tdone[t] = (nhi - nlo <= 1 || pop == 0) ? 1u : 0u;
+          }
+        }
+      }
+      __syncthreads();
+    }
+
+    // outputs (wavefront 0 holds the analysis)
+    if (wv == 0) {
+      if (l < kMaxC) {
+        const int64_t o = c * kMaxC + l;
+        uint32_t cnt = 0;
+#pragma unroll
+        for (int q = 0; q < kMaxC; ++q)
+          if (q == l) cnt = an.ccount[q];
+        a.cl_count[o] = l < an.ncl ? cnt : 0u;
+        a.p50[o] = l < an.ncl ? (int64_t)L.tlb[2 * l] : 0;
+        a.p99[o] = l < an.ncl ? (int64_t)L.tlb[2 * l + 1] : 0;
+      }
+      if (l == 0) {
+        a.n_clusters[c] = (uint8_t)an.ncl;
+        if (a.bw_q8) a.bw_q8[c] = (int32_t)an.H;
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -1157,6 +1473,9 @@ __global__ __launch_bounds__(kWave) void kde_lane_kernel(KdeArgs a) {
         const uint64_t zz[kMaxC] = {0, 0, 0, 0};
         lane_write(a, c, 0, z, zz, zz, 0);
         done = true;
+      } else if (kFirst && m.n >= kBlockMin) {
+        a.list2[C - 1 - (int64_t)atomicAdd(&a.counters[11], 1u)] = (uint32_t)c;
+        done = true;
       } else if (m.n <= (uint32_t)kLaneN) {
         const int G = (grid64((uint64_t)m.mx, L.th) >> sh) - (grid64((uint64_t)m.mn, L.th) >> sh) + 1;
         if (G <= GC) {
@@ -1300,19 +1619,20 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   if (cells == 0) return hipSuccess;
 
   // resident workgroups per kernel, cached per device
-  static std::atomic<int> grids[64][6];
+  static std::atomic<int> grids[64][7];
   int dev = 0;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  int g[6];
-  for (int i = 0; i < 6; ++i) g[i] = grids[dev][i].load();
+  int g[7];
+  for (int i = 0; i < 7; ++i) g[i] = grids[dev][i].load();
   if (g[0] == 0) grids[dev][0].store(g[0] = resident(kde_scatter_kernel, kScatterThreads));
   if (g[1] == 0) grids[dev][1].store(g[1] = resident(kde_cell_kernel<0>, kWave));
   if (g[2] == 0) grids[dev][2].store(g[2] = resident(kde_cell_kernel<1>, kWave));
   if (g[3] == 0) grids[dev][3].store(g[3] = resident(kde_cell_kernel<2>, kWave));
   if (g[4] == 0) grids[dev][4].store(g[4] = resident(kde_lane_kernel<kLaneG>, kWave));
   if (g[5] == 0) grids[dev][5].store(g[5] = resident(kde_lane_kernel<kLaneGW>, kWave));
-  for (int i = 0; i < 6; ++i)
+  if (g[6] == 0) grids[dev][6].store(g[6] = resident(kde_block_kernel, kBlockThreads));
+  for (int i = 0; i < 7; ++i)
     if (g[i] <= 0) return hipErrorInvalidDevice;
   hipLaunchKernelGGL(kde_scatter_kernel, dim3(l.n_seg < g[0] ? l.n_seg : g[0]), dim3(kScatterThreads), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -1320,6 +1640,8 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   hipLaunchKernelGGL(kde_lane_kernel<kLaneG>, dim3(chunks < g[4] ? (int)chunks : g[4]), dim3(kWave), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(kde_lane_kernel<kLaneGW>, dim3(g[5]), dim3(kWave), 0, st, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(kde_block_kernel, dim3(g[6]), dim3(kBlockThreads), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(kde_cell_kernel<0>, dim3(g[1]), dim3(kWave), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;

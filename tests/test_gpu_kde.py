@@ -148,7 +148,7 @@ def test_kde_hand_built_groups():
         # extremes of the duration range
         _spikes((2**63 - 1, 5), (2**62, 5), (3, 7)),
     ]
-    for n in (2, 5, 20, 100, 256, 257, 1000, 20000):
+    for n in (2, 5, 20, 100, 256, 257, 1000, 2047, 2048, 2049, 20000):
         groups.append(np.exp(rng.normal(np.log(80_000), 0.1, n)).astype(np.uint64))
     for sizes in [(500, 200, 50), (60, 60, 60), (1000, 2000), (300, 400, 4000, 400)]:
         comps = [np.exp(np.log(30_000 * 4**i) + 0.1 * np.clip(rng.normal(0, 1, m), -4, 4)).astype(np.uint64)
@@ -186,6 +186,26 @@ def test_kde_summary_mismatch_is_reported():
     assert (nc[bad] == 0).all()
     keep = np.setdiff1d(np.arange(len(nc)), bad)
     P.assert_kde_equal(k, {f: np.asarray(o[f])[keep] for f in P.KDE_FIELDS}, "mismatch", rows=keep)
+
+
+def test_kde_summary_mismatch_in_large_cells():
+    _announce("kde summary mismatch in cells of 3,000 and 50,000 durations")
+    rng = np.random.default_rng(5)
+    groups = [np.exp(rng.normal(np.log(50_000), 0.2, n)).astype(np.uint64) for n in (3000, 300, 50_000, 3000)]
+    K = len(groups)
+    ev = _groups_to_events(groups, K, 2)
+    ev_d = _dev(ev)
+    s = pa.summarize(ev_d, 1, 1, K, 2)
+    o = oracle.kde(ev, K, 2)
+    s["min_ns"][0] = s["max_ns"][0]  # durations below the summarized minimum
+    s["max_ns"][2] = s["min_ns"][2]  # and above the maximum
+    k = pa.kde(ev_d, s, 1, 1, K, 2)
+    torch.cuda.synchronize()
+    assert int(k["dev_status"].item()) == pa.argus.DEV_KDE_SUMMARY
+    nc = k["n_clusters"].cpu().numpy()
+    assert nc[0] == 0 and nc[2] == 0
+    keep = np.array([1, 3])
+    P.assert_kde_equal(k, {f: np.asarray(o[f])[keep] for f in P.KDE_FIELDS}, "large mismatch", rows=keep)
 
 
 @pytest.mark.parametrize("name,n_check", [("production", 96), ("cluster", 48), ("skew", 48)])
