@@ -9,11 +9,15 @@
 //               the cluster records of neighbouring ids are read together):
 //               present ranks, grid bounds lo / hi by 64-bit atomics,
 //               malformed records.
-//   w1_cdf      one lane per rank (64 ranks of one kernel id per wavefront):
-//               the count-weighted lognormal mixture of Eq. 2 at every grid
-//               point, quantised to 16 bits, into a [S][K][G][R] workspace
-//               (ranks contiguous, so the writes and the next kernel's reads
-//               are coalesced).
+//   w1_cdf      one lane per rank (64 ranks of one kernel id per wavefront,
+//               eight kernel ids per wavefront): the count-weighted lognormal
+//               mixture of Eq. 2 at every grid point, quantised to 16 bits,
+//               into a [S][K][G][R] workspace (ranks contiguous, so the
+//               writes and the next kernel's reads are coalesced). Phi comes
+//               from a cubic Hermite table (error below 2e-10); a grid point
+//               whose quantised value is not settled by that bound (within
+//               1e-4 of a step of 2^-16) is recomputed with erfc in double,
+//               the defining formula, so every output equals the erfc form.
 //   w1_score    one workgroup per (step, kernel): for each grid point the
 //               exact sums S_a = sum_b |q_a - q_b| over all present ranks
 //               from a counting sort of the 16-bit values in LDS (a
@@ -28,6 +32,10 @@
 //               flags.
 // The pairwise matrix of the paper is never formed: S_a is the row sum of
 // |F_a - F_b| at one grid point, which is all the mean-W1 score needs.
+#include <cmath>
+#include <mutex>
+#include <vector>
+
 #include "argus_internal.h"
 #include "argus_select.h"
 
@@ -40,6 +48,21 @@ constexpr int kMaxC = ARGUS_KDE_MAXC;
 constexpr double kZ99 = 2.326;                     // standard normal 99th percentile, as printed (Eq. 2)
 constexpr double kSqrt2 = 1.41421356237309504880;  // Phi(z) = erfc(-z / sqrt 2) / 2
 constexpr int kFineWords = 32768;                  // 65536 16-bit bin counters, two per word
+
+// Phi(z) by cubic Hermite interpolation on [-kPhiZ, kPhiZ] in steps of
+// 1/kPhiSteps; outside, 0 or 1 (Phi(-8) < 6.3e-16). The interpolation error
+// is at most h^4 / 384 max|Phi''''| <= 1.6e-10 (h = 1/64, |Phi''''| =
+// |z^3 - 3z| phi(z) <= 1.2), about 1e-5 of a 2^-16 step of the mixture; with
+// rounding the quantised value is certain once v +- kBand fall in one step.
+constexpr double kPhiZ = 8.0;
+constexpr int kPhiSteps = 64;
+constexpr int kPhiN = 2 * 8 * kPhiSteps;  // intervals
+constexpr double kBand = 1e-4;            // in units of 2^-16
+constexpr int kCdfKPerWave = 8;
+
+// per interval i (z from -kPhiZ + i / kPhiSteps), the cubic in t in [0, 1]:
+// c0 + t (c1 + t (c2 + t c3)); filled once per device from the host's erfc / exp
+__device__ double g_phi_tab[kPhiN * 4];
 
 struct W1Args {
   const uint8_t* ncl;
@@ -160,47 +183,98 @@ __device__ __forceinline__ void grid_of(const W1Args& a, int64_t sk, double& lnl
 }
 
 // -------------------------------------------------------------------- CDF
+__device__ __forceinline__ uint32_t quant16(double v) {
+  if (!(v > 0.0)) return 0u;
+  const double f = floor(v);
+  return f >= 65535.0 ? 65535u : (uint32_t)f;
+}
+
 __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
+  __shared__ double tab[kPhiN * 4];
+  for (int i = threadIdx.x; i < kPhiN * 4; i += 256) tab[i] = g_phi_tab[i];
+  __syncthreads();
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int k = blockIdx.x * 4 + w, r = blockIdx.y * 64 + lane, s = blockIdx.z;
-  if (k >= a.K || r >= a.R) return;
-  const int64_t sk = (int64_t)s * a.K + k;
-  if (!evaluated(a, a.o.n_present[sk])) return;
-  const int64_t c = cell_of(a, r, s, k);
-  uint32_t nc;
-  uint64_t tot;
-  if (cell_state(a, c, nc, tot) <= 0) return;
-  double mu[kMaxC], den[kMaxC], wt[kMaxC];
-  bool spread[kMaxC];
-#pragma unroll
-  for (int cl = 0; cl < kMaxC; ++cl) {
-    mu[cl] = den[cl] = wt[cl] = 0.0;
-    spread[cl] = false;
-    if ((uint32_t)cl >= nc) continue;
-    const int64_t p = a.p50[c * kMaxC + cl], t = a.p99[c * kMaxC + cl];
-    const double x = p > 1 ? (double)p : 1.0;
-    double y = t > 1 ? (double)t : 1.0;
-    if (y < x) y = x;
-    mu[cl] = log(x);
-    const double sigma = (log(y) - mu[cl]) / kZ99;
-    spread[cl] = sigma > 0.0;
-    den[cl] = sigma * kSqrt2;
-    wt[cl] = (double)a.cnt[c * kMaxC + cl] / (double)tot;
-  }
-  double lnlo, du;
-  grid_of(a, sk, lnlo, du);
-  uint16_t* out = a.q + (sk * a.G) * a.R + r;
-  for (int g = 0; g < a.G; ++g) {
-    const double u = lnlo + (double)g * du;
-    double F = 0.0;
+  const int r = blockIdx.y * 64 + lane, s = blockIdx.z;
+  if (r >= a.R) return;
+  for (int j = 0; j < kCdfKPerWave; ++j) {
+    const int k = (blockIdx.x * 4 + w) * kCdfKPerWave + j;
+    if (k >= a.K) break;
+    const int64_t sk = (int64_t)s * a.K + k;
+    if (!evaluated(a, a.o.n_present[sk])) continue;
+    const int64_t c = cell_of(a, r, s, k);
+    uint32_t nc;
+    uint64_t tot;
+    if (cell_state(a, c, nc, tot) <= 0) continue;
+    double mu[kMaxC], den[kMaxC], isg[kMaxC], wt[kMaxC];
+    bool spread[kMaxC];
 #pragma unroll
     for (int cl = 0; cl < kMaxC; ++cl) {
-      if ((uint32_t)cl >= nc) break;
-      const double phi = spread[cl] ? 0.5 * erfc((mu[cl] - u) / den[cl]) : (u >= mu[cl] ? 1.0 : 0.0);
-      F += wt[cl] * phi;
+      mu[cl] = den[cl] = isg[cl] = wt[cl] = 0.0;
+      spread[cl] = false;
+      if ((uint32_t)cl >= nc) continue;
+      const int64_t p = a.p50[c * kMaxC + cl], t = a.p99[c * kMaxC + cl];
+      const double x = p > 1 ? (double)p : 1.0;
+      double y = t > 1 ? (double)t : 1.0;
+      if (y < x) y = x;
+      mu[cl] = log(x);
+      const double sigma = (log(y) - mu[cl]) / kZ99;
+      spread[cl] = sigma > 0.0;
+      den[cl] = sigma * kSqrt2;
+      isg[cl] = spread[cl] ? 1.0 / sigma : 0.0;
+      wt[cl] = (double)a.cnt[c * kMaxC + cl] / (double)tot;
     }
-    const double v = floor(F * 65536.0);
-    out[(int64_t)g * a.R] = v >= 65535.0 ? (uint16_t)65535 : (uint16_t)(uint32_t)v;
+    double lnlo, du;
+    grid_of(a, sk, lnlo, du);
+    uint16_t* out = a.q + (sk * a.G) * a.R + r;
+    for (int gb = 0; gb < a.G; gb += 64) {
+      const int gn = a.G - gb < 64 ? a.G - gb : 64;
+      uint64_t unsure = 0;
+      for (int gi = 0; gi < gn; ++gi) {
+        const double u = lnlo + (double)(gb + gi) * du;
+        double F = 0.0;
+#pragma unroll
+        for (int cl = 0; cl < kMaxC; ++cl) {
+          if ((uint32_t)cl >= nc) break;
+          double ph;
+          if (!spread[cl]) {
+            ph = u >= mu[cl] ? 1.0 : 0.0;
+          } else {
+            const double z = (u - mu[cl]) * isg[cl];
+            if (z <= -kPhiZ) {
+              ph = 0.0;
+            } else if (z >= kPhiZ) {
+              ph = 1.0;
+            } else {
+              const double sx = (z + kPhiZ) * (double)kPhiSteps;
+              int i = (int)sx;
+              i = i < kPhiN - 1 ? i : kPhiN - 1;
+              const double t = sx - (double)i;
+              const double* cf = tab + 4 * i;
+              ph = cf[0] + t * (cf[1] + t * (cf[2] + t * cf[3]));
+            }
+          }
+          F += wt[cl] * ph;
+        }
+        const double v = F * 65536.0;
+        const uint32_t qa = quant16(v - kBand), qb = quant16(v + kBand);
+        if (qa == qb) out[(int64_t)(gb + gi) * a.R] = (uint16_t)qa;
+        else unsure |= 1ull << gi;
+      }
+      // grid points near a quantisation step: the defining erfc form
+      while (unsure) {
+        const int gi = __builtin_ctzll(unsure);
+        unsure &= unsure - 1;
+        const double u = lnlo + (double)(gb + gi) * du;
+        double F = 0.0;
+#pragma unroll
+        for (int cl = 0; cl < kMaxC; ++cl) {
+          if ((uint32_t)cl >= nc) break;
+          const double phi = spread[cl] ? 0.5 * erfc((mu[cl] - u) / den[cl]) : (u >= mu[cl] ? 1.0 : 0.0);
+          F += wt[cl] * phi;
+        }
+        out[(int64_t)(gb + gi) * a.R] = (uint16_t)quant16(F * 65536.0);
+      }
+    }
   }
 }
 
@@ -483,6 +557,33 @@ void launch_score(const W1Args& wa, hipStream_t st) {
   hipLaunchKernelGGL((w1_score<NT, V>), dim3((unsigned)((int64_t)wa.S * wa.K)), dim3(NT), 0, st, wa);
 }
 
+// Fill g_phi_tab on the current device once.
+hipError_t ensure_phi_table() {
+  static std::mutex mu;
+  static bool done[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (done[dev]) return hipSuccess;
+  std::vector<double> tab(kPhiN * 4);
+  const double h = 1.0 / kPhiSteps, inv_sqrt_2pi = 0.39894228040143267794;
+  auto Phi = [](double z) { return 0.5 * std::erfc(-z / kSqrt2); };
+  auto dphi = [&](double z) { return h * inv_sqrt_2pi * std::exp(-0.5 * z * z); };  // d Phi / d t
+  for (int i = 0; i < kPhiN; ++i) {
+    const double z0 = -kPhiZ + (double)i * h, z1 = -kPhiZ + (double)(i + 1) * h;
+    const double y0 = Phi(z0), y1 = Phi(z1), m0 = dphi(z0), m1 = dphi(z1);
+    tab[4 * i] = y0;
+    tab[4 * i + 1] = m0;
+    tab[4 * i + 2] = 3.0 * (y1 - y0) - 2.0 * m0 - m1;
+    tab[4 * i + 3] = 2.0 * (y0 - y1) + m0 + m1;
+  }
+  e = hipMemcpyToSymbol(HIP_SYMBOL(g_phi_tab), tab.data(), sizeof(double) * tab.size());
+  if (e == hipSuccess) done[dev] = true;
+  return e;
+}
+
 }  // namespace
 
 size_t w1_workspace_bytes(int32_t R, int32_t S, int32_t K, int32_t G) {
@@ -494,13 +595,16 @@ hipError_t launch_w1(const W1Launch& l, hipStream_t st) {
   W1Args wa{l.n_clusters, l.count, l.p50, l.p99, l.R, l.S, l.K, l.p.grid, l.p.min_ranks, l.p.alpha_pm, l.o,
             static_cast<uint16_t*>(l.workspace)};
   const int64_t SK = (int64_t)l.S * l.K;
+  hipError_t e = ensure_phi_table();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(w1_init, dim3((unsigned)((SK + 255) / 256)), dim3(256), 0, st, wa);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(w1_bounds, dim3((l.K + 63) / 64, (l.R + 63) / 64, l.S), dim3(256), 0, st, wa);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(w1_cdf, dim3((l.K + 3) / 4, (l.R + 63) / 64, l.S), dim3(256), 0, st, wa);
+  hipLaunchKernelGGL(w1_cdf, dim3((l.K + 4 * kCdfKPerWave - 1) / (4 * kCdfKPerWave), (l.R + 63) / 64, l.S), dim3(256),
+                     0, st, wa);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // register-resident slots per thread: R <= 1024 with 256 threads, else 1024 threads
