@@ -38,6 +38,18 @@ __device__ __forceinline__ void lds_store(T* p, T v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
+// Workgroup barrier that orders LDS only. __syncthreads() also releases
+// global memory at workgroup scope, which on gfx950 waits for every vector
+// memory operation of the wave (loads and stores share one counter),
+// including prefetched loads still in flight. Where threads of a workgroup
+// exchange data only through LDS, this barrier keeps those loads (and
+// stores) in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // 64-lane wavefront reductions (gfx950 runs wave64 only).
 __device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

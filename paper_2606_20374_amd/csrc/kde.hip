@@ -273,6 +273,305 @@ __global__ __launch_bounds__(kScatterThreads) void kde_scatter_kernel(KdeArgs a)
   }
 }
 
+// ----------------------------------------------------------- staged scatter
+// For id spaces of up to kStageK kernel ids. Scattering each duration with
+// its own 8-byte store leaves partly written cache lines for the many rare
+// kernel ids, and HBM then writes about twice the durations' bytes. Here
+// each kernel id keeps a window of kStageW positions, [done, done + 8), in
+// LDS; a duration whose position falls inside the window is staged, any
+// later one (a frequent id within one round) is stored directly. After each
+// round of 8,192 events the workgroup writes out the staged positions up to
+// the last complete aligned group of 8 (64 bytes), or all of them when the
+// id overflowed its window, and advances the window. The rule that decides
+// staged or direct reads only the window start, which changes between
+// rounds, so the result does not depend on when the flushes happen. The
+// workgroup shares only LDS state, so its barriers order LDS alone and the
+// next round's loads stay in flight across them.
+constexpr int kStageThreads = 1024;
+constexpr int kStageK = 2048;
+constexpr int kStageW = 8;
+constexpr int kStageD = 2;  // groups of four events per thread and round
+
+struct StageCtx {
+  uint64_t (*stage)[kStageW];
+  uint32_t* cur;
+  const uint32_t* done;
+  uint64_t* out;
+  uint32_t len, lo7;  // segment length; lo mod 8, the global alignment of local position 0
+  int32_t K, NS;
+};
+
+__device__ __forceinline__ void stage_one(const StageCtx& s, int32_t kid, int32_t st, int64_t t0, int64_t t1) {
+  if (kid >= 0 && kid < s.K && st >= 0 && st < s.NS && t0 >= 0 && t1 >= t0) {
+    const uint32_t p = atomicAdd(&s.cur[kid], 1u);
+    const uint64_t d = (uint64_t)t1 - (uint64_t)t0;
+    if (p - s.done[kid] < (uint32_t)kStageW) s.stage[kid][(p + s.lo7) & (kStageW - 1)] = d;
+    else if (p < s.len) s.out[p] = d;
+  }
+}
+
+// Write out kernel id k's staged positions: up to the last complete aligned
+// group, everything when the window overflowed, or everything (final).
+__device__ __forceinline__ void stage_flush(const StageCtx& s, uint32_t* done, int k, bool final) {
+  const uint32_t c = s.cur[k], dn = done[k];
+  if (c == dn) return;
+  uint32_t e, nd;
+  if (c - dn > (uint32_t)kStageW) {
+    e = dn + kStageW;
+    nd = c;
+  } else if (final) {
+    e = nd = c;
+  } else {
+    const int64_t al = (int64_t)((c + s.lo7) & ~(uint32_t)(kStageW - 1)) - (int64_t)s.lo7;
+    if (al <= (int64_t)dn) return;
+    e = nd = (uint32_t)al;
+  }
+  for (uint32_t p = dn; p < e; ++p)
+    if (p < s.len) s.out[p] = s.stage[k][(p + s.lo7) & (kStageW - 1)];
+  done[k] = nd;
+}
+
+// Buffer-resource variants for segments below kBufEvents events. On gfx950
+// stores and loads share one wait counter, so a store whose issue depends on
+// data (staged or not) leaves the compiler unable to count what follows a
+// prefetched load, and it waits for everything, prefetch included, before
+// each use. Here every step issues a fixed set of memory instructions:
+// loads past the end read zeros, and a lane with nothing to store gives an
+// offset past the buffer, which the hardware drops.
+typedef unsigned v2u __attribute__((ext_vector_type(2)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
+constexpr uint32_t kOob = 0x80000000u;   // past every buffer below (all under 2^31 bytes)
+constexpr int64_t kBufEvents = 1ll << 26;  // 2^26 events of 8 bytes: 512 MB per buffer
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ void buf_store_u64(__amdgpu_buffer_rsrc_t r, uint32_t off, uint64_t v) {
+  __builtin_amdgcn_raw_buffer_store_b64(v2u{(uint32_t)v, (uint32_t)(v >> 32)}, r, (int)off, 0, 0);
+}
+
+__device__ __forceinline__ void stage_one_buf(const StageCtx& s, __amdgpu_buffer_rsrc_t ro, bool ok, int32_t kid,
+                                              int32_t st, int64_t t0, int64_t t1) {
+  const uint64_t d = (uint64_t)t1 - (uint64_t)t0;
+  uint32_t off = kOob;
+  if (ok && kid >= 0 && kid < s.K && st >= 0 && st < s.NS && t0 >= 0 && t1 >= t0) {
+    const uint32_t p = atomicAdd(&s.cur[kid], 1u);
+    if (p - s.done[kid] < (uint32_t)kStageW) s.stage[kid][(p + s.lo7) & (kStageW - 1)] = d;
+    else if (p < s.len) off = p * 8u;
+  }
+  buf_store_u64(ro, off, d);
+}
+
+// Flushes of the buffer path in two phases. Plan: each id with staged
+// positions to write (as stage_flush decides) takes an entry of an LDS list
+// of kFlushCap; ids that find the list full keep their positions staged for
+// a later round (the staging rule allows any flush time). Write: one lane
+// per (entry, position), kFlushCap * kStageW / kStageThreads stores per
+// thread whether used or not.
+constexpr int kFlushCap = 512;
+
+struct FlushEntry {
+  uint32_t k, dn, e, nd;
+};
+
+__device__ __forceinline__ void stage_plan(const StageCtx& s, const uint32_t* done, int k, FlushEntry* list,
+                                           uint32_t* n_list) {
+  uint32_t dn = 0, e = 0, nd = 0;
+  bool act = false;
+  if (k < s.K) {
+    const uint32_t c = s.cur[k];
+    dn = done[k];
+    if (c - dn > (uint32_t)kStageW) {
+      e = dn + kStageW;
+      nd = c;
+      act = true;
+    } else if (c != dn) {
+      const int64_t al = (int64_t)((c + s.lo7) & ~(uint32_t)(kStageW - 1)) - (int64_t)s.lo7;
+      if (al > (int64_t)dn) {
+        e = nd = (uint32_t)al;
+        act = true;
+      }
+    }
+  }
+  // one list claim per wavefront
+  const uint64_t m = __ballot(act);
+  uint32_t base = 0;
+  const int leader = m ? __builtin_ctzll(m) : 0;
+  if (m && lane_id() == leader) base = atomicAdd(n_list, (uint32_t)__popcll(m));
+  base = __builtin_amdgcn_readlane(base, leader);
+  const uint32_t idx = base + (uint32_t)__popcll(m & ((1ull << lane_id()) - 1ull));
+  if (act && idx < (uint32_t)kFlushCap) list[idx] = FlushEntry{(uint32_t)k, dn, e, nd};
+}
+
+__device__ __forceinline__ void stage_write(const StageCtx& s, __amdgpu_buffer_rsrc_t ro, uint32_t* done,
+                                            const FlushEntry* list, uint32_t n_list, int tid) {
+  const uint32_t n = n_list < (uint32_t)kFlushCap ? n_list : (uint32_t)kFlushCap;
+#pragma unroll
+  for (int j = 0; j < kFlushCap * kStageW / kStageThreads; ++j) {
+    const uint32_t slot = (uint32_t)(j * kStageThreads + tid);
+    const uint32_t ent = slot / kStageW, i = slot % kStageW;
+    uint32_t off = kOob;
+    uint64_t v = 0;
+    if (ent < n) {
+      const FlushEntry f = list[ent];
+      const uint32_t p = f.dn + i;
+      if (p < f.e && p < s.len) {
+        off = p * 8u;
+        v = s.stage[f.k][(p + s.lo7) & (kStageW - 1)];
+      }
+      if (i == 0) done[f.k] = f.nd;
+    }
+    buf_store_u64(ro, off, v);
+  }
+}
+
+__global__ __launch_bounds__(kStageThreads) void kde_scatter_staged_kernel(KdeArgs a) {
+  __shared__ uint64_t stage[kStageK][kStageW];
+  __shared__ uint32_t cur[kStageK], done[kStageK];
+  __shared__ uint32_t wave_tot[kStageThreads / kWave];
+  __shared__ uint32_t claim, n_list;
+  __shared__ FlushEntry list[kFlushCap];
+  const int tid = threadIdx.x, K = a.K;
+  const int per = (K + kStageThreads - 1) / kStageThreads;
+  const v4i* K4 = reinterpret_cast<const v4i*>(a.kernel_id);
+  const v4i* S4 = reinterpret_cast<const v4i*>(a.stream);
+  const v2l* T0 = reinterpret_cast<const v2l*>(a.start_ns);
+  const v2l* T1 = reinterpret_cast<const v2l*>(a.end_ns);
+  while (true) {
+    if (tid == 0) claim = atomicAdd(&a.counters[0], 1u);
+    lds_barrier();
+    const uint32_t g = claim;
+    if (g >= (uint32_t)a.n_seg) break;
+    // cursors = exclusive prefix of the segment's per-kernel counts
+    const uint32_t* cnt = a.count + (int64_t)g * K;
+    const int k0 = tid * per, k1 = min(K, k0 + per);
+    uint32_t own = 0;
+    for (int k = k0; k < k1; ++k) own += cnt[k];
+    const uint32_t incl = wave_incl_scan(own);
+    if (lane_id() == kWave - 1) wave_tot[tid / kWave] = incl;
+    lds_barrier();
+    uint32_t base = incl - own;
+    for (int w = 0; w < tid / kWave; ++w) base += wave_tot[w];
+    for (int k = k0; k < k1; ++k) {
+      cur[k] = done[k] = base;
+      base += cnt[k];
+    }
+    lds_barrier();
+    const int64_t lo = a.seg_off[g], hi = a.seg_off[g + 1];
+    const bool bad = !(lo >= 0 && lo <= hi && hi <= a.n_events && hi - lo <= (int64_t)UINT32_MAX);
+    const StageCtx s{stage, cur, done, a.bucket + (bad ? 0 : lo), bad ? 0u : (uint32_t)(hi - lo),
+                     bad ? 0u : (uint32_t)(lo & 7), K, a.NS};
+    if (!bad) {
+      int64_t a4 = hi, b4 = hi;  // aligned body [a4, b4) in groups of four events
+      if (a.vec_ok) {
+        const int64_t up = (lo + 3) & ~(int64_t)3, dn = hi & ~(int64_t)3;
+        a4 = up < hi ? up : hi;
+        b4 = dn > a4 ? dn : a4;
+      }
+      // head [lo, a4) (the whole segment without aligned arrays) and tail [b4, hi)
+      for (int64_t i = lo + tid; i < a4; i += kStageThreads)
+        stage_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
+      for (int64_t i = b4 + tid; i < hi; i += kStageThreads)
+        stage_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
+      const int64_t qa = a4 >> 2, qb = b4 >> 2;
+      if (hi - lo <= kBufEvents) {
+        // rounds of kStageD groups of four events per thread with the next
+        // round's groups in flight, every step the same memory instructions;
+        // staged windows are flushed after every round
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the head / tail stores above are done
+        const int64_t ng = qb - qa;
+        const __amdgpu_buffer_rsrc_t rk = buf_rsrc(a.kernel_id + a4, ng * 16), rs = buf_rsrc(a.stream + a4, ng * 16);
+        const __amdgpu_buffer_rsrc_t r0 = buf_rsrc(a.start_ns + a4, ng * 32), r1 = buf_rsrc(a.end_ns + a4, ng * 32);
+        const __amdgpu_buffer_rsrc_t ro = buf_rsrc(s.out, (int64_t)s.len * 8);
+        v4u bk[kStageD], bs[kStageD], ba0[kStageD], ba1[kStageD], bb0[kStageD], bb1[kStageD];
+        auto load = [&](int d, int64_t rq) {
+          const uint32_t o16 = rq < ng ? (uint32_t)rq * 16u : kOob, o32 = rq < ng ? (uint32_t)rq * 32u : kOob;
+          bk[d] = __builtin_amdgcn_raw_buffer_load_b128(rk, (int)o16, 0, 0);
+          bs[d] = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)o16, 0, 0);
+          ba0[d] = __builtin_amdgcn_raw_buffer_load_b128(r0, (int)o32, 0, 0);
+          ba1[d] = __builtin_amdgcn_raw_buffer_load_b128(r0, (int)(o32 + 16u), 0, 0);
+          bb0[d] = __builtin_amdgcn_raw_buffer_load_b128(r1, (int)o32, 0, 0);
+          bb1[d] = __builtin_amdgcn_raw_buffer_load_b128(r1, (int)(o32 + 16u), 0, 0);
+        };
+#pragma unroll
+        for (int d = 0; d < kStageD; ++d) load(d, tid + (int64_t)d * kStageThreads);
+        for (int64_t rb = 0; rb < ng; rb += (int64_t)kStageD * kStageThreads) {
+#pragma unroll
+          for (int d = 0; d < kStageD; ++d) {
+            const int64_t rq = rb + tid + (int64_t)d * kStageThreads;
+            const v4i k4 = __builtin_bit_cast(v4i, bk[d]), s4 = __builtin_bit_cast(v4i, bs[d]);
+            const v2l x0 = __builtin_bit_cast(v2l, ba0[d]), x1 = __builtin_bit_cast(v2l, ba1[d]);
+            const v2l y0 = __builtin_bit_cast(v2l, bb0[d]), y1 = __builtin_bit_cast(v2l, bb1[d]);
+            load(d, rq + (int64_t)kStageD * kStageThreads);
+            const bool ok = rq < ng;
+            stage_one_buf(s, ro, ok, k4.x, s4.x, x0.x, y0.x);
+            stage_one_buf(s, ro, ok, k4.y, s4.y, x0.y, y0.y);
+            stage_one_buf(s, ro, ok, k4.z, s4.z, x1.x, y1.x);
+            stage_one_buf(s, ro, ok, k4.w, s4.w, x1.y, y1.y);
+          }
+          if (tid == 0) n_list = 0;
+          lds_barrier();
+#pragma unroll
+          for (int kk = 0; kk < kStageK / kStageThreads; ++kk) stage_plan(s, done, tid + kk * kStageThreads, list, &n_list);
+          lds_barrier();
+          stage_write(s, ro, done, list, n_list, tid);
+          lds_barrier();
+        }
+      } else {
+        // segments too long for 32-bit buffer offsets: the same rounds with
+        // global loads and stores
+        v4i bk[kStageD], bs[kStageD];
+        v2l ba0[kStageD], ba1[kStageD], bb0[kStageD], bb1[kStageD];
+#pragma unroll
+        for (int d = 0; d < kStageD; ++d) {
+          const int64_t q = qa + tid + (int64_t)d * kStageThreads;
+          bk[d] = bs[d] = 0;
+          ba0[d] = ba1[d] = bb0[d] = bb1[d] = 0;
+          if (q < qb) {
+            bk[d] = __builtin_nontemporal_load(K4 + q);
+            bs[d] = __builtin_nontemporal_load(S4 + q);
+            ba0[d] = __builtin_nontemporal_load(T0 + 2 * q);
+            ba1[d] = __builtin_nontemporal_load(T0 + 2 * q + 1);
+            bb0[d] = __builtin_nontemporal_load(T1 + 2 * q);
+            bb1[d] = __builtin_nontemporal_load(T1 + 2 * q + 1);
+          }
+        }
+        for (int64_t r0 = qa; r0 < qb; r0 += (int64_t)kStageD * kStageThreads) {
+#pragma unroll
+          for (int d = 0; d < kStageD; ++d) {
+            const int64_t q = r0 + tid + (int64_t)d * kStageThreads;
+            const v4i k4 = bk[d], s4 = bs[d];
+            const v2l x0 = ba0[d], x1 = ba1[d], y0 = bb0[d], y1 = bb1[d];
+            const int64_t qn = q + (int64_t)kStageD * kStageThreads;
+            if (qn < qb) {
+              bk[d] = __builtin_nontemporal_load(K4 + qn);
+              bs[d] = __builtin_nontemporal_load(S4 + qn);
+              ba0[d] = __builtin_nontemporal_load(T0 + 2 * qn);
+              ba1[d] = __builtin_nontemporal_load(T0 + 2 * qn + 1);
+              bb0[d] = __builtin_nontemporal_load(T1 + 2 * qn);
+              bb1[d] = __builtin_nontemporal_load(T1 + 2 * qn + 1);
+            }
+            if (q < qb) {
+              stage_one(s, k4.x, s4.x, x0.x, y0.x);
+              stage_one(s, k4.y, s4.y, x0.y, y0.y);
+              stage_one(s, k4.z, s4.z, x1.x, y1.x);
+              stage_one(s, k4.w, s4.w, x1.y, y1.y);
+            }
+          }
+          lds_barrier();
+          for (int k = tid; k < K; k += kStageThreads) stage_flush(s, done, k, false);
+          lds_barrier();
+        }
+      }
+    }
+    for (int k = tid; k < K; k += kStageThreads) stage_flush(s, done, k, true);
+    uint32_t* ends = a.cell_end + (int64_t)g * K;
+    for (int k = tid; k < K; k += kStageThreads) ends[k] = cur[k];
+    lds_barrier();
+  }
+}
+
 // -------------------------------------------------------------------- cells
 
 template <int TIER>
@@ -1619,12 +1918,12 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   if (cells == 0) return hipSuccess;
 
   // resident workgroups per kernel, cached per device
-  static std::atomic<int> grids[64][7];
+  static std::atomic<int> grids[64][8];
   int dev = 0;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  int g[7];
-  for (int i = 0; i < 7; ++i) g[i] = grids[dev][i].load();
+  int g[8];
+  for (int i = 0; i < 8; ++i) g[i] = grids[dev][i].load();
   if (g[0] == 0) grids[dev][0].store(g[0] = resident(kde_scatter_kernel, kScatterThreads));
   if (g[1] == 0) grids[dev][1].store(g[1] = resident(kde_cell_kernel<0>, kWave));
   if (g[2] == 0) grids[dev][2].store(g[2] = resident(kde_cell_kernel<1>, kWave));
@@ -1632,9 +1931,13 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   if (g[4] == 0) grids[dev][4].store(g[4] = resident(kde_lane_kernel<kLaneG>, kWave));
   if (g[5] == 0) grids[dev][5].store(g[5] = resident(kde_lane_kernel<kLaneGW>, kWave));
   if (g[6] == 0) grids[dev][6].store(g[6] = resident(kde_block_kernel, kBlockThreads));
-  for (int i = 0; i < 7; ++i)
+  if (g[7] == 0) grids[dev][7].store(g[7] = resident(kde_scatter_staged_kernel, kStageThreads));
+  for (int i = 0; i < 8; ++i)
     if (g[i] <= 0) return hipErrorInvalidDevice;
-  hipLaunchKernelGGL(kde_scatter_kernel, dim3(l.n_seg < g[0] ? l.n_seg : g[0]), dim3(kScatterThreads), 0, st, a);
+  if (l.n_kernels <= kStageK)
+    hipLaunchKernelGGL(kde_scatter_staged_kernel, dim3(l.n_seg < g[7] ? l.n_seg : g[7]), dim3(kStageThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL(kde_scatter_kernel, dim3(l.n_seg < g[0] ? l.n_seg : g[0]), dim3(kScatterThreads), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int64_t chunks = (cells + kWave - 1) / kWave;
   hipLaunchKernelGGL(kde_lane_kernel<kLaneG>, dim3(chunks < g[4] ? (int)chunks : g[4]), dim3(kWave), 0, st, a);

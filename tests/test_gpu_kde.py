@@ -188,6 +188,39 @@ def test_kde_summary_mismatch_is_reported():
     P.assert_kde_equal(k, {f: np.asarray(o[f])[keep] for f in P.KDE_FIELDS}, "mismatch", rows=keep)
 
 
+def _dev_unaligned(ev):
+    """Device copies whose event arrays start 4 or 8 bytes past a 16-byte
+    boundary: the kernels must take their element-wise load paths."""
+    out = {}
+    for k, v in ev.items():
+        t = torch.from_numpy(np.ascontiguousarray(v))
+        if k == "seg_off":
+            out[k] = t.to(DEV)
+            continue
+        buf = torch.empty(t.numel() + 1, dtype=t.dtype, device=DEV)
+        out[k] = buf[1:]
+        out[k].copy_(t.to(DEV))
+        assert out[k].data_ptr() % 16 != 0
+    return out
+
+
+def test_kde_unaligned_event_arrays():
+    _announce("kde with event arrays off 16-byte alignment (tiny trace, cells of 40 to 6,000 durations)")
+    t = tracegen.make("tiny")
+    c = t.cfg
+    ev = t.fill_host()
+    _, k = _kde_gpu(_dev_unaligned(ev), c.n_ranks, c.n_steps, c.n_kernels, c.n_streams)
+    P.assert_kde_equal(k, oracle.kde(ev, c.n_kernels, c.n_streams), "tiny unaligned")
+    assert int(k["dev_status"].item()) == 0
+    rng = np.random.default_rng(12)
+    groups = [np.exp(rng.normal(np.log(30_000 * 3**i), 0.15, n)).astype(np.uint64)
+              for i, n in enumerate((6000, 40, 700, 2500, 9, 3000))]
+    ev = _groups_to_events(groups, len(groups), 3)
+    _, k = _kde_gpu(_dev_unaligned(ev), 1, 1, len(groups), 3)
+    P.assert_kde_equal(k, oracle.kde(ev, len(groups), 3), "groups unaligned")
+    assert int(k["dev_status"].item()) == 0
+
+
 def test_kde_summary_mismatch_in_large_cells():
     _announce("kde summary mismatch in cells of 3,000 and 50,000 durations")
     rng = np.random.default_rng(5)

@@ -93,6 +93,28 @@ def test_ragged_corrupt_segments():
     P.assert_int_equal(g, o, P.SUM_INT_FIELDS, "ragged")
 
 
+def test_unaligned_event_arrays():
+    _announce("summarize with event arrays off 16-byte alignment")
+    t = tracegen.make("tiny", invalid_ppm=3000)
+    c = t.cfg
+    ev = t.fill_host()
+    d = {}
+    for k, v in ev.items():
+        h = torch.from_numpy(np.ascontiguousarray(v))
+        if k == "seg_off":
+            d[k] = h.to(DEV)
+            continue
+        buf = torch.empty(h.numel() + 1, dtype=h.dtype, device=DEV)
+        d[k] = buf[1:]
+        d[k].copy_(h.to(DEV))
+        assert d[k].data_ptr() % 16 != 0
+    g = pa.summarize(d, c.n_ranks, c.n_steps, c.n_kernels, c.n_streams)
+    torch.cuda.synchronize()
+    o = oracle.summarize(ev, c.n_kernels, c.n_streams)
+    P.assert_int_equal(g, o, P.SUM_INT_FIELDS, "unaligned")
+    assert int(g["dev_status"].item()) == 0
+
+
 def test_hand_built_edge_events():
     _announce("hand-built edge events")
     base = 2**60 + 7
