@@ -85,15 +85,20 @@ struct KdeArgs {
   int32_t* dev_status;
   // [0] scatter queue, [1] tier-0 queue, [2] list-1 length, [3] list-1 queue,
   // [4] list-2 length, [5] list-2 queue, [6] first lane pass queue, [7] list-0 length,
-  // [8] wide lane pass queue, [9] wide list length, [10] workgroup tier queue, [11] heavy list length
+  // [8] wide lane pass queue, [9] wide list length, [10] workgroup tier queue, [11] heavy list length,
+  // [12] lane list length
   uint32_t* counters;
   uint64_t* bucket;    // [n_events]: segment g's durations at seg_off[g] + local position
   uint32_t* cell_end;  // [cells]: local end offset of each cell's durations
-  uint32_t* list1;     // [cells]: wide cells for the second lane pass, later cells handed from the
-                       // workgroup tier and tier 0 to tier 1 (the wide list is consumed first)
+  uint32_t* list1;     // [cells]: the cells of the wide lane pass (from the bottom) and of the
+                       // first lane pass (from the top), each in cost-class order; later
+                       // cells handed from the workgroup tier and tier 0 to tier 1 (both lane
+                       // lists are consumed first)
   uint32_t* list2;     // [cells]: cells handed from the lane tier to tier 0 (list 0, from the bottom) and
                        // to the workgroup tier (heavy list, from the top), later from tier 1 to tier 2
                        // (both are consumed before tier 1 starts)
+  uint16_t* lane_key;  // [cells]: route code (a lane pass's cost class, heavy, tier 0, or none)
+  uint32_t* lane_cls;  // [2 * 1024]: cells per cost class, then the classes' fill cursors
   uint32_t theta[64];  // ceil(2^(23 + t/64))
 };
 
@@ -565,6 +570,9 @@ __global__ __launch_bounds__(kStageThreads) void kde_scatter_staged_kernel(KdeAr
         }
       }
     }
+    // every staging write and cursor increment of the segment (the head and
+    // tail, and the element-wise path, run without a round barrier after them)
+    lds_barrier();
     for (int k = tid; k < K; k += kStageThreads) stage_flush(s, done, k, true);
     uint32_t* ends = a.cell_end + (int64_t)g * K;
     for (int k = tid; k < K; k += kStageThreads) ends[k] = cur[k];
@@ -1741,10 +1749,175 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
   return true;
 }
 
-// Lane passes. GC = kLaneG: every cell, 64 consecutive cells per claim;
-// cells of up to kLaneN durations whose grid has 65 .. kLaneGW points go to
-// the wide list, the rest that does not fit to list 0. GC = kLaneGW: the
-// wide list, 64 entries per claim; what does not fit goes to list 0.
+// ------------------------------------------------------------------ routing
+// Before the lane passes every cell is routed once, one thread per cell:
+// empty cells (and cells whose summary does not match the buckets) are
+// written, heavy cells go to the workgroup tier's list, cells too large for
+// either lane pass to tier 0's list, and the rest to one of the two lane
+// passes, ordered by a cost class. A lane pass runs 64 cells in lockstep, so
+// a wavefront takes as long as its costliest cell, and cells in kernel-id
+// order mix grids of 10 and 64 points and 10 and 255 durations. The class
+// groups cells of similar grid size and duration count, whose loops run
+// similar trip counts: ((G - 1) / 2, (n - 1) / 16) for the first lane pass
+// (G <= 64), kLaneClasses + ((G - 65) / 8, (n - 1) / 16) for the wide pass
+// (65 <= G <= 256). A counting sort over the classes (counts here,
+// positions in kde_lane_order_kernel) lays each lane list out in class
+// order. Each workgroup routes a contiguous range of cells and claims its
+// list ranges with one atomic per list and class.
+constexpr int kRouteThreads = 512;
+constexpr int kLaneClasses = 512;                          // 32 grid-size x 16 duration-count classes
+constexpr int kWideClasses = 384;                          // 24 x 16 for the wide pass
+constexpr int kClasses = 1024;                             // both, padded to two per thread
+constexpr uint16_t kNoClass = 0xFFFF, kHeavy = 0xFFFE, kTier0 = 0xFFFD;
+constexpr int kOrderPer = 16;  // cells per thread and round in kde_lane_order_kernel
+static_assert(kClasses == 2 * kRouteThreads && kLaneClasses + kWideClasses <= kClasses, "class scan");
+static_assert(((kLaneG - 1) >> 1) * 16 + ((kLaneN - 1) >> 4) < kLaneClasses, "lane classes");
+static_assert(((kLaneGW - 65) >> 3) * 16 + ((kLaneN - 1) >> 4) < kWideClasses, "wide classes");
+
+// Route code of a cell from its checked summary: a class, kHeavy, kTier0, or
+// kNoClass (nothing left to do: the empty record is written by the caller).
+__device__ __forceinline__ uint16_t route_code(const CellMeta& m, const uint32_t* th, int sh) {
+  if (m.n == 0 || m.off < 0) return kNoClass;
+  if (m.n >= kBlockMin) return kHeavy;
+  if (m.n > (uint32_t)kLaneN) return kTier0;
+  const int G = (grid64((uint64_t)m.mx, th) >> sh) - (grid64((uint64_t)m.mn, th) >> sh) + 1;
+  const int nq = (int)((m.n - 1) >> 4);
+  if (G <= kLaneG) return (uint16_t)(((G - 1) >> 1) * 16 + nq);
+  if (G <= kLaneGW) return (uint16_t)(kLaneClasses + ((G - 65) >> 3) * 16 + nq);
+  return kTier0;
+}
+
+// Index for each lane with pred among the new entries of an LDS list
+// counter: one atomic per wavefront. Called by every lane of the wavefront.
+__device__ __forceinline__ uint32_t wave_append(uint32_t* counter, bool pred) {
+  const uint64_t m = __ballot(pred);
+  if (m == 0) return 0;
+  const int leader = __builtin_ctzll(m);
+  uint32_t base = 0;
+  if (lane_id() == leader) base = atomicAdd(counter, (uint32_t)__popcll(m));
+  base = __builtin_amdgcn_readlane(base, leader);
+  return base + (uint32_t)__popcll(m & ((1ull << lane_id()) - 1ull));
+}
+
+// Contiguous range of cells of workgroup b out of nb.
+__device__ __forceinline__ void cell_range(int64_t C, int64_t b, int64_t nb, int64_t& c0, int64_t& c1) {
+  const int64_t per = (C + nb - 1) / nb;
+  c0 = b * per < C ? b * per : C;
+  c1 = c0 + per < C ? c0 + per : C;
+}
+
+__global__ __launch_bounds__(kRouteThreads) void kde_route_kernel(KdeArgs a) {
+  __shared__ uint32_t hist[kClasses];
+  __shared__ uint32_t th[64];
+  __shared__ uint32_t n_heavy, n_tier0, base_heavy, base_tier0;
+  const int tid = threadIdx.x;
+  if (tid < 64) th[tid] = a.theta[tid];
+  hist[tid] = hist[tid + kRouteThreads] = 0;
+  if (tid == 0) n_heavy = n_tier0 = 0;
+  __syncthreads();
+  const int64_t C = (int64_t)a.n_seg * a.K;
+  int64_t c0, c1;
+  cell_range(C, blockIdx.x, gridDim.x, c0, c1);
+  const int sh = 6 - a.sub_bits;
+  // 1. route codes; empty records; per-workgroup counts
+  for (int64_t cb = c0; cb < c1; cb += kRouteThreads) {
+    const int64_t c = cb + tid;
+    uint16_t code = kNoClass;
+    if (c < c1) {
+      const CellMeta m = load_meta(a, c);
+      code = route_code(m, th, sh);
+      if (code == kNoClass) {
+        if (m.n != 0) flag(a, ARGUS_DEV_KDE_SUMMARY);
+        const uint32_t z[kMaxC] = {0, 0, 0, 0};
+        const uint64_t zz[kMaxC] = {0, 0, 0, 0};
+        lane_write(a, c, 0, z, zz, zz, 0);
+      } else if (code < kClasses) {
+        atomicAdd(&hist[code], 1u);
+      }
+      a.lane_key[c] = code;
+    }
+    wave_append(&n_heavy, code == kHeavy);
+    wave_append(&n_tier0, code == kTier0);
+  }
+  __syncthreads();
+  // 2. list ranges of this workgroup
+  if (tid == 0) {
+    uint32_t nl = 0, nw = 0;
+    for (int k = 0; k < kLaneClasses; ++k) nl += hist[k];
+    for (int k = kLaneClasses; k < kClasses; ++k) nw += hist[k];
+    if (nl) atomicAdd(&a.counters[12], nl);
+    if (nw) atomicAdd(&a.counters[9], nw);
+    base_heavy = n_heavy ? atomicAdd(&a.counters[11], n_heavy) : 0u;
+    base_tier0 = n_tier0 ? atomicAdd(&a.counters[7], n_tier0) : 0u;
+    n_heavy = n_tier0 = 0;
+  }
+  for (int k = tid; k < kClasses; k += kRouteThreads)
+    if (hist[k]) atomicAdd(&a.lane_cls[k], hist[k]);
+  __syncthreads();
+  // 3. heavy and tier-0 entries (the lane lists are laid out by the next kernel)
+  for (int64_t cb = c0; cb < c1; cb += kRouteThreads) {
+    const int64_t c = cb + tid;
+    const uint16_t code = c < c1 ? a.lane_key[c] : kNoClass;
+    const uint32_t ih = wave_append(&n_heavy, code == kHeavy);
+    if (code == kHeavy) a.list2[C - 1 - (int64_t)(base_heavy + ih)] = (uint32_t)c;
+    const uint32_t i0 = wave_append(&n_tier0, code == kTier0);
+    if (code == kTier0) a.list2[base_tier0 + i0] = (uint32_t)c;
+  }
+}
+
+// Positions of the lane passes' cells: class offsets from an exclusive scan
+// of the class counts, a range per class and round claimed with one atomic,
+// ranks inside the round from LDS atomics. First-pass cells of position p
+// go to list1[C - 1 - p], wide cells to list1[p - (first-pass total)].
+__global__ __launch_bounds__(kRouteThreads) void kde_lane_order_kernel(KdeArgs a) {
+  __shared__ uint32_t off[kClasses], lcnt[kClasses], lbase[kClasses];
+  __shared__ uint32_t wsum[kRouteThreads / kWave];
+  const int tid = threadIdx.x, wv = tid / kWave;
+  {
+    const uint32_t v0 = a.lane_cls[2 * tid], v1 = a.lane_cls[2 * tid + 1];
+    const uint32_t incl = wave_incl_scan(v0 + v1);
+    if (lane_id() == kWave - 1) wsum[wv] = incl;
+    __syncthreads();
+    uint32_t base = incl - v0 - v1;
+    for (int w = 0; w < wv; ++w) base += wsum[w];
+    off[2 * tid] = base;
+    off[2 * tid + 1] = base + v0;
+  }
+  __syncthreads();
+  const uint32_t n_first = off[kLaneClasses];
+  const int64_t C = (int64_t)a.n_seg * a.K;
+  int64_t c0, c1;
+  cell_range(C, blockIdx.x, gridDim.x, c0, c1);
+  for (int64_t cb = c0; cb < c1; cb += (int64_t)kOrderPer * kRouteThreads) {
+    lcnt[tid] = lcnt[tid + kRouteThreads] = 0;
+    __syncthreads();
+    uint16_t key[kOrderPer];
+    uint32_t rank[kOrderPer];
+#pragma unroll
+    for (int u = 0; u < kOrderPer; ++u) {
+      const int64_t c = cb + (int64_t)u * kRouteThreads + tid;
+      key[u] = c < c1 ? a.lane_key[c] : kNoClass;
+      rank[u] = key[u] < kClasses ? atomicAdd(&lcnt[key[u]], 1u) : 0u;
+    }
+    __syncthreads();
+    for (int k = tid; k < kClasses; k += kRouteThreads)
+      if (lcnt[k]) lbase[k] = atomicAdd(&a.lane_cls[kClasses + k], lcnt[k]);
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kOrderPer; ++u) {
+      if (key[u] >= kClasses) continue;
+      const int64_t c = cb + (int64_t)u * kRouteThreads + tid;
+      const int64_t p = (int64_t)off[key[u]] + lbase[key[u]] + rank[u];
+      if (key[u] < kLaneClasses) a.list1[C - 1 - p] = (uint32_t)c;
+      else a.list1[p - n_first] = (uint32_t)c;
+    }
+    __syncthreads();
+  }
+}
+
+// Lane passes. GC = kLaneG: the routed cells in class order, 64 list
+// entries per claim; GC = kLaneGW: the wide list. A cell that does not fit
+// the lane limits goes to list 0 (tier 0).
 template <int GC>
 __global__ __launch_bounds__(kWave) void kde_lane_kernel(KdeArgs a) {
   constexpr bool kFirst = GC == kLaneG;
@@ -1752,9 +1925,9 @@ __global__ __launch_bounds__(kWave) void kde_lane_kernel(KdeArgs a) {
   const int l = lane_id();
   L.th[l] = a.theta[l];
   wave_sync();
-  const int64_t C = kFirst ? (int64_t)a.n_seg * a.K
-                           : (int64_t)__builtin_amdgcn_readfirstlane(
-                                 __hip_atomic_load(&a.counters[9], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+  const int64_t Ctot = (int64_t)a.n_seg * a.K;
+  const int64_t C = (int64_t)__builtin_amdgcn_readfirstlane(
+      __hip_atomic_load(&a.counters[kFirst ? 12 : 9], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
   const int sh = 6 - a.sub_bits;
   while (true) {
     uint32_t claim = 0;
@@ -1763,26 +1936,12 @@ __global__ __launch_bounds__(kWave) void kde_lane_kernel(KdeArgs a) {
     if ((int64_t)claim * kWave >= C) break;
     const int64_t i = (int64_t)claim * kWave + l;
     if (i < C) {
-      const int64_t c = kFirst ? i : (int64_t)a.list1[i];
+      const int64_t c = kFirst ? (int64_t)a.list1[Ctot - 1 - i] : (int64_t)a.list1[i];
       const CellMeta m = load_meta(a, c);
       bool done = false;
-      if (kFirst && (m.n == 0 || m.off < 0)) {
-        if (m.n != 0) flag(a, ARGUS_DEV_KDE_SUMMARY);
-        const uint32_t z[kMaxC] = {0, 0, 0, 0};
-        const uint64_t zz[kMaxC] = {0, 0, 0, 0};
-        lane_write(a, c, 0, z, zz, zz, 0);
-        done = true;
-      } else if (kFirst && m.n >= kBlockMin) {
-        a.list2[C - 1 - (int64_t)atomicAdd(&a.counters[11], 1u)] = (uint32_t)c;
-        done = true;
-      } else if (m.n <= (uint32_t)kLaneN) {
+      if (m.off >= 0 && m.n <= (uint32_t)kLaneN) {
         const int G = (grid64((uint64_t)m.mx, L.th) >> sh) - (grid64((uint64_t)m.mn, L.th) >> sh) + 1;
-        if (G <= GC) {
-          done = lane_cell<GC>(a, L, c, m);
-        } else if (kFirst && G <= kLaneGW) {
-          a.list1[atomicAdd(&a.counters[9], 1u)] = (uint32_t)c;
-          done = true;
-        }
+        if (G <= GC) done = lane_cell<GC>(a, L, c, m);
       }
       if (!done) a.list2[atomicAdd(&a.counters[7], 1u)] = (uint32_t)c;
     }
@@ -1857,8 +2016,9 @@ int resident(Kern kern, int threads) {
   return cus * (per_cu > 0 ? per_cu : 1);
 }
 
-__global__ void kde_clear_kernel(uint32_t* counters, int32_t* dev_status) {
+__global__ void kde_clear_kernel(uint32_t* counters, uint32_t* lane_cls, int32_t* dev_status) {
   if (threadIdx.x < 16) counters[threadIdx.x] = 0;
+  for (int i = threadIdx.x; i < 2 * kClasses; i += blockDim.x) lane_cls[i] = 0;
   if (threadIdx.x == 0 && dev_status) *dev_status = 0;
 }
 
@@ -1869,7 +2029,8 @@ size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 }  // namespace
 
 size_t kde_workspace_bytes(int64_t n_events, int64_t cells) {
-  return 256 + al256((size_t)n_events * 8) + 3 * al256((size_t)cells * 4);
+  return 256 + al256((size_t)n_events * 8) + 3 * al256((size_t)cells * 4) + al256((size_t)cells * 2) +
+         al256((size_t)2 * kClasses * 4);
 }
 
 hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
@@ -1910,10 +2071,14 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   a.list1 = reinterpret_cast<uint32_t*>(ws + off);
   off += al256((size_t)cells * 4);
   a.list2 = reinterpret_cast<uint32_t*>(ws + off);
+  off += al256((size_t)cells * 4);
+  a.lane_key = reinterpret_cast<uint16_t*>(ws + off);
+  off += al256((size_t)cells * 2);
+  a.lane_cls = reinterpret_cast<uint32_t*>(ws + off);
   const uint32_t* th = thresholds();
   for (int t = 0; t < 64; ++t) a.theta[t] = th[t];
 
-  hipLaunchKernelGGL(kde_clear_kernel, dim3(1), dim3(64), 0, st, a.counters, a.dev_status);
+  hipLaunchKernelGGL(kde_clear_kernel, dim3(1), dim3(256), 0, st, a.counters, a.lane_cls, a.dev_status);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (cells == 0) return hipSuccess;
 
@@ -1938,6 +2103,13 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
     hipLaunchKernelGGL(kde_scatter_staged_kernel, dim3(l.n_seg < g[7] ? l.n_seg : g[7]), dim3(kStageThreads), 0, st, a);
   else
     hipLaunchKernelGGL(kde_scatter_kernel, dim3(l.n_seg < g[0] ? l.n_seg : g[0]), dim3(kScatterThreads), 0, st, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // routing and the class order of the lane passes: contiguous ranges of
+  // at least 16,384 cells per workgroup, at most 512 workgroups
+  const int64_t route_wg = (cells + 16383) / 16384 < 512 ? (cells + 16383) / 16384 : 512;
+  hipLaunchKernelGGL(kde_route_kernel, dim3((unsigned)route_wg), dim3(kRouteThreads), 0, st, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(kde_lane_order_kernel, dim3((unsigned)route_wg), dim3(kRouteThreads), 0, st, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int64_t chunks = (cells + kWave - 1) / kWave;
   hipLaunchKernelGGL(kde_lane_kernel<kLaneG>, dim3(chunks < g[4] ? (int)chunks : g[4]), dim3(kWave), 0, st, a);
