@@ -3,13 +3,23 @@
 // Eq. 1; the step-by-step definition is in include/argus.h).
 //
 // Kernels, in launch order:
-//   kde_scatter_kernel   one 512-thread workgroup per segment (persistent
-//                        queue): the segment's valid durations are bucketed
-//                        by kernel id into the workspace, a counting sort
-//                        whose counts are argus_summarize's, so each cell's
-//                        durations become contiguous. 16-byte loads of four
-//                        events per thread, next group in flight. HBM bound:
+//   kde_scatter_staged_kernel / kde_scatter_kernel
+//                        one workgroup per segment (persistent queue): the
+//                        segment's valid durations are bucketed by kernel id
+//                        into the workspace, a counting sort whose counts are
+//                        argus_summarize's, so each cell's durations become
+//                        contiguous. The staged variant (id spaces of up to
+//                        2,048 ids) collects each id's positions in LDS and
+//                        writes them as aligned 64-byte groups. HBM bound:
 //                        24 B read and 8 B written per event.
+//   kde_route_kernel,    every cell routed once: empty cells written, heavy
+//   kde_lane_order_kernel cells to the workgroup tier, large or wide-grid
+//                        cells to tier 0, the rest to the lane passes in
+//                        cost-class order (grid size x duration count).
+//   kde_lane_kernel<64>, one cell per lane, 64 cells per wavefront (grids of
+//   kde_lane_kernel<256> up to 64 / 65-256 points, up to 255 durations).
+//   kde_block_kernel     one 512-thread workgroup per cell of 2,048 or more
+//                        durations.
 //   kde_cell_kernel<0>   one wavefront per cell, cells claimed 64 at a time
 //                        with their summaries, n^-0.2 and (for cells of up to
 //                        256 durations) the next cell's durations prefetched
@@ -17,10 +27,10 @@
 //                        in LDS, exact bandwidth, integer-weight density
 //                        (sparse over occupied grid points when that is
 //                        cheaper), valleys, filters, and p50 / p99 by exact
-//                        radix selection inside the target grid bin. 6 KB of
+//                        radix selection inside the target grid bin. 7.5 KB of
 //                        LDS per wavefront; cells that need more go to a list.
-//   kde_cell_kernel<1>   the listed cells with 22 KB per wavefront;
-//   kde_cell_kernel<2>   what still does not fit, 56 KB per wavefront (any
+//   kde_cell_kernel<1>   the listed cells with 20 KB per wavefront;
+//   kde_cell_kernel<2>   what still does not fit, 105 KB per wavefront (any
 //                        grid of the 64-bit duration range fits).
 #include <atomic>
 #include <cmath>
