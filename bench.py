@@ -103,6 +103,29 @@ def cpu_baseline(trace, sample_ranks: int, gpu_sum: dict) -> dict:
             "seconds": round(t_oracle, 3), "_mismatches": mismatches}
 
 
+def cpu_baseline_sharded(trace, n_workers: int, seg_per_shard: int = 64) -> dict:
+    """The same single-threaded oracle summarize, unmodified, run on disjoint
+    segment shards in n_workers threads at once (ctypes releases the GIL
+    during each call); shards are generated beforehand, outside the timing."""
+    import oracle
+    from concurrent.futures import ThreadPoolExecutor
+    cfg = trace.cfg
+    G = cfg.n_ranks * cfg.n_steps
+    n = max(1, min(n_workers, G // seg_per_shard))
+    shards = [trace.fill_host(i * seg_per_shard, (i + 1) * seg_per_shard, n_threads=os.cpu_count() or 1)
+              for i in range(n)]
+    n_ev = sum(len(e["kernel_id"]) for e in shards)
+    with ThreadPoolExecutor(max_workers=n) as ex:
+        list(ex.map(lambda e: oracle.summarize(e, cfg.n_kernels, cfg.n_streams), shards[:1]))  # warm-up
+        t0 = time.perf_counter()
+        list(ex.map(lambda e: oracle.summarize(e, cfg.n_kernels, cfg.n_streams), shards))
+        dt = time.perf_counter() - t0
+    return {"value": n_ev / dt, "unit": "events/s", "cores": n, "kind": "oracle",
+            "sample": f"{n} disjoint shards of {seg_per_shard} rank-steps ({n_ev} events) of the same workload, "
+                      f"oracle summarize on each shard in its own thread at once, generation excluded",
+            "seconds": round(dt, 3)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -371,6 +394,9 @@ def main():
         mism = cb.pop("_mismatches")
         result["cpu_baseline"] = cb
         result["parity_sample"] = {"segments": sample * S, "mismatches": mism}
+        workers = min(16, os.cpu_count() or 1)
+        print(f"[bench] sharded cpu baseline: {workers} threads", file=sys.stderr, flush=True)
+        result["cpu_baseline_sharded"] = cpu_baseline_sharded(trace, workers)
         if mism:
             print(json.dumps(result))
             raise SystemExit(f"parity failure on the sampled segments: {mism} mismatching elements")
