@@ -9,16 +9,15 @@
 
 namespace argus {
 
-constexpr int kSelBins = 256;  // 8-bit digits: the first 256 threads own one bin each
-
-// hist[bin] += 1 for every active lane. Two rounds count all active lanes
-// sharing the first remaining lane's bin with one atomic (the bin is read
-// with readlane, no LDS round trip); the rest add individually. Must be
-// reached by every lane of the wavefront.
+// hist[bin] += 1 for every active lane. Each of ROUNDS rounds counts all
+// active lanes sharing the first remaining lane's bin with one atomic (the
+// bin is read with readlane, no LDS round trip); the rest add individually.
+// Must be reached by every lane of the wavefront.
+template <int ROUNDS = 2>
 __device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool active) {
   const int lane = threadIdx.x & 63;
 #pragma unroll
-  for (int it = 0; it < 2; ++it) {
+  for (int it = 0; it < ROUNDS; ++it) {
     const unsigned long long act = __ballot(active);
     if (act == 0) return;
     const int leader = __ffsll((long long)act) - 1;
@@ -31,19 +30,27 @@ __device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool acti
   if (active) atomicAdd(&hist[bin], 1u);
 }
 
-template <int T>
+// Shared state of a selection of T ranks with DB-bit digits (2^DB bins per
+// target); at most 16 wavefronts per block.
+template <int T, int DB = 8>
 struct SelShared {
-  uint32_t hist[T][256];
-  uint32_t wave_tot[T * 4];
+  uint32_t hist[T][1 << DB];
+  uint32_t wave_tot[T * 16];
   uint32_t digit[T], before[T];
 };
 
 // MSD radix select of the ranks k[0..T) among the valid register keys of
 // the whole block of NT >= 256 threads (bit j of vm: key[j] valid), all keys
-// <= range. Every thread of the block must call it.
-template <int NT, int V, int T, typename KeyT>
+// <= range, DB bits per pass (wider digits: fewer passes over the keys, each
+// with a larger histogram to clear and scan), HR aggregation rounds per
+// histogram add. Every thread of the block must call it.
+template <int NT, int V, int T, int DB = 8, int HR = 2, typename KeyT>
 __device__ void select_ranks(const KeyT (&key)[V], uint64_t vm, uint64_t range, const uint32_t (&k)[T],
-                             uint64_t (&out)[T], SelShared<T>& sh) {
+                             uint64_t (&out)[T], SelShared<T, DB>& sh) {
+  constexpr int NB = 1 << DB;
+  constexpr int BPT = NB > NT ? NB / NT : 1;  // bins per scanning thread
+  constexpr int NSCAN = NB / BPT;             // scanning threads
+  static_assert(NT >= 256 && NT <= 1024 && NB % NSCAN == 0, "block size and digit width");
   uint64_t prefix[T];
   uint32_t kk[T];
 #pragma unroll
@@ -53,14 +60,12 @@ __device__ void select_ranks(const KeyT (&key)[V], uint64_t vm, uint64_t range, 
   }
   if (range != 0) {
     const int nbits = 64 - __builtin_clzll(range);
-    const int passes = (nbits + 7) >> 3;
+    const int passes = (nbits + DB - 1) / DB;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     for (int p = passes - 1; p >= 0; --p) {
-      const int shift = p * 8;
+      const int shift = p * DB;
       const bool top = p == passes - 1;
-      if (tid < kSelBins)
-#pragma unroll
-        for (int t = 0; t < T; ++t) sh.hist[t][tid] = 0;
+      for (int i = tid; i < T * NB; i += NT) (&sh.hist[0][0])[i] = 0;
       __syncthreads();
       // targets with equal prefixes share one histogram: rep[t] is the first
       int rep[T];
@@ -75,43 +80,56 @@ __device__ void select_ranks(const KeyT (&key)[V], uint64_t vm, uint64_t range, 
       for (int j = 0; j < V; ++j) {
         const uint64_t kj = (uint64_t)key[j];
         const bool ok = (vm >> j) & 1u;
-        const uint32_t digit = (uint32_t)(kj >> shift) & 255u;
-        const uint64_t hi = top ? 0 : kj >> (shift + 8);
+        const uint32_t digit = (uint32_t)(kj >> shift) & (uint32_t)(NB - 1);
+        const uint64_t hi = top || shift + DB >= 64 ? 0 : kj >> (shift + DB);
 #pragma unroll
         for (int t = 0; t < T; ++t)
-          if (rep[t] == t) hist_add(sh.hist[t], digit, ok && (top || hi == prefix[t]));
+          if (rep[t] == t) hist_add<HR>(sh.hist[t], digit, ok && (top || hi == prefix[t]));
       }
       __syncthreads();
-      // per-target inclusive scan over 256 bins, one bin per thread
-      uint32_t h[T], v[T];
-      if (tid < kSelBins) {
+      // per-target inclusive scan over the bins, BPT consecutive bins per
+      // scanning thread
+      uint32_t h[T][BPT], v[T];
+      if (tid < NSCAN) {
 #pragma unroll
         for (int t = 0; t < T; ++t) {
-          h[t] = sh.hist[rep[t]][tid];
-          v[t] = h[t];
+          uint32_t sum = 0;
+#pragma unroll
+          for (int b = 0; b < BPT; ++b) {
+            h[t][b] = sh.hist[rep[t]][tid * BPT + b];
+            sum += h[t][b];
+          }
+          v[t] = sum;
           for (int o = 1; o < 64; o <<= 1) {
             const uint32_t n = __shfl_up(v[t], o, 64);
             if (lane >= o) v[t] += n;
           }
-          if (lane == 63) sh.wave_tot[t * 4 + w] = v[t];
+          if (lane == 63) sh.wave_tot[t * 16 + w] = v[t];
         }
       }
       __syncthreads();
-      if (tid < kSelBins) {
+      if (tid < NSCAN) {
 #pragma unroll
         for (int t = 0; t < T; ++t) {
-          for (int ww = 0; ww < w; ++ww) v[t] += sh.wave_tot[t * 4 + ww];
-          const uint32_t excl = v[t] - h[t];
-          if (excl <= kk[t] && kk[t] < v[t]) {
-            sh.digit[t] = (uint32_t)tid;
-            sh.before[t] = excl;
+          uint32_t run = v[t];
+          for (int ww = 0; ww < w; ++ww) run += sh.wave_tot[t * 16 + ww];
+#pragma unroll
+          for (int b = BPT - 1; b >= 0; --b) run -= h[t][b];
+          // run: bins before this thread's first bin
+#pragma unroll
+          for (int b = 0; b < BPT; ++b) {
+            if (run <= kk[t] && kk[t] < run + h[t][b]) {
+              sh.digit[t] = (uint32_t)(tid * BPT + b);
+              sh.before[t] = run;
+            }
+            run += h[t][b];
           }
         }
       }
       __syncthreads();
 #pragma unroll
       for (int q = 0; q < T; ++q) {
-        prefix[q] = (prefix[q] << 8) | sh.digit[q];
+        prefix[q] = DB >= 64 ? sh.digit[q] : (prefix[q] << DB) | sh.digit[q];
         kk[q] -= sh.before[q];
       }
       __syncthreads();

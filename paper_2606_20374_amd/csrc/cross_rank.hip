@@ -33,8 +33,30 @@ namespace {
 typedef unsigned __int128 u128;
 typedef __int128 i128;
 
+// Radix-select digit widths: a kernel's means span about 2^22 ns, which 11-bit
+// digits resolve in two passes (8-bit digits: three); a rank's permille
+// ratios span a few thousand (two 8-bit passes; a 4,096-bin single pass
+// costs more to clear and scan than it saves).
+constexpr int kStatsDigit = 11;
+constexpr int kRankDigit = 8;
+// One aggregation round per histogram add: it takes the dominant bin of the
+// leading digit; a second round costs more than the conflicts it saves.
+constexpr int kAggRounds = 1;
+
+// floor(sum / count) with sum read as uint64, saturated at INT64_MAX. Below
+// 2^53 both operands are exact doubles and the correctly rounded quotient
+// truncates to the exact floor or one above it (never below: the floor is
+// representable), which one exact product detects; larger sums take the
+// integer division.
 __device__ __forceinline__ int64_t cell_x(uint32_t count, int64_t sum) {
-  const uint64_t x = (uint64_t)sum / count;
+  const uint64_t s = (uint64_t)sum;
+  uint64_t x;
+  if (s < (1ull << 53)) {
+    x = (uint64_t)((double)s / (double)count);
+    if (x * count > s) --x;
+  } else {
+    x = s / count;
+  }
   return x > (uint64_t)INT64_MAX ? INT64_MAX : (int64_t)x;
 }
 
@@ -74,8 +96,8 @@ struct StatsArgs {
 
 template <int NT, int V>
 __global__ __launch_bounds__(NT) void xr_kernel_stats(StatsArgs a) {
-  __shared__ SelShared<3> sh3;
-  __shared__ SelShared<1> sh1;
+  __shared__ SelShared<3, kStatsDigit> sh3;
+  __shared__ SelShared<1, kStatsDigit> sh1;
   __shared__ uint32_t n_sh;
   __shared__ unsigned long long red_min, red_max, red_lo, red_hi;
   const int tid = threadIdx.x;
@@ -144,14 +166,14 @@ __global__ __launch_bounds__(NT) void xr_kernel_stats(StatsArgs a) {
   const uint32_t nm1 = (uint32_t)(n - 1);
   const uint32_t ranks[3] = {nm1 / 4, nm1 / 2, (uint32_t)((3ull * nm1) / 4)};
   uint64_t qs[3];
-  select_ranks<NT, V, 3>(key, vm, vmax - vmin, ranks, qs, sh3);
+  select_ranks<NT, V, 3, kStatsDigit, kAggRounds>(key, vm, vmax - vmin, ranks, qs, sh3);
   const uint64_t dmed = qs[1];  // median - vmin
 #pragma unroll
   for (int j = 0; j < V; ++j) key[j] = key[j] >= dmed ? key[j] - dmed : dmed - key[j];
   const uint64_t top = vmax - vmin - dmed;
   const uint32_t r1[1] = {nm1 / 2};
   uint64_t md[1];
-  select_ranks<NT, V, 1>(key, vm, top > dmed ? top : dmed, r1, md, sh1);
+  select_ranks<NT, V, 1, kStatsDigit, kAggRounds>(key, vm, top > dmed ? top : dmed, r1, md, sh1);
   if (tid == 0) {
     a.q1[sk] = (int64_t)(vmin + qs[0]);
     a.med[sk] = (int64_t)(vmin + qs[1]);
@@ -185,7 +207,7 @@ __device__ __forceinline__ uint32_t ratio_pm(int64_t x, int64_t med) {
 
 template <int NT, int V>
 __global__ __launch_bounds__(NT) void xr_rank(RankArgs a) {
-  __shared__ SelShared<1> sh;
+  __shared__ SelShared<1, kRankDigit> sh;
   __shared__ uint32_t ne_sh, nf_sh, rmin_sh, rmax_sh;
   const int tid = threadIdx.x;
   const int32_t K = a.K;
@@ -267,7 +289,7 @@ __global__ __launch_bounds__(NT) void xr_rank(RankArgs a) {
     for (int j = 0; j < V; ++j) rat[j] -= (em >> j) & 1u ? lo : 0u;
     const uint32_t rk[1] = {(uint32_t)(n_eval - 1) / 2};
     uint64_t sel[1];
-    select_ranks<NT, V, 1>(rat, em, rmax_sh - lo, rk, sel, sh);
+    select_ranks<NT, V, 1, kRankDigit, kAggRounds>(rat, em, rmax_sh - lo, rk, sel, sh);
     score = (int32_t)(lo + (uint32_t)sel[0]);
   }
   const bool strag = n_eval >= a.p.min_kernels && (int64_t)score >= 1000 + (int64_t)a.p.tau_rank_pm;
