@@ -67,16 +67,23 @@ __global__ __launch_bounds__(256) void xr_transpose(const uint32_t* __restrict__
   __shared__ int64_t tile[64][65];
   const int k0 = blockIdx.x * 64, r0 = blockIdx.y * 64, s = blockIdx.z;
   const int t = threadIdx.x, c64 = t & 63;
-  for (int rr = t >> 6; rr < 64; rr += 4) {
-    const int r = r0 + rr, k = k0 + c64;
-    int64_t x = -1;
+  // all 32 loads of a thread are issued before the first is used (the sum
+  // is read whether or not the count is zero)
+  uint32_t n[16];
+  int64_t sm[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int r = r0 + (t >> 6) + 4 * i, k = k0 + c64;
+    n[i] = 0;
+    sm[i] = 0;
     if (r < R && k < K) {
       const int64_t c = ((int64_t)r * S + s) * K + k;
-      const uint32_t n = count[c];
-      if (n) x = cell_x(n, sum[c]);
+      n[i] = count[c];
+      sm[i] = sum[c];
     }
-    tile[rr][c64] = x;
   }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) tile[(t >> 6) + 4 * i][c64] = n[i] ? cell_x(n[i], sm[i]) : -1;
   __syncthreads();
   for (int kk = t >> 6; kk < 64; kk += 4) {
     const int k = k0 + kk, r = r0 + c64;
@@ -193,10 +200,16 @@ struct RankArgs {
   argus_xr_out_t o;
 };
 
-// floor(1000 x / med), saturated at INT32_MAX (x >= 0, med >= 1)
+// floor(1000 x / med), saturated at INT32_MAX (x >= 0, med >= 1). Below
+// 2^53 the quotient comes from a correctly rounded double division and one
+// product check, as in cell_x.
 __device__ __forceinline__ uint32_t ratio_pm(int64_t x, int64_t med) {
   uint64_t q;
-  if ((uint64_t)x <= ~0ull / 1000u) {
+  if ((uint64_t)x < (1ull << 53) / 1000u && (uint64_t)med < (1ull << 53)) {
+    const uint64_t num = (uint64_t)x * 1000u;
+    q = (uint64_t)((double)num / (double)med);
+    if (q * (uint64_t)med > num) --q;
+  } else if ((uint64_t)x <= ~0ull / 1000u) {
     q = ((uint64_t)x * 1000u) / (uint64_t)med;
   } else {
     const u128 w = ((u128)(uint64_t)x * 1000u) / (u128)(uint64_t)med;
