@@ -238,46 +238,69 @@ __global__ __launch_bounds__(NT) void xr_rank(RankArgs a) {
   for (int j = 0; j < (V + 3) / 4; ++j) fl[j] = 0;
   uint64_t em = 0;
   uint32_t ne = 0, nf = 0, rmin = 0xFFFFFFFFu, rmax = 0;
+  // cells in groups of four: every load of a group (the cells and their
+  // kernels' statistics) is issued before the first is used
+  constexpr int VB = V < 4 ? V : 4;
+  static_assert(V % VB == 0, "cell groups");
 #pragma unroll
-  for (int j = 0; j < V; ++j) {
-    const int k = tid + j * NT;
-    rat[j] = 0;
-    if (k >= K) continue;
-    const int64_t c = rs * K + k;
-    const int64_t sk = (int64_t)s * K + k;
-    const uint32_t cnt = a.count[c];
-    float z = 0.0f, mean = 0.0f;
-    uint32_t f = 0;
-    if (cnt) {
-      const int64_t sm = a.sum[c];
-      mean = (float)((double)sm / (double)cnt);
-      const uint32_t n = a.o.n_present[sk];
-      if (n >= (uint32_t)a.p.min_ranks && n) {
-        const int64_t x = cell_x(cnt, sm);
-        const int64_t med = a.o.med_ns[sk], mad = a.o.mad_ns[sk];
-        const int64_t q1 = a.o.q1_ns[sk], q3 = a.o.q3_ns[sk];
-        const int64_t madf = mad > 1 ? mad : 1;
-        const int64_t iqr = q3 - q1 > 1 ? q3 - q1 : 1;
-        z = (float)((double)(x - med) / (1.4826 * (double)madf));
-        f = 4;
-        if (cnt >= (uint32_t)a.p.c_min_pair && (i128)1000 * ((i128)x - med) > (i128)a.p.k_mad_pm * madf &&
-            (i128)1000 * x >= (i128)a.p.ratio_pm * med)
-          f |= 1;
-        if ((i128)1000 * ((i128)x - q3) > (i128)a.p.alpha_pm * iqr) f |= 2;
-        if (med >= 1) {
-          const uint32_t r = ratio_pm(x, med);
-          rat[j] = r;
-          em |= 1ull << j;
-          ++ne;
-          rmin = r < rmin ? r : rmin;
-          rmax = r > rmax ? r : rmax;
-          if (f & 1) ++nf;
+  for (int jb = 0; jb < V; jb += VB) {
+    uint32_t cnt_[VB], np_[VB];
+    int64_t sm_[VB], med_[VB], mad_[VB], q1_[VB], q3_[VB];
+#pragma unroll
+    for (int u = 0; u < VB; ++u) {
+      const int j = jb + u;
+      const int k = tid + j * NT < K ? tid + j * NT : K - 1;
+      const int64_t c = rs * K + k;
+      const int64_t sk = (int64_t)s * K + k;
+      cnt_[u] = a.count[c];
+      sm_[u] = a.sum[c];
+      np_[u] = a.o.n_present[sk];
+      med_[u] = a.o.med_ns[sk];
+      mad_[u] = a.o.mad_ns[sk];
+      q1_[u] = a.o.q1_ns[sk];
+      q3_[u] = a.o.q3_ns[sk];
+    }
+#pragma unroll
+    for (int u = 0; u < VB; ++u) {
+      const int j = jb + u;
+      const int k = tid + j * NT;
+      rat[j] = 0;
+      if (k >= K) continue;
+      const int64_t c = rs * K + k;
+      const uint32_t cnt = cnt_[u];
+      float z = 0.0f, mean = 0.0f;
+      uint32_t f = 0;
+      if (cnt) {
+        const int64_t sm = sm_[u];
+        mean = (float)((double)sm / (double)cnt);
+        const uint32_t n = np_[u];
+        if (n >= (uint32_t)a.p.min_ranks && n) {
+          const int64_t x = cell_x(cnt, sm);
+          const int64_t med = med_[u], mad = mad_[u];
+          const int64_t q1 = q1_[u], q3 = q3_[u];
+          const int64_t madf = mad > 1 ? mad : 1;
+          const int64_t iqr = q3 - q1 > 1 ? q3 - q1 : 1;
+          z = (float)((double)(x - med) / (1.4826 * (double)madf));
+          f = 4;
+          if (cnt >= (uint32_t)a.p.c_min_pair && (i128)1000 * ((i128)x - med) > (i128)a.p.k_mad_pm * madf &&
+              (i128)1000 * x >= (i128)a.p.ratio_pm * med)
+            f |= 1;
+          if ((i128)1000 * ((i128)x - q3) > (i128)a.p.alpha_pm * iqr) f |= 2;
+          if (med >= 1) {
+            const uint32_t r = ratio_pm(x, med);
+            rat[j] = r;
+            em |= 1ull << j;
+            ++ne;
+            rmin = r < rmin ? r : rmin;
+            rmax = r > rmax ? r : rmax;
+            if (f & 1) ++nf;
+          }
         }
       }
+      a.o.z[c] = z;
+      if (a.o.mean_ns) a.o.mean_ns[c] = mean;
+      fl[j >> 2] |= f << (8 * (j & 3));
     }
-    a.o.z[c] = z;
-    if (a.o.mean_ns) a.o.mean_ns[c] = mean;
-    fl[j >> 2] |= f << (8 * (j & 3));
   }
   for (int o = 32; o > 0; o >>= 1) {
     ne += __shfl_xor(ne, o, 64);
