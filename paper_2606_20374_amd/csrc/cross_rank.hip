@@ -12,11 +12,11 @@
 // Three launches per call:
 //   1. transpose: [R][S][K] (count, sum) -> x in a [S][K][R] workspace,
 //      64x64 tiles through LDS so both the read and the write are coalesced;
-//   2. per (step, kernel): one 1024-thread workgroup holds the kernel's x of
-//      every rank in registers (up to 16 per thread) and runs an MSD radix
-//      select over x - min, 8-bit digits, for q1, median and q3 together,
-//      then once more on |x - median| for the MAD; exact 128-bit sum for the
-//      mean;
+//   2. per (step, kernel): one workgroup of 256-1024 threads holds the
+//      kernel's x of every rank in registers (up to 24 per thread) and runs
+//      an MSD radix select over x - min, 11-bit digits, for q1, median and
+//      q3 together, then once more on |x - median| for the MAD; exact
+//      128-bit sum for the mean;
 //   3. per (rank, step): per-cell z, mean and flags, a radix select of the
 //      rank's typical per-kernel ratio to the median, the straggler decision
 //      and the degraded-pair bit.

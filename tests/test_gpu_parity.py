@@ -283,6 +283,25 @@ def test_cross_rank_identical_and_huge_values():
     _xr_both(cnt, sm, R, 1, 2)
 
 
+def test_cross_rank_quotient_paths():
+    # the exact mean floor(sum / count) takes a double quotient below 2^53 and
+    # the integer division above; permille ratios likewise below 2^53 / 1000
+    _announce("cross-rank quotient paths")
+    rng = np.random.default_rng(5)
+    R, K = 48, 6
+    cnt = rng.integers(1, 2**32, size=(R, K), dtype=np.uint64)
+    cnt[:, 0] = 1 << 20
+    cnt[:, 1] = 3
+    q = (np.uint64(2**53) - np.uint64(1)) // cnt  # largest quotient with sum < 2^53
+    sm = q * cnt + (cnt - np.uint64(1)) * (rng.random((R, K)) < 0.5)
+    sm[::4, 2] = np.uint64(2**53)  # exactly 2^53: the integer path
+    sm[1::4, 3] = np.uint64(2**53) - np.uint64(1)
+    # means around 9e12: 1000 x on both sides of 2^53 (about 9.007e15)
+    cnt[:, 4] = rng.integers(1, 1000, R).astype(np.uint64)
+    sm[:, 4] = rng.integers(8 * 10**12, 10**13, R).astype(np.uint64) * cnt[:, 4]
+    _xr_both(cnt.reshape(-1).astype(np.uint32), sm.reshape(-1).astype(np.int64), R, 1, K)
+
+
 # ------------------------------------------------------------------- L1
 def test_l1_golden_and_random():
     _announce("L1 golden + random")
