@@ -292,35 +292,26 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
 // Adds one to the 16-bit counter of bin v (two counters per word) for every
 // active lane and returns the counter's value before the lane's own claim,
 // so lanes with equal v get distinct consecutive values. Lanes sharing the
-// first remaining lane's value are served by one atomic (two rounds: at the
-// ends of the grid most ranks share the value 0 or 65535); the rest claim
-// one by one. Must be reached by every lane of the wavefront.
+// first active lane's value are served by one atomic (at the ends of the
+// grid most ranks share the value 0 or 65535); the rest claim one by one
+// (a second shared round cost more than it saved). Must be reached by every
+// lane of the wavefront.
 __device__ __forceinline__ uint32_t claim_bin(uint32_t* fine, uint32_t v, bool active) {
   const int lane = threadIdx.x & 63;
-  const unsigned long long below = (1ull << lane) - 1ull;
-  uint32_t res = 0;
-#pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    const unsigned long long act = __ballot(active);
-    if (act == 0) return res;
-    const int leader = __ffsll((long long)act) - 1;
-    const uint32_t lv = __builtin_amdgcn_readlane(v, leader);
-    const bool mine = active && v == lv;
-    const unsigned long long same = __ballot(mine);
-    const uint32_t sh = (lv & 1u) * 16u;
-    uint32_t old = 0;
-    if (lane == leader) old = atomicAdd(&fine[lv >> 1], (uint32_t)__popcll(same) << sh);
-    old = __builtin_amdgcn_readlane(old, leader);
-    if (mine) {
-      res = ((old >> sh) & 0xFFFFu) + (uint32_t)__popcll(same & below);
-      active = false;
-    }
-  }
-  if (active) {
-    const uint32_t sh = (v & 1u) * 16u;
-    res = (atomicAdd(&fine[v >> 1], 1u << sh) >> sh) & 0xFFFFu;
-  }
-  return res;
+  const unsigned long long act = __ballot(active);
+  if (act == 0) return 0;
+  const int leader = __ffsll((long long)act) - 1;
+  const uint32_t lv = __builtin_amdgcn_readlane(v, leader);
+  const bool mine = active && v == lv;
+  const unsigned long long same = __ballot(mine);
+  const uint32_t sh = (lv & 1u) * 16u;
+  uint32_t old = 0;
+  if (lane == leader) old = atomicAdd(&fine[lv >> 1], (uint32_t)__popcll(same) << sh);
+  old = __builtin_amdgcn_readlane(old, leader);
+  if (mine) return ((old >> sh) & 0xFFFFu) + (uint32_t)__popcll(same & ((1ull << lane) - 1ull));
+  if (!active) return 0;
+  const uint32_t shv = (v & 1u) * 16u;
+  return (atomicAdd(&fine[v >> 1], 1u << shv) >> shv) & 0xFFFFu;
 }
 
 template <int NT, int V>
@@ -409,7 +400,7 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
     }
     // 1. bucket (high byte) counts
 #pragma unroll
-    for (int j = 0; j < V; ++j) hist_add(bcnt, (qt[j] & 0xFFFFu) >> 8, present(j));
+    for (int j = 0; j < V; ++j) hist_add<1>(bcnt, (qt[j] & 0xFFFFu) >> 8, present(j));
     __syncthreads();
     // 2. bucket scan, first half; clear the bins of the occupied buckets
     uint32_t bc = 0, binc = 0;
