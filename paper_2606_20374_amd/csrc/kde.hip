@@ -1285,22 +1285,28 @@ __global__ __launch_bounds__(kWave, TIER == 0 ? 4 : 1) void kde_cell_kernel(KdeA
 }
 
 // --------------------------------------------------------- workgroup tier
-// Cells of at least kBlockMin durations, one 512-thread workgroup per cell:
-// every wavefront streams a share of the durations (four loads in flight per
-// lane) into the LDS grid histogram, wavefront 0 runs the analysis, and the
-// p50 / p99 targets are then resolved by selection passes in which all
-// threads stream the durations once more. Each target owns a region of
-// kSelRegion LDS words per pass: a histogram of the next kSelDigit bits of
-// its candidate range while more than kSelCap durations remain in it, else
-// the list of those durations, whose element of the wanted rank is found by
-// counting. Wavefront w resolves target w after each pass. Cells whose grid
-// or valleys do not fit go to tier 1 unchanged.
-constexpr int kBlockThreads = 512;
+// Cells of at least kBlockMin durations, one two-wavefront workgroup per
+// cell: both wavefronts stream the durations (kBlockDepth loads in flight
+// per lane) into the LDS grid histogram, wavefront 0 runs the analysis, and
+// the p50 / p99 targets are then resolved by selection passes in which both
+// stream the durations once more. Each target owns a region of kSelRegion
+// LDS words per pass: a histogram of the next kSelDigit bits of its
+// candidate range while more than kSelCap durations remain in it, else the
+// list of those durations, whose element of the wanted rank is found by
+// counting. Wavefront w resolves targets w, w + 2, ... after each pass.
+// Cells whose grid or valleys do not fit go to tier 1 unchanged. While
+// wavefront 0 analyses a cell its partner waits, so the workgroup is kept
+// small: eight workgroups share a CU (LDS bound), and their streaming passes
+// fill the time (workgroups of 512 / 256 threads: 20.6 / 15.6 ms on the
+// cluster step, 128: 13.6 ms).
+constexpr int kBlockThreads = 128;
+constexpr int kBlockWaves = kBlockThreads / kWave;
+constexpr int kBlockDepth = 8;  // duration loads in flight per thread in the streaming passes
 constexpr uint32_t kBlockMin = 2048;
 constexpr int kSelRegion = Tier<1>::kWords / kMaxT;  // 512 words per target
 constexpr int kSelDigit = 9;                         // log2(kSelRegion)
 constexpr int kSelCap = 64;
-static_assert(kBlockThreads / kWave == kMaxT, "one wavefront per selection target");
+static_assert(kMaxT % kBlockWaves == 0, "selection targets shared out over the wavefronts");
 static_assert((1 << kSelDigit) == kSelRegion && 2 * kSelCap <= kSelRegion, "selection regions");
 
 __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) {
@@ -1336,12 +1342,12 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
     for (int j = tid; j < G; j += kBlockThreads) cgrid[j] = 0;
     __syncthreads();
     bool out_of_range = false;
-    for (uint64_t i0 = tid; i0 < n; i0 += 4 * kBlockThreads) {
-      uint64_t v[4];
+    for (uint64_t i0 = tid; i0 < n; i0 += kBlockDepth * kBlockThreads) {
+      uint64_t v[kBlockDepth];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = i0 + u * kBlockThreads < n ? vals[i0 + u * kBlockThreads] : 0ull;
+      for (int u = 0; u < kBlockDepth; ++u) v[u] = i0 + u * kBlockThreads < n ? vals[i0 + u * kBlockThreads] : 0ull;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < kBlockDepth; ++u) {
         if (i0 + u * kBlockThreads >= n) break;
         const int x = (grid64(v[u], L.th) >> sh) - lo;
         if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
@@ -1419,18 +1425,18 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
           }
         }
       };
-      for (uint64_t i0 = tid; i0 < n; i0 += 4 * kBlockThreads) {
-        uint64_t v[4];
+      for (uint64_t i0 = tid; i0 < n; i0 += kBlockDepth * kBlockThreads) {
+        uint64_t v[kBlockDepth];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = i0 + u * kBlockThreads < n ? vals[i0 + u * kBlockThreads] : 0ull;
+        for (int u = 0; u < kBlockDepth; ++u) v[u] = i0 + u * kBlockThreads < n ? vals[i0 + u * kBlockThreads] : 0ull;
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < kBlockDepth; ++u)
           if (i0 + u * kBlockThreads < n) consider(v[u]);
       }
       __syncthreads();
-      // wavefront wv resolves target wv
-      if ((live >> wv) & 1u) {
-        const int t = wv;
+      // wavefront wv resolves targets wv, wv + kBlockWaves, ...
+      for (int t = wv; t < kMaxT; t += kBlockWaves) {
+        if (!((live >> t) & 1u)) continue;
         const uint64_t r = readlane64(L.trank[t], 0);
         const uint64_t base = readlane64(L.tlb[t], 0);
         if (tsh[t] < 0) {
