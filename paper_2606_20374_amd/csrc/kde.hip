@@ -18,7 +18,7 @@
 //                        cost-class order (grid size x duration count).
 //   kde_lane_kernel<64>, one cell per lane, 64 cells per wavefront (grids of
 //   kde_lane_kernel<256> up to 64 / 65-256 points, up to 255 durations).
-//   kde_block_kernel     one 512-thread workgroup per cell of 2,048 or more
+//   kde_block_kernel     one 128-thread workgroup per cell of 2,048 or more
 //                        durations.
 //   kde_cell_kernel<0>   one wavefront per cell, cells claimed 64 at a time
 //                        with their summaries, n^-0.2 and (for cells of up to
