@@ -366,16 +366,35 @@ __device__ __forceinline__ void buf_store_u64(__amdgpu_buffer_rsrc_t r, uint32_t
   __builtin_amdgcn_raw_buffer_store_b64(v2u{(uint32_t)v, (uint32_t)(v >> 32)}, r, (int)off, 0, 0);
 }
 
-__device__ __forceinline__ void stage_one_buf(const StageCtx& s, __amdgpu_buffer_rsrc_t ro, bool ok, int32_t kid,
-                                              int32_t st, int64_t t0, int64_t t1) {
-  const uint64_t d = (uint64_t)t1 - (uint64_t)t0;
-  uint32_t off = kOob;
-  if (ok && kid >= 0 && kid < s.K && st >= 0 && st < s.NS && t0 >= 0 && t1 >= t0) {
-    const uint32_t p = atomicAdd(&s.cur[kid], 1u);
-    if (p - s.done[kid] < (uint32_t)kStageW) s.stage[kid][(p + s.lo7) & (kStageW - 1)] = d;
-    else if (p < s.len) off = p * 8u;
+// Four events at once. Every lane takes a cursor for all four before any
+// result is used, so the four LDS round trips overlap: an event that is not
+// valid (or past the end) counts on the spare slot kStageK, which no flush
+// reads, and stores nothing.
+__device__ __forceinline__ void stage_four_buf(const StageCtx& s, __amdgpu_buffer_rsrc_t ro, bool ok, v4i k4, v4i s4,
+                                               v2l x0, v2l x1, v2l y0, v2l y1) {
+  const int32_t kid[4] = {k4.x, k4.y, k4.z, k4.w}, st[4] = {s4.x, s4.y, s4.z, s4.w};
+  const int64_t t0[4] = {x0.x, x0.y, x1.x, x1.y}, t1[4] = {y0.x, y0.y, y1.x, y1.y};
+  bool val[4];
+  uint32_t slot[4], p[4], dn[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    val[i] = ok && kid[i] >= 0 && kid[i] < s.K && st[i] >= 0 && st[i] < s.NS && t0[i] >= 0 && t1[i] >= t0[i];
+    slot[i] = val[i] ? (uint32_t)kid[i] : (uint32_t)kStageK;
   }
-  buf_store_u64(ro, off, d);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) p[i] = atomicAdd(&s.cur[slot[i]], 1u);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) dn[i] = s.done[slot[i]];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint64_t d = (uint64_t)t1[i] - (uint64_t)t0[i];
+    uint32_t off = kOob;
+    if (val[i]) {
+      if (p[i] - dn[i] < (uint32_t)kStageW) s.stage[slot[i]][(p[i] + s.lo7) & (kStageW - 1)] = d;
+      else if (p[i] < s.len) off = p[i] * 8u;
+    }
+    buf_store_u64(ro, off, d);
+  }
 }
 
 // Flushes of the buffer path in two phases. Plan: each id with staged
@@ -443,7 +462,7 @@ __device__ __forceinline__ void stage_write(const StageCtx& s, __amdgpu_buffer_r
 
 __global__ __launch_bounds__(kStageThreads) void kde_scatter_staged_kernel(KdeArgs a) {
   __shared__ uint64_t stage[kStageK][kStageW];
-  __shared__ uint32_t cur[kStageK], done[kStageK];
+  __shared__ uint32_t cur[kStageK + 1], done[kStageK + 1];  // + the spare slot
   __shared__ uint32_t wave_tot[kStageThreads / kWave];
   __shared__ uint32_t claim, n_list;
   __shared__ FlushEntry list[kFlushCap];
@@ -519,11 +538,7 @@ __global__ __launch_bounds__(kStageThreads) void kde_scatter_staged_kernel(KdeAr
             const v2l x0 = __builtin_bit_cast(v2l, ba0[d]), x1 = __builtin_bit_cast(v2l, ba1[d]);
             const v2l y0 = __builtin_bit_cast(v2l, bb0[d]), y1 = __builtin_bit_cast(v2l, bb1[d]);
             load(d, rq + (int64_t)kStageD * kStageThreads);
-            const bool ok = rq < ng;
-            stage_one_buf(s, ro, ok, k4.x, s4.x, x0.x, y0.x);
-            stage_one_buf(s, ro, ok, k4.y, s4.y, x0.y, y0.y);
-            stage_one_buf(s, ro, ok, k4.z, s4.z, x1.x, y1.x);
-            stage_one_buf(s, ro, ok, k4.w, s4.w, x1.y, y1.y);
+            stage_four_buf(s, ro, rq < ng, k4, s4, x0, x1, y0, y1);
           }
           if (tid == 0) n_list = 0;
           lds_barrier();
