@@ -27,7 +27,7 @@
 //                        in LDS, exact bandwidth, integer-weight density
 //                        (sparse over occupied grid points when that is
 //                        cheaper), valleys, filters, and p50 / p99 by exact
-//                        radix selection inside the target grid bin. 7.5 KB of
+//                        radix selection inside the target grid bin. 7.8 KB of
 //                        LDS per wavefront; cells that need more go to a list.
 //   kde_cell_kernel<1>   the listed cells with 20 KB per wavefront;
 //   kde_cell_kernel<2>   what still does not fit, 105 KB per wavefront (any
@@ -54,14 +54,14 @@ constexpr int kRegVals = 4;       // cells of up to 256 durations stay in regist
 constexpr int kDigit = 6;         // radix-selection digit width (64 counters per target)
 
 // LDS per tier: grid words (histogram, chunk offsets, occupied-point list
-// and symmetric zero-padded weight table: at most 3 G + 2 T + 337 words; the
+// and symmetric zero-padded weight table: at most 3 G + 2 T + 465 words; the
 // selection lists of the wavefront tiers take 1,024) and valley capacity.
 // Tier 2 holds any grid of the duration range (at most 4,032 points, T < G).
 template <int TIER>
 struct Tier;
 template <>
 struct Tier<0> {
-  static constexpr int kWords = 1536, kCand = 64;
+  static constexpr int kWords = 1664, kCand = 64;
 };
 template <>
 struct Tier<1> {
@@ -69,7 +69,7 @@ struct Tier<1> {
 };
 template <>
 struct Tier<2> {
-  static constexpr int kWords = 20512, kCand = 2047;
+  static constexpr int kWords = 20640, kCand = 2047;
 };
 
 // n^-0.2 for small n, filled once per device from the host's pow().
@@ -678,36 +678,47 @@ __device__ __forceinline__ void load_small(const KdeArgs& a, const CellMeta& m, 
 // Zero padding of the symmetric weight table beyond T: the density loop
 // takes occupied grid points by whole histogram chunks of 64, so it meets
 // distances up to T + 126.
-constexpr int kWPad = 127;
+constexpr int kWPad = 191;
 
-// f(j) = sum_b c(b) w(|j - b|) for this lane's grid point j = jb + lane, in
-// registers, over the occupied grid points list[k0, k1) (pairs (b, c(b)),
-// read with wavefront-uniform addresses). ws is the symmetric weight table,
-// ws[d] = w(|d|), zero from T + 1 to T + kWPad. Eight points per step, so
-// eight weight reads are in flight; the list holds eight readable pairs past
-// its end. Acc = uint32_t is exact while the cell has fewer than 65,536
+// f(j) = sum_b c(b) w(|j - b|) for this lane's grid points j = jb + lane
+// (fa) and j + 64 (fb), in registers, over the occupied grid points
+// list[k0, k1) (pairs (b, c(b)), read with wavefront-uniform addresses): one
+// pass over the list serves both 64-point chunks. ws is the symmetric weight
+// table, ws[d] = w(|d|), zero from T + 1 to T + kWPad; the list range is
+// whole 64-point chunks covering the reach of both, [jb - T, jb + 127 + T],
+// so it starts at most 63 points lower and ends at most 63 higher, and every
+// |j - b| and |j + 64 - b| read is at most T + 190. Eight points per step, so sixteen
+// weight reads are in flight; the list holds eight readable pairs past its
+// end. Acc = uint32_t is exact while the cell has fewer than 65,536
 // durations (f <= 65536 n) and multiplies in 24 bits (c < 2^24, w <= 2^16).
 template <typename Acc>
-__device__ __forceinline__ Acc density_list(const uint32_t* ws, const uint2* list, int k0, int k1, int jb) {
+__device__ __forceinline__ void density_pair(const uint32_t* ws, const uint2* list, int k0, int k1, int jb, Acc& fa,
+                                             Acc& fb) {
   const int j = jb + lane_id();
   const uint32_t* wj = ws + j;
-  Acc fj = 0;
+  fa = fb = 0;
   for (int k = k0; k < k1; k += 8) {
-    uint32_t cb[8], wv[8];
+    uint32_t cb[8], wa[8], wb[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const uint2 e = list[k + u];
       const bool in = k + u < k1;
       cb[u] = in ? e.y : 0u;
-      wv[u] = wj[-(in ? (int)e.x : j)];
+      const int b = in ? (int)e.x : j;
+      wa[u] = wj[-b];
+      wb[u] = wj[kWave - b];
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      if constexpr (sizeof(Acc) == 4) fj += __umul24(cb[u], wv[u]);
-      else fj += (uint64_t)cb[u] * wv[u];
+      if constexpr (sizeof(Acc) == 4) {
+        fa += __umul24(cb[u], wa[u]);
+        fb += __umul24(cb[u], wb[u]);
+      } else {
+        fa += (uint64_t)cb[u] * wa[u];
+        fb += (uint64_t)cb[u] * wb[u];
+      }
     }
   }
-  return fj;
 }
 
 // Rank of this lane's element e (lane < k) among list[0, k) in ascending
@@ -811,46 +822,59 @@ __device__ bool kde_analyze(const KdeArgs& a, CellLds<TIER>& L, const CellMeta& 
     wave_sync();
     int carry_start = -1, carry_drop = 0;
     uint64_t prev_last = 0;
-    for (int jb = 0; jb < G; jb += kWave) {
-      const int j = jb + l;
-      const bool valid = j < G;
-      const int kb0 = (jb - T > 0 ? jb - T : 0) / kWave;
-      const int kb1 = (jb + kWave - 1 + T < G - 1 ? jb + kWave - 1 + T : G - 1) / kWave;
+    for (int jp = 0; jp < G; jp += 2 * kWave) {
+      // densities of the chunks at jp and jp + 64 in one pass over the list
+      const int kb0 = (jp - T > 0 ? jp - T : 0) / kWave;
+      const int kb1 = (jp + 2 * kWave - 1 + T < G - 1 ? jp + 2 * kWave - 1 + T : G - 1) / kWave;
       const int k0 = (int)cs[kb0], k1 = (int)cs[kb1 + 1];
-      uint64_t fj = n < 65536u ? (uint64_t)density_list<uint32_t>(ws, list, k0, k1, jb)
-                               : density_list<uint64_t>(ws, list, k0, k1, jb);
-      if (!valid) fj = 0;
-      uint64_t fl = __shfl_up(fj, 1, kWave);
-      if (l == 0) fl = prev_last;
-      const bool start = valid && (j == 0 || fj != fl);
-      const bool drop = start && j > 0 && fl > fj;
-      const bool rise = start && j > 0 && fl < fj;
-      const uint64_t S = __ballot(start), D = __ballot(drop);
-      int a_idx = carry_start, a_drop = carry_drop;
-      const uint64_t below = S & ((1ull << l) - 1ull);
-      if (below) {
-        const int al = 63 - __builtin_clzll(below);
-        a_idx = jb + al;
-        a_drop = (int)((D >> al) & 1ull);
+      uint64_t fpair[2];
+      if (n < 65536u) {
+        uint32_t fa, fb;
+        density_pair<uint32_t>(ws, list, k0, k1, jp, fa, fb);
+        fpair[0] = fa;
+        fpair[1] = fb;
+      } else {
+        density_pair<uint64_t>(ws, list, k0, k1, jp, fpair[0], fpair[1]);
       }
-      const bool is_valley = rise && a_drop;
-      const uint64_t Vb = __ballot(is_valley);
-      if (is_valley) {
-        const int idx = m + __popcll(Vb & ((1ull << l) - 1ull));
-        if (idx < CAND) {
-          L.cpos[idx] = (a_idx + j - 1) / 2;
-          L.cval[idx] = fl;
+      // valleys chunk by chunk, in grid order
+      for (int h = 0; h < 2; ++h) {
+        const int jb = jp + h * kWave;
+        if (jb >= G) break;
+        const int j = jb + l;
+        const bool valid = j < G;
+        uint64_t fj = valid ? fpair[h] : 0ull;
+        uint64_t fl = __shfl_up(fj, 1, kWave);
+        if (l == 0) fl = prev_last;
+        const bool start = valid && (j == 0 || fj != fl);
+        const bool drop = start && j > 0 && fl > fj;
+        const bool rise = start && j > 0 && fl < fj;
+        const uint64_t S = __ballot(start), D = __ballot(drop);
+        int a_idx = carry_start, a_drop = carry_drop;
+        const uint64_t below = S & ((1ull << l) - 1ull);
+        if (below) {
+          const int al = 63 - __builtin_clzll(below);
+          a_idx = jb + al;
+          a_drop = (int)((D >> al) & 1ull);
         }
+        const bool is_valley = rise && a_drop;
+        const uint64_t Vb = __ballot(is_valley);
+        if (is_valley) {
+          const int idx = m + __popcll(Vb & ((1ull << l) - 1ull));
+          if (idx < CAND) {
+            L.cpos[idx] = (a_idx + j - 1) / 2;
+            L.cval[idx] = fl;
+          }
+        }
+        m += __popcll(Vb);
+        if (TIER < 2 && m > CAND) return false;
+        if (S) {
+          const int ls = 63 - __builtin_clzll(S);
+          carry_start = jb + ls;
+          carry_drop = (int)((D >> ls) & 1ull);
+        }
+        const int last = G - 1 - jb < kWave - 1 ? G - 1 - jb : kWave - 1;
+        prev_last = readlane64(fj, last);
       }
-      m += __popcll(Vb);
-      if (TIER < 2 && m > CAND) return false;
-      if (S) {
-        const int ls = 63 - __builtin_clzll(S);
-        carry_start = jb + ls;
-        carry_drop = (int)((D >> ls) & 1ull);
-      }
-      const int last = G - 1 - jb < kWave - 1 ? G - 1 - jb : kWave - 1;
-      prev_last = readlane64(fj, last);
     }
     if (m > CAND) m = CAND;  // cannot happen in tier 2: a grid of G points has < G / 2 valleys
     wave_sync();
@@ -1318,11 +1342,12 @@ constexpr int kBlockThreads = 128;
 constexpr int kBlockWaves = kBlockThreads / kWave;
 constexpr int kBlockDepth = 8;  // duration loads in flight per thread in the streaming passes
 constexpr uint32_t kBlockMin = 2048;
-constexpr int kSelRegion = Tier<1>::kWords / kMaxT;  // 512 words per target
+constexpr int kSelRegion = 512;                      // words per target, within the tier-1 grid words
 constexpr int kSelDigit = 9;                         // log2(kSelRegion)
 constexpr int kSelCap = 64;
 static_assert(kMaxT % kBlockWaves == 0, "selection targets shared out over the wavefronts");
-static_assert((1 << kSelDigit) == kSelRegion && 2 * kSelCap <= kSelRegion, "selection regions");
+static_assert((1 << kSelDigit) == kSelRegion && 2 * kSelCap <= kSelRegion && kMaxT * kSelRegion <= Tier<1>::kWords,
+              "selection regions");
 
 __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) {
   __shared__ CellLds<1> L;
