@@ -1097,27 +1097,36 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
     wave_sync();
     if (ndirect > 0) {
       uint64_t* lists = reinterpret_cast<uint64_t*>(L.buf);  // kMaxT lists of kWave durations
-      auto gather = [&](uint64_t v) {
+      // four durations of the lane against each target in turn: a target's
+      // (wavefront-uniform) bin is read from LDS once per four durations
+      auto gather4 = [&](const uint64_t (&v)[4], const bool (&ok)[4]) {
         for (int t = 0; t < NT; ++t) {
           if (L.tpop[t] > (uint32_t)kWave) continue;
-          if (v >= L.tlb[t] && v < L.tub[t]) {
-            const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
-            if (slot < (uint32_t)kWave) lists[t * kWave + slot] = v;
+          const uint64_t lb = L.tlb[t], ub = L.tub[t];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            if (ok[u] && v[u] >= lb && v[u] < ub) {
+              const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
+              if (slot < (uint32_t)kWave) lists[t * kWave + slot] = v[u];
+            }
           }
         }
       };
       if (in_regs) {
+        bool ok[4];
 #pragma unroll
-        for (int r = 0; r < kRegVals; ++r)
-          if ((uint32_t)(l + r * kWave) < n) gather(rv[r]);
+        for (int r = 0; r < kRegVals; ++r) ok[r] = (uint32_t)(l + r * kWave) < n;
+        gather4(rv, ok);
       } else {
         for (uint64_t i0 = l; i0 < n; i0 += 4 * kWave) {
           uint64_t v[4];
+          bool ok[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-            if (i0 + u * kWave < n) gather(v[u]);
+          for (int u = 0; u < 4; ++u) {
+            ok[u] = i0 + u * kWave < n;
+            v[u] = ok[u] ? vals[i0 + u * kWave] : 0ull;
+          }
+          gather4(v, ok);
         }
       }
       wave_sync();
@@ -1153,29 +1162,36 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
     const int shift = kDigit * (npass - 1 - p);
     for (int i = l; i < NT * R; i += kWave) hist[i] = 0;
     wave_sync();
-    auto consider = [&](uint64_t v) {
+    // as in 9a: four durations against each open target in turn
+    auto consider4 = [&](const uint64_t (&v)[4], const bool (&ok)[4]) {
       for (int t = 0; t < NT; ++t) {
         if (L.tdone[t]) continue;
-        const uint64_t lb = L.tlb[t];
-        if (v >= lb && v < L.tub[t]) {
-          const uint64_t u = v - lb;
-          const uint64_t hi_part = shift + kDigit >= 64 ? 0 : u >> (shift + kDigit);
-          if (hi_part == L.tpre[t]) atomicAdd(&hist[t * R + (int)((u >> shift) & (R - 1))], 1u);
+        const uint64_t lb = L.tlb[t], ub = L.tub[t], pre = L.tpre[t];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          if (ok[w] && v[w] >= lb && v[w] < ub) {
+            const uint64_t u = v[w] - lb;
+            const uint64_t hi_part = shift + kDigit >= 64 ? 0 : u >> (shift + kDigit);
+            if (hi_part == pre) atomicAdd(&hist[t * R + (int)((u >> shift) & (R - 1))], 1u);
+          }
         }
       }
     };
     if (in_regs) {
+      bool ok[4];
 #pragma unroll
-      for (int r = 0; r < kRegVals; ++r)
-        if ((uint32_t)(l + r * kWave) < n) consider(rv[r]);
+      for (int r = 0; r < kRegVals; ++r) ok[r] = (uint32_t)(l + r * kWave) < n;
+      consider4(rv, ok);
     } else {
       for (uint64_t i0 = l; i0 < n; i0 += 4 * kWave) {
         uint64_t v[4];
+        bool ok[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          if (i0 + u * kWave < n) consider(v[u]);
+        for (int u = 0; u < 4; ++u) {
+          ok[u] = i0 + u * kWave < n;
+          v[u] = ok[u] ? vals[i0 + u * kWave] : 0ull;
+        }
+        consider4(v, ok);
       }
     }
     wave_sync();
