@@ -1135,7 +1135,16 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
         const int k = (int)L.tpop[t];
         const uint64_t* list = lists + t * kWave;
         const uint64_t e = l < k ? list[l] : 0ull;
-        const uint32_t rank = rank_in_list(list, k, e);
+        uint32_t rank = 0;
+        if (k <= 16) {
+          // few elements: compare against each one read from its lane
+          for (int i = 0; i < k; ++i) {
+            const uint64_t ei = readlane64(e, i);
+            rank += (ei < e || (ei == e && i < l)) ? 1u : 0u;
+          }
+        } else {
+          rank = rank_in_list(list, k, e);
+        }
         const uint64_t hit = __ballot(l < k && (uint64_t)rank == L.trank[t]);
         const uint64_t val = readlane64(e, hit ? __builtin_ctzll(hit) : 0);
         if (l == 0) {
