@@ -75,6 +75,10 @@ struct Tier<2> {
 // n^-0.2 for small n, filled once per device from the host's pow().
 __device__ double g_kde_pow[kPowTab];
 
+// n^-0.2 for the rare cells of kPowTab or more durations, out of line: inlined,
+// pow's constants are hoisted into the cell loops' registers and spilled there
+__device__ __attribute__((noinline)) double pow_m02(double n) { return pow(n, -0.2); }
+
 struct KdeArgs {
   const int32_t* kernel_id;
   const int32_t* stream;
@@ -789,7 +793,7 @@ __device__ bool kde_analyze(const KdeArgs& a, CellLds<TIER>& L, const CellMeta& 
     if (!__builtin_mul_overflow((uint64_t)n, s2, &ns2) && s1 < (1ull << 32)) vnum = (double)(ns2 - s1 * s1);
     else vnum = u128_to_f64((unsigned __int128)n * s2 - (unsigned __int128)s1 * s1);
     const double var = vnum / ((double)n * (double)(n - 1));
-    const double pw = n < (uint32_t)kPowTab ? cm.pw : pow((double)n, -0.2);
+    const double pw = n < (uint32_t)kPowTab ? cm.pw : pow_m02((double)n);
     const double h = 1.06 * sqrt(var) * pw;
     H = (int64_t)floor(h * 256.0 + 0.5);
   }
