@@ -701,12 +701,12 @@ __device__ __forceinline__ void density_pair(const uint32_t* ws, const uint2* li
   const int j = jb + lane_id();
   const uint32_t* wj = ws + j;
   fa = fb = 0;
-  for (int k = k0; k < k1; k += 8) {
+  auto step = [&](int k, bool tail) {
     uint32_t cb[8], wa[8], wb[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const uint2 e = list[k + u];
-      const bool in = k + u < k1;
+      const bool in = !tail || k + u < k1;  // wavefront-uniform
       cb[u] = in ? e.y : 0u;
       const int b = in ? (int)e.x : j;
       wa[u] = wj[-b];
@@ -722,7 +722,11 @@ __device__ __forceinline__ void density_pair(const uint32_t* ws, const uint2* li
         fb += (uint64_t)cb[u] * wb[u];
       }
     }
-  }
+  };
+  // whole steps of eight listed points need no bounds test; one tail step
+  int k = k0;
+  for (; k + 8 <= k1; k += 8) step(k, false);
+  if (k < k1) step(k, true);
 }
 
 // Rank of this lane's element e (lane < k) among list[0, k) in ascending
@@ -830,7 +834,7 @@ __device__ bool kde_analyze(const KdeArgs& a, CellLds<TIER>& L, const CellMeta& 
       // densities of the chunks at jp and jp + 64 in one pass over the list
       const int kb0 = (jp - T > 0 ? jp - T : 0) / kWave;
       const int kb1 = (jp + 2 * kWave - 1 + T < G - 1 ? jp + 2 * kWave - 1 + T : G - 1) / kWave;
-      const int k0 = (int)cs[kb0], k1 = (int)cs[kb1 + 1];
+      const int k0 = (int)__builtin_amdgcn_readfirstlane(cs[kb0]), k1 = (int)__builtin_amdgcn_readfirstlane(cs[kb1 + 1]);
       uint64_t fpair[2];
       if (n < 65536u) {
         uint32_t fa, fb;
