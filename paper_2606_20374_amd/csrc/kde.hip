@@ -54,14 +54,14 @@ constexpr int kRegVals = 4;       // cells of up to 256 durations stay in regist
 constexpr int kDigit = 6;         // radix-selection digit width (64 counters per target)
 
 // LDS per tier: grid words (histogram, chunk offsets, occupied-point list
-// and symmetric zero-padded weight table: at most 3 G + 2 T + 465 words; the
+// and symmetric zero-padded weight table: at most 3 G + 2 T + 515 words; the
 // selection lists of the wavefront tiers take 1,024) and valley capacity.
 // Tier 2 holds any grid of the duration range (at most 4,032 points, T < G).
 template <int TIER>
 struct Tier;
 template <>
 struct Tier<0> {
-  static constexpr int kWords = 1664, kCand = 64;
+  static constexpr int kWords = 1712, kCand = 64;
 };
 template <>
 struct Tier<1> {
@@ -69,7 +69,7 @@ struct Tier<1> {
 };
 template <>
 struct Tier<2> {
-  static constexpr int kWords = 20640, kCand = 2047;
+  static constexpr int kWords = 20688, kCand = 2047;
 };
 
 // n^-0.2 for small n, filled once per device from the host's pow().
@@ -614,6 +614,9 @@ __global__ __launch_bounds__(kStageThreads) void kde_scatter_staged_kernel(KdeAr
 template <int TIER>
 struct CellLds {
   static constexpr int W = Tier<TIER>::kWords, CA = Tier<TIER>::kCand;
+  // first, so that its LDS address is a multiple of 256 bytes and the weight
+  // reads' constant offsets fold into the instructions' offset fields
+  alignas(256) uint32_t buf[W];  // grid histogram (then its prefix) | analysis data; later selection data
   uint64_t cval[CA];    // valley depth f
   uint64_t tlb[kMaxT];  // target bin: smallest duration
   uint64_t tub[kMaxT];  // target bin: one past the largest duration
@@ -622,7 +625,6 @@ struct CellLds {
   uint32_t tpop[kMaxT];  // durations in the target bin
   uint32_t tdone[kMaxT]; // target already resolved
   uint32_t tcnt[kMaxT];  // durations gathered for the target so far
-  alignas(16) uint32_t buf[W];  // grid histogram (then its prefix) | analysis data; later selection data
   int32_t cpos[CA];     // valley grid index
   uint32_t th[64];
 };
@@ -680,37 +682,39 @@ __device__ __forceinline__ void load_small(const KdeArgs& a, const CellMeta& m, 
 }
 
 // Zero padding of the symmetric weight table beyond T: the density loop
-// takes occupied grid points by whole histogram chunks of 64, so it meets
-// distances up to T + 126.
-constexpr int kWPad = 191;
+// takes occupied grid points by whole histogram chunks of 64 for pairs of
+// chunks, so it meets distances up to T + 190.
+constexpr int kWPad = 192;  // >= 190 (see density_pair)
+constexpr int kListPad = 32;  // readable pairs past the list's end (a step reads 8)
+static_assert((2 * kListPad + kWPad) % 64 == 0 && kListPad >= 8 && kWPad >= 190, "weight table layout");
 
 // f(j) = sum_b c(b) w(|j - b|) for this lane's grid points j = jb + lane
 // (fa) and j + 64 (fb), in registers, over the occupied grid points
-// list[k0, k1) (pairs (b, c(b)), read with wavefront-uniform addresses): one
+// list[k0, k1) (pairs (4 b, c(b)), read with wavefront-uniform addresses): one
 // pass over the list serves both 64-point chunks. ws is the symmetric weight
 // table, ws[d] = w(|d|), zero from T + 1 to T + kWPad; the list range is
 // whole 64-point chunks covering the reach of both, [jb - T, jb + 127 + T],
 // so it starts at most 63 points lower and ends at most 63 higher, and every
 // |j - b| and |j + 64 - b| read is at most T + 190. Eight points per step, so sixteen
-// weight reads are in flight; the list holds eight readable pairs past its
+// weight reads are in flight; the list holds kListPad readable pairs past its
 // end. Acc = uint32_t is exact while the cell has fewer than 65,536
 // durations (f <= 65536 n) and multiplies in 24 bits (c < 2^24, w <= 2^16).
 template <typename Acc>
 __device__ __forceinline__ void density_pair(const uint32_t* ws, const uint2* list, int k0, int k1, int jb, Acc& fa,
                                              Acc& fb) {
   const int j = jb + lane_id();
-  const uint32_t* wj = ws + j;
+  const char* wj = reinterpret_cast<const char*>(ws + j);
   fa = fb = 0;
   auto step = [&](int k, bool tail) {
     uint32_t cb[8], wa[8], wb[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const uint2 e = list[k + u];
+      const uint2 e = list[k + u];  // (4 b, c(b)): the byte offset of ws[j - b] below ws + j
       const bool in = !tail || k + u < k1;  // wavefront-uniform
       cb[u] = in ? e.y : 0u;
-      const int b = in ? (int)e.x : j;
-      wa[u] = wj[-b];
-      wb[u] = wj[kWave - b];
+      const uint32_t ob = in ? e.x : 4u * (uint32_t)j;
+      wa[u] = *reinterpret_cast<const uint32_t*>(wj - ob);
+      wb[u] = *reinterpret_cast<const uint32_t*>(wj + 4 * kWave - ob);
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -763,8 +767,10 @@ __device__ bool kde_analyze(const KdeArgs& a, CellLds<TIER>& L, const CellMeta& 
   uint32_t* cgrid = L.buf;
   // 2. bandwidth from the exact first and second moments of the grid index;
   // the occupied grid points are listed on the way, in ascending order, as
-  // (b, c(b)) pairs, with cs[i] = pairs before histogram chunk i. LDS words:
-  // [0, G) histogram | cs | list (+ 8 pairs) | weight table
+  // (4 b, c(b)) pairs, with cs[i] = pairs before histogram chunk i. LDS words:
+  // [0, G) histogram | cs | list (+ kListPad pairs) | weight table; 2 kListPad + kWPad
+  // is a multiple of 64 words, so the weight reads' constant part is a multiple of
+  // 256 bytes and folds into the instructions' offsets
   const int NCH = (G + kWave - 1) / kWave + 1;
   uint32_t* cs = L.buf + G;
   const int lofs = (G + NCH + 1) & ~1;
@@ -780,12 +786,12 @@ __device__ bool kde_analyze(const KdeArgs& a, CellLds<TIER>& L, const CellMeta& 
     if (l == 0) cs[ch] = (uint32_t)nnz;
     if (k != 0) {
       const int idx = nnz + __popcll(occ & ((1ull << l) - 1ull));
-      if (TIER == 2 || lofs + 2 * idx + 1 < WORDS) list[idx] = make_uint2((uint32_t)j, k);
+      if (TIER == 2 || lofs + 2 * idx + 1 < WORDS) list[idx] = make_uint2(4u * (uint32_t)j, k);  // (4 b, c(b))
     }
     nnz += __popcll(occ);
   }
   if (l == 0) cs[NCH - 1] = (uint32_t)nnz;
-  const int tofs = lofs + 2 * (nnz + 8);
+  const int tofs = lofs + 2 * (nnz + kListPad);
   if (TIER < 2 && tofs > WORDS) return false;
   s1 = wave_sum_u64(s1);
   s2 = wave_sum_u64(s2);
