@@ -1721,9 +1721,15 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
     int r0 = 0;
     for (int j = 0; j < G; ++j) {
       const int b0 = j - T > 0 ? j - T : 0, b1 = j + T < G - 1 ? j + T : G - 1;
+      // left of j the distance falls to 0, right of it it rises from 1: two
+      // loops walk the weight column by pointer (counts < 256, weights <= 2^16)
       uint32_t f = 0;
+      const uint32_t* wl = &L.w[j - b0][l];
 #pragma unroll 4
-      for (int b = b0; b <= b1; ++b) f += lane_cnt(L, b, l) * L.w[j > b ? j - b : b - j][l];
+      for (int b = b0; b <= j; ++b, wl -= kWave) f += __umul24(lane_cnt(L, b, l), *wl);
+      const uint32_t* wr = &L.w[1][l];
+#pragma unroll 4
+      for (int b = j + 1; b <= b1; ++b, wr += kWave) f += __umul24(lane_cnt(L, b, l), *wr);
       if (j == 0) {
         v = f;
       } else if (f != v) {
