@@ -1623,7 +1623,7 @@ constexpr int kLaneList = 16;   // durations of one target grid bin
 
 template <int GC>
 struct LaneLds {
-  uint32_t cp[GC / 4][kWave];      // grid counts, then inclusive prefix counts: four 8-bit values per word
+  alignas(4) uint8_t cp[GC][kWave];  // grid counts, then inclusive prefix counts (8 bits: n <= 255)
   uint32_t w[kLaneT][kWave];       // kernel weights; later the durations of one target bin (lo, hi words)
   uint32_t cand[kLaneCand][kWave]; // valleys: density << 8 | grid index
   uint32_t th[64];
@@ -1631,7 +1631,7 @@ struct LaneLds {
 
 template <int GC>
 __device__ __forceinline__ uint32_t lane_cnt(const LaneLds<GC>& L, int j, int l) {
-  return (L.cp[j >> 2][l] >> ((j & 3) * 8)) & 0xFFu;
+  return L.cp[j][l];
 }
 
 template <int GC>
@@ -1667,7 +1667,7 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
 
   // 1. grid histogram; eight loads in flight per lane, and LDS adds that
   // return nothing, so no iteration waits on the previous one
-  for (int j = 0; j < (G + 3) / 4; ++j) L.cp[j][l] = 0;
+  for (int j = 0; j < G; ++j) L.cp[j][l] = 0;
   bool out_of_range = false;
   for (uint32_t i0 = 0; i0 < n; i0 += 8) {
     uint64_t d[8];
@@ -1677,7 +1677,8 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
     for (int u = 0; u < 8; ++u) {
       if (i0 + u >= n) break;
       const int x = (grid64(d[u], L.th) >> sh) - lo;
-      if (x >= 0 && x < G) atomicAdd(&L.cp[x >> 2][l], 1u << ((x & 3) * 8));
+      // the lane's count byte lives in a word shared with three other lanes
+      if (x >= 0 && x < G) atomicAdd(reinterpret_cast<uint32_t*>(&L.cp[x][l & ~3]), 1u << ((l & 3) * 8));
       else out_of_range = true;
     }
   }
@@ -1725,11 +1726,12 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
       // loops walk the weight column by pointer (counts < 256, weights <= 2^16)
       uint32_t f = 0;
       const uint32_t* wl = &L.w[j - b0][l];
+      const uint8_t* cl = &L.cp[b0][l];
 #pragma unroll 4
-      for (int b = b0; b <= j; ++b, wl -= kWave) f += __umul24(lane_cnt(L, b, l), *wl);
+      for (int b = b0; b <= j; ++b, wl -= kWave, cl += kWave) f += __umul24(*cl, *wl);
       const uint32_t* wr = &L.w[1][l];
 #pragma unroll 4
-      for (int b = j + 1; b <= b1; ++b, wr += kWave) f += __umul24(lane_cnt(L, b, l), *wr);
+      for (int b = j + 1; b <= b1; ++b, wr += kWave, cl += kWave) f += __umul24(*cl, *wr);
       if (j == 0) {
         v = f;
       } else if (f != v) {
@@ -1748,15 +1750,9 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
   // grid counts -> inclusive prefix counts (at most n <= 255), in place
   {
     uint32_t run = 0;
-    for (int j = 0; j < (G + 3) / 4; ++j) {
-      const uint32_t wd = L.cp[j][l];
-      uint32_t out = 0;
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        run += (wd >> (8 * b)) & 0xFFu;
-        out |= run << (8 * b);
-      }
-      L.cp[j][l] = out;
+    for (int j = 0; j < G; ++j) {
+      run += L.cp[j][l];
+      L.cp[j][l] = (uint8_t)run;
     }
   }
   auto P = [&](int j) -> uint32_t { return j < 0 ? 0u : lane_cnt(L, j, l); };
