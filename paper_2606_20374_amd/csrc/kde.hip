@@ -1620,6 +1620,7 @@ constexpr int kLaneGW = 256;    // grid points per cell, second lane pass (liste
 constexpr int kLaneT = 32;      // kernel weights (t < 32)
 constexpr int kLaneCand = 8;    // valleys before filtering
 constexpr int kLaneList = 16;   // durations of one target grid bin
+static_assert(2 * kLaneList <= kLaneT, "two target lists in the weight words");
 
 template <int GC>
 struct LaneLds {
@@ -1795,50 +1796,92 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
   }
 
   // 8. per cluster: count, then p50 / p99 as the element of the wanted rank
-  // inside its grid bin, found among the bin's durations gathered in LDS
+  // inside its grid bin, found among the bin's durations gathered in LDS. The
+  // targets' ranks increase, so the bin search goes on from the last bin. A
+  // cluster's two bins are gathered in one pass over the durations, as 32-bit
+  // offsets from the bin start (16 words each), when both bins are narrower
+  // than 2^32 ns; otherwise one bin per pass as 64-bit values (32 words).
   const int ncl = m + 1;
   uint32_t before = 0;
+  int jc = 0;
   for (int q = 0; q < ncl; ++q) {
     const uint32_t hiP = P(hi_of(q, m)), size = hiP - before;
     for (int qq = 0; qq < kMaxC; ++qq)
       if (qq == q) cnt[qq] = size;
+    uint32_t rr[2], k[2];
+    uint64_t lb[2], ub[2];
+    bool narrow = true;
     for (int t2 = 0; t2 < 2; ++t2) {
       const uint32_t r = t2 == 0 ? before + (size - 1) / 2 : before + (99 * size + 99) / 100 - 1;
-      int j = 0;
-      while (P(j) <= r) ++j;  // smallest grid index whose prefix count passes r
-      const uint32_t below = P(j - 1), k = P(j) - below;
-      if (k > (uint32_t)kLaneList) return false;
-      const uint64_t lb = grid64_lb((lo + j) << sh, L.th), ub = grid64_lb((lo + j + 1) << sh, L.th);
-      uint32_t got = 0;
-      for (uint32_t i0 = 0; i0 < n && got < k; i0 += 8) {
+      while (P(jc) <= r) ++jc;  // smallest grid index whose prefix count passes r
+      const uint32_t below = P(jc - 1);
+      k[t2] = P(jc) - below;
+      if (k[t2] > (uint32_t)kLaneList) return false;
+      rr[t2] = r - below;
+      lb[t2] = grid64_lb((lo + jc) << sh, L.th);
+      ub[t2] = grid64_lb((lo + jc + 1) << sh, L.th);
+      narrow = narrow && ub[t2] - lb[t2] <= (1ull << 32);
+    }
+    const bool same = lb[1] == lb[0];
+    uint64_t pick[2] = {0, 0};
+    if (narrow) {
+      // list t at words [16 t, 16 t + k[t]): offsets from lb[t]
+      uint32_t got0 = 0, got1 = same ? k[1] : 0u;
+      for (uint32_t i0 = 0; i0 < n && (got0 < k[0] || got1 < k[1]); i0 += 8) {
         uint64_t d[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) d[u] = i0 + u < n ? vals[i0 + u] : ~0ull;
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          if (d[u] >= lb && d[u] < ub && got < k) {
-            L.w[2 * got][l] = (uint32_t)d[u];
-            L.w[2 * got + 1][l] = (uint32_t)(d[u] >> 32);
-            ++got;
+          if (d[u] >= lb[0] && d[u] < ub[0] && got0 < k[0]) L.w[got0++][l] = (uint32_t)(d[u] - lb[0]);
+          if (!same && d[u] >= lb[1] && d[u] < ub[1] && got1 < k[1]) L.w[kLaneList + got1++][l] = (uint32_t)(d[u] - lb[1]);
+        }
+      }
+      for (int t2 = 0; t2 < 2; ++t2) {
+        const int base = same ? 0 : t2 * kLaneList;
+        uint32_t off = 0;
+        for (uint32_t i = 0; i < k[t2]; ++i) {
+          const uint32_t e = L.w[base + i][l];
+          uint32_t rank = 0;
+          for (uint32_t x = 0; x < k[t2]; ++x) {
+            const uint32_t y = L.w[base + x][l];
+            rank += (y < e || (y == e && x < i)) ? 1u : 0u;
+          }
+          if (rank == rr[t2]) off = e;
+        }
+        pick[t2] = lb[t2] + off;
+      }
+    } else {
+      for (int t2 = 0; t2 < 2; ++t2) {
+        uint32_t got = 0;
+        for (uint32_t i0 = 0; i0 < n && got < k[t2]; i0 += 8) {
+          uint64_t d[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) d[u] = i0 + u < n ? vals[i0 + u] : ~0ull;
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            if (d[u] >= lb[t2] && d[u] < ub[t2] && got < k[t2]) {
+              L.w[2 * got][l] = (uint32_t)d[u];
+              L.w[2 * got + 1][l] = (uint32_t)(d[u] >> 32);
+              ++got;
+            }
           }
         }
-      }
-      const uint32_t rr = r - below;
-      uint64_t pick = 0;
-      for (uint32_t i = 0; i < k; ++i) {
-        const uint64_t e = ((uint64_t)L.w[2 * i + 1][l] << 32) | L.w[2 * i][l];
-        uint32_t rank = 0;
-        for (uint32_t x = 0; x < k; ++x) {
-          const uint64_t y = ((uint64_t)L.w[2 * x + 1][l] << 32) | L.w[2 * x][l];
-          rank += (y < e || (y == e && x < i)) ? 1u : 0u;
+        for (uint32_t i = 0; i < k[t2]; ++i) {
+          const uint64_t e = ((uint64_t)L.w[2 * i + 1][l] << 32) | L.w[2 * i][l];
+          uint32_t rank = 0;
+          for (uint32_t x = 0; x < k[t2]; ++x) {
+            const uint64_t y = ((uint64_t)L.w[2 * x + 1][l] << 32) | L.w[2 * x][l];
+            rank += (y < e || (y == e && x < i)) ? 1u : 0u;
+          }
+          if (rank == rr[t2]) pick[t2] = e;
         }
-        if (rank == rr) pick = e;
       }
-      for (int qq = 0; qq < kMaxC; ++qq) {
-        if (qq != q) continue;
-        if (t2 == 0) p50[qq] = pick;
-        else p99[qq] = pick;
-      }
+    }
+    for (int qq = 0; qq < kMaxC; ++qq) {
+      if (qq != q) continue;
+      p50[qq] = pick[0];
+      p99[qq] = pick[1];
     }
     before = hiP;
   }
