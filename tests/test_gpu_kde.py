@@ -154,6 +154,11 @@ def test_kde_hand_built_groups():
         comps = [np.exp(np.log(30_000 * 4**i) + 0.1 * np.clip(rng.normal(0, 1, m), -4, 4)).astype(np.uint64)
                  for i, m in enumerate(sizes)]
         groups.append(np.concatenate(comps))
+    # lane-pass cells whose target bins are wider than 2^32 ns (64-bit lists)
+    # and just narrower (32-bit offsets close to 2^32), one bimodal
+    for centre in (1e12, 3e11):
+        groups.append(np.exp(rng.normal(np.log(centre), 0.05, 100)).astype(np.uint64))
+    groups.append(np.concatenate([np.exp(rng.normal(np.log(c), 0.02, 60)).astype(np.uint64) for c in (1e12, 2e12)]))
     K = len(groups) + 3  # a few empty kernel ids
     ev = _groups_to_events(groups, K, 4)
     k, o = _both(ev, 1, 1, K, 4, "hand-built")
