@@ -245,15 +245,17 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
             } else if (z >= kPhiZ) {
               ph = 1.0;
             } else {
-              const double sx = (z + kPhiZ) * (double)kPhiSteps;
+              // fused multiply-adds: their rounding differs from separate
+              // operations by far less than the band below allows for
+              const double sx = fma(z, (double)kPhiSteps, kPhiZ * (double)kPhiSteps);
               int i = (int)sx;
               i = i < kPhiN - 1 ? i : kPhiN - 1;
               const double t = sx - (double)i;
               const double* cf = tab + 4 * i;
-              ph = cf[0] + t * (cf[1] + t * (cf[2] + t * cf[3]));
+              ph = fma(t, fma(t, fma(t, cf[3], cf[2]), cf[1]), cf[0]);
             }
           }
-          F += wt[cl] * ph;
+          F = fma(wt[cl], ph, F);
         }
         const double v = F * 65536.0;
         const uint32_t qa = quant16(v - kBand), qb = quant16(v + kBand);
