@@ -12,7 +12,9 @@ import os
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "liboracle.so")
+# ARGUS_ORACLE_LIB names another build of the same sources (the sanitizer
+# build of the test suite)
+LIB_PATH = os.environ.get("ARGUS_ORACLE_LIB") or os.path.join(HERE, "liboracle.so")
 NB = 32
 
 # Proposed defaults (the paper prints no values for these thresholds).

@@ -258,8 +258,10 @@ void orc_kde_group(int64_t n, const uint64_t* durations, int32_t sub_bits, int32
   uint32_t th[64];
   kde_thresholds(th);
   uint64_t* d = malloc((size_t)(n > 0 ? n : 1) * sizeof(uint64_t));
-  memcpy(d, durations, (size_t)n * sizeof(uint64_t));
-  qsort(d, (size_t)n, sizeof(uint64_t), cmp_u64);
+  if (n > 0) {
+    memcpy(d, durations, (size_t)n * sizeof(uint64_t));
+    qsort(d, (size_t)n, sizeof(uint64_t), cmp_u64);
+  }
   kde_group(n, d, sub_bits, frac_pm, min_count, gap, th, n_clusters, cnt, p50, p99, bw_q8, n_cand, f_dbg,
             cand_dbg);
   free(d);
