@@ -327,6 +327,11 @@ int argus_iter_windows(const int64_t* step_ns, int32_t n_ranks, int32_t n_steps,
  *     with the largest f (the upper one on ties).
  *  8. Per cluster, ascending: count; p50 = the lower median and p99 = the
  *     element ceil(0.99 m) (nearest rank) of its m raw durations, sorted.
+ * Steps 1-3 approximate Eq. 1: samples are floored onto the grid, the
+ * bandwidth comes from the floored values and is rounded to 1/256 step, and
+ * the weights are 16-bit integers. Against Eq. 1 evaluated exactly (raw logs,
+ * unrounded bandwidth, float64 Gaussian) the tested groups keep the same
+ * number of clusters, with at most 6.5e-4 of the samples in another cluster.
  * The only floating-point steps are sqrt, n^-0.2 and exp in step 2 and 3;
  * integer outputs follow from them exactly. Thresholds and tie rules are
  * this library's readings: the paper names the filters but gives no values.

@@ -43,6 +43,15 @@
  *  - p50 = lower median, p99 = nearest-rank 99th percentile (element
  *    ceil(0.99 m) of the m sorted durations) of each cluster's raw durations.
  *
+ * The floored samples, the quantised bandwidth and the integer weights make
+ * this an approximation of Eq. 1. Its distance from Eq. 1 as printed (float64
+ * Gaussian KDE of the raw logs with the unquantised bandwidth, same valley and
+ * filter rules) is measured and bounded in tests/test_oracle_kde_eq1.py: the
+ * same number of clusters in every group tested, boundaries displaced only
+ * across empty cells, by one grid step, or inside a valley bottom where Eq. 1
+ * itself is flat to 1e-3, and at most 6.5e-4 of the samples assigned to
+ * another cluster.
+ *
  * Parity pins (tests/test_oracle_kde.py): the threshold table and grid
  * function against exact big-integer logarithms; bandwidth against the closed
  * form of two-spike data; hand-worked spike patterns for each filter rule and
