@@ -71,6 +71,7 @@ extern "C" {
 #define ARGUS_KDE_MAXC 4         /* argus_kde: clusters reported per cell */
 #define ARGUS_MAX_W1_RANKS 16384 /* argus_w1: n_ranks limit */
 #define ARGUS_MAX_W1_GRID 2048   /* argus_w1: grid points limit */
+#define ARGUS_MAX_W1_STEPS 65535 /* argus_w1: n_steps limit */
 #define ARGUS_MAX_L2_RANKS 65536 /* argus_l2: n_ranks limit */
 #define ARGUS_MAX_L2_DIMS 16     /* argus_l2: parallelism dimensions limit */
 
@@ -95,7 +96,10 @@ enum {
   ARGUS_DEV_GROUPS_DUPLICATE = 32, /* argus_l2: a rank listed more than once in one dimension (only its first
                                       listing counts) */
   ARGUS_DEV_L2_DOMAIN = 64,        /* argus_l2: a mean duration at or above 2^40 ns (that cell is left out) */
-  ARGUS_DEV_COMPACT_CAPACITY = 128 /* argus_compact: the records did not all fit in the caller's buffer */
+  ARGUS_DEV_COMPACT_CAPACITY = 128, /* argus_compact: the records did not all fit in the caller's buffer */
+  ARGUS_DEV_SUMMARY_STALLED = 256   /* argus_summarize: a bounded wait inside the kernel expired in every one of
+                                       its redo passes over some segment (never expected: it means a defect in
+                                       the library or the device); that segment's cells may be incomplete */
 };
 
 int argus_abi_version(void);
@@ -433,7 +437,8 @@ size_t argus_w1_workspace(int32_t n_ranks, int32_t n_steps, int32_t n_kernels, i
 
 /* clusters: the n_clusters, count, p50_ns and p99_ns outputs of argus_kde
  * ([n_ranks][n_steps][n_kernels] and [..][ARGUS_KDE_MAXC]); count, p50_ns and
- * p99_ns must be 16-byte aligned. n_ranks <= ARGUS_MAX_W1_RANKS. Every output
+ * p99_ns must be 16-byte aligned. n_ranks <= ARGUS_MAX_W1_RANKS, n_steps <=
+ * ARGUS_MAX_W1_STEPS. Every output
  * except dev_status is required; the workspace must be 256-byte aligned and
  * not shared by calls that may overlap. */
 int argus_w1(const argus_kde_out_t* clusters, int32_t n_ranks, int32_t n_steps, int32_t n_kernels,

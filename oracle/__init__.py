@@ -7,6 +7,7 @@ package. Inputs and outputs are numpy arrays on the host.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 
 import numpy as np
@@ -59,6 +60,8 @@ def lib():
         L.orc_w1.restype = ctypes.c_int
         L.orc_w1_cdf_q.argtypes = [I32, V, V, V, ctypes.c_double]
         L.orc_w1_cdf_q.restype = ctypes.c_uint32
+        L.orc_w1_cdf_q_at.argtypes = [I32, V, V, V, ctypes.c_double]
+        L.orc_w1_cdf_q_at.restype = ctypes.c_uint32
         L.orc_l2.argtypes = [I32, I32, I32] + [V] * 5 + [I32] * 6 + [V] * 8
         L.orc_l2.restype = ctypes.c_int
         _lib = L
@@ -255,6 +258,18 @@ def w1_cdf_q(count, p50, p99, x: float) -> int:
     a = np.ascontiguousarray(p50, dtype=np.int64)
     b = np.ascontiguousarray(p99, dtype=np.int64)
     return lib().orc_w1_cdf_q(len(cnt), _p(cnt), _p(a), _p(b), x)
+
+
+def w1_cdf_q_grid(count, p50, p99, lo: int, hi: int, g: int, G: int) -> int:
+    """The 16-bit mixture CDF of one rank's clusters at grid point g of the
+    W1 grid [lo, hi] with G points, u = ln lo + g (ln hi - ln lo) / (G - 1),
+    as the oracle's W1 takes it."""
+    cnt = np.ascontiguousarray(count, dtype=np.uint32)
+    a = np.ascontiguousarray(p50, dtype=np.int64)
+    b = np.ascontiguousarray(p99, dtype=np.int64)
+    lnlo, lnhi = math.log(float(lo)), math.log(float(hi))
+    u = lnlo + float(g) * ((lnhi - lnlo) / float(G - 1))
+    return lib().orc_w1_cdf_q_at(len(cnt), _p(cnt), _p(a), _p(b), u)
 
 
 def l2(count, sum_ns, R: int, S: int, E: int, route, group_off, members, **params) -> dict:

@@ -207,3 +207,9 @@ int orc_w1(int32_t R, int32_t S, int32_t K, const uint8_t* n_clusters, const uin
 uint32_t orc_w1_cdf_q(int32_t ncl, const uint32_t* count, const int64_t* p50, const int64_t* p99, double x) {
   return mixture_q(ncl, count, p50, p99, log(x));
 }
+
+/* The same at log-duration u, as the score takes it at grid point g:
+ * u = ln lo + g (ln hi - ln lo) / (G - 1) (tests). */
+uint32_t orc_w1_cdf_q_at(int32_t ncl, const uint32_t* count, const int64_t* p50, const int64_t* p99, double u) {
+  return mixture_q(ncl, count, p50, p99, u);
+}

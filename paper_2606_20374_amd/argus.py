@@ -21,7 +21,9 @@ NBINS = 32
 OK, EINVAL, EUNSUPPORTED, EHIP = 0, -1, -2, -3
 DEV_BAD_SEGMENT, DEV_L1_DOMAIN, DEV_KDE_SUMMARY, DEV_W1_INPUT = 1, 2, 4, 8
 DEV_GROUPS_MALFORMED, DEV_GROUPS_DUPLICATE, DEV_L2_DOMAIN, DEV_COMPACT_CAPACITY = 16, 32, 64, 128
+DEV_SUMMARY_STALLED = 256
 KDE_MAXC = 4
+MAX_W1_STEPS = 65535
 
 V, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
 

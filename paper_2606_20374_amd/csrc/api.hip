@@ -238,7 +238,8 @@ int argus_w1(const argus_kde_out_t* clusters, int32_t n_ranks, int32_t n_steps, 
              const argus_w1_params_t* params, const argus_w1_out_t* out, void* workspace, size_t workspace_bytes,
              void* stream) {
   if (!clusters || !params || !out) return ARGUS_EINVAL;
-  if (n_ranks < 1 || n_ranks > ARGUS_MAX_W1_RANKS || n_steps < 1 || n_kernels < 1) return ARGUS_EINVAL;
+  if (n_ranks < 1 || n_ranks > ARGUS_MAX_W1_RANKS || n_steps < 1 || n_steps > ARGUS_MAX_W1_STEPS || n_kernels < 1)
+    return ARGUS_EINVAL;
   const int64_t SK = (int64_t)n_steps * n_kernels;
   if (SK > INT32_MAX || SK * n_ranks > INT32_MAX) return ARGUS_EINVAL;
   const argus_w1_params_t& p = *params;

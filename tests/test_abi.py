@@ -135,7 +135,7 @@ def test_w1_defaults_and_workspace():
     lambda c, p, o, d: setattr(o, "score", None),
     lambda c, p, o, d: d.__setitem__("R", 16385),
     lambda c, p, o, d: d.__setitem__("S", 0),
-    "misaligned", "small",
+    "misaligned", "small", "steps",
 ])
 def test_w1_rejects_bad_arguments(mutate):
     c = A.KdeOut(0x1000, 0x1000, 0x1000, 0x1000, None, None)
@@ -148,6 +148,9 @@ def test_w1_rejects_bad_arguments(mutate):
         ws = 0x10080
     elif mutate == "small":
         n = 2 * 8 * 2 * 4 * 64 - 1
+    elif mutate == "steps":  # one step above the limit, everything else valid
+        d["S"] = A.MAX_W1_STEPS + 1
+        n = 2 * 8 * d["S"] * 4 * 64
     else:
         mutate(c, p, o, d)
     assert pa.lib().argus_w1(ctypes.byref(c), d["R"], d["S"], d["K"], ctypes.byref(p), ctypes.byref(o), ws, n,

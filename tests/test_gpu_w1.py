@@ -14,10 +14,19 @@ percentiles, durations near 2^63, identical ranks, one present rank, too few
 ranks, malformed records, the smallest and a large grid, ragged rank counts
 up to the 16,384-rank limit), W1 over the oracle's own KDE clusters of the
 tiny and medium traces, the full GPU chain summarize -> kde -> w1 on the tiny
-trace, and the production and cluster workloads at full size in the launch
-configuration the benchmark times, checked on sampled kernels.
+trace, and the production, cluster and skew workloads at full size in the
+launch configuration the benchmark times: there every KDE cell is compared
+with the oracle, and W1 on 48-64 kernels that include the ten heaviest ids
+(the skew workload's eight hot Pareto ids among them).
+
+The 16-bit CDF values the score is built from (the workspace) are compared
+with the oracle's at sampled grid points of every case: they may differ by
+one unit only where the mixture lies within rounding of a multiple of
+1/65536 (device and host log / erfc differ in the last place), and the test
+counts such points and bounds them.
 """
 import gc
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 import pytest
@@ -86,11 +95,49 @@ def assert_w1_equal(gw: dict, ow: dict, R, S, K, what, kernels=None, max_ambiguo
     return n_amb
 
 
+def check_cdf_values(gw, ncl, cnt, a, b, R, S, K, what, n_points=4000, seed=0, kernels=None):
+    """Sampled 16-bit CDF values of the workspace ([S][K][G][R]) against the
+    oracle's at the same grid points. ncl/cnt/a/b: the clusters W1 ran on,
+    [R][S][K] (cnt/a/b with KDE_MAXC slots). Returns the number of points
+    that differ (by one unit at most)."""
+    G = int(gw["_grid"])
+    ncl = np.asarray(ncl).reshape(R, S, K)
+    cnt = np.asarray(cnt).reshape(R, S, K, MAXC)
+    a = np.asarray(a).reshape(R, S, K, MAXC)
+    b = np.asarray(b).reshape(R, S, K, MAXC)
+    npres = P.to_np(gw["n_present"]).reshape(S, K)
+    lo = P.to_np(gw["lo_ns"]).reshape(S, K)
+    hi = P.to_np(gw["hi_ns"]).reshape(S, K)
+    ks = np.arange(K) if kernels is None else np.asarray(kernels)
+    ev_sk = [(s, k) for s in range(S) for k in ks if npres[s, k] >= 3]
+    if not ev_sk:
+        return 0
+    rng = np.random.default_rng(seed)
+    pts = []
+    while len(pts) < n_points:
+        s, k = ev_sk[int(rng.integers(len(ev_sk)))]
+        r = int(rng.integers(R))
+        if 1 <= ncl[r, s, k] <= MAXC and cnt[r, s, k, :ncl[r, s, k]].sum() > 0:
+            pts.append((s, k, int(rng.integers(G)), r))
+    idx = torch.tensor([((s * K + k) * G + g) * R + r for s, k, g, r in pts], dtype=torch.int64)
+    ws = gw["_workspace"].view(torch.int16)
+    got = ws[idx.to(ws.device)].cpu().numpy().view(np.uint16).astype(np.int64)
+    want = np.array([oracle.w1_cdf_q_grid(cnt[r, s, k, :ncl[r, s, k]], a[r, s, k, :ncl[r, s, k]],
+                                          b[r, s, k, :ncl[r, s, k]], lo[s, k], hi[s, k], g, G)
+                     for s, k, g, r in pts], dtype=np.int64)
+    diff = np.abs(got - want)
+    assert diff.max() <= 1, (what, "cdf values", pts[int(diff.argmax())], got[diff.argmax()], want[diff.argmax()])
+    n_diff = int((diff > 0).sum())
+    assert n_diff <= max(1, n_points // 1000), (what, "cdf values differing by one unit", n_diff)
+    return n_diff
+
+
 def _both(ncl, cnt, a, b, R, S, K, what, **params):
     gw = pa.w1(_dev_clusters(ncl, cnt, a, b), R, S, K, **params)
     torch.cuda.synchronize()
     ow = oracle.w1(ncl, cnt, a, b, R, S, K, **params)
     assert_w1_equal(gw, ow, R, S, K, what)
+    check_cdf_values(gw, ncl, cnt, a, b, R, S, K, what, n_points=500)
     expect = pa.argus.DEV_W1_INPUT if ow["malformed"] else 0
     assert int(gw["dev_status"].item()) == expect, what
     return gw, ow
@@ -196,6 +243,7 @@ def test_w1_full_chain_tiny():
     ko = oracle.kde(t.fill_host(), K, NS)
     ow = oracle.w1(ko["n_clusters"], ko["count"], ko["p50_ns"], ko["p99_ns"], R, S, K)
     assert_w1_equal(gw, ow, R, S, K, "tiny chain")
+    check_cdf_values(gw, ko["n_clusters"], ko["count"], ko["p50_ns"], ko["p99_ns"], R, S, K, "tiny chain")
     truth = t.truth()
     (strag,) = truth["stragglers"]
     flag = P.to_np(gw["flag"]).reshape(R, S, K)
@@ -205,8 +253,37 @@ def test_w1_full_chain_tiny():
         assert flag[pr, :, pk].all()
 
 
-def _full_size(name, n_sample):
-    _announce(f"w1 full size {name}: GPU summarize -> kde -> w1, {n_sample} sampled kernels")
+def heaviest_ids(trace, n):
+    """The n kernel ids with the most events in the workload's template."""
+    counts = np.bincount(trace.tmpl_kid, minlength=trace.cfg.n_kernels)
+    return np.argsort(-counts, kind="stable")[:n]
+
+
+def oracle_w1_kernels(ko, R, S, K, ks, n_threads=None):
+    """The oracle's W1 of kernels ks only (one pairwise oracle call per
+    kernel, kernels in parallel host threads), laid out [R][S][len(ks)] and
+    [S][len(ks)] as assert_w1_equal expects."""
+    sl = lambda x, k, w: np.ascontiguousarray(np.asarray(x).reshape(R, S, K, *w)[:, :, k:k + 1])  # noqa: E731
+
+    def one(k):
+        return oracle.w1(sl(ko["n_clusters"], k, ()), sl(ko["count"], k, (MAXC,)), sl(ko["p50_ns"], k, (MAXC,)),
+                         sl(ko["p99_ns"], k, (MAXC,)), R, S, 1)
+
+    with ThreadPoolExecutor(n_threads or P.host_threads()) as ex:
+        parts = list(ex.map(one, [int(k) for k in ks]))
+    out = {}
+    for f in ("n_present", "lo_ns", "hi_ns", "q1", "q3", "fence", "n_flag"):
+        out[f] = np.stack([np.asarray(p[f]).reshape(S) for p in parts], axis=1)  # [S][nk]
+    for f in ("score", "flag"):
+        out[f] = np.stack([np.asarray(p[f]).reshape(R, S) for p in parts], axis=2)  # [R][S][nk]
+    return out
+
+
+def _full_size(name, n_sample, n_heavy=10):
+    """GPU summarize -> kde -> w1 at full size; every KDE cell against the
+    oracle, W1 on n_sample kernels: the n_heavy heaviest ids and random
+    others."""
+    _announce(f"w1 full size {name}: GPU summarize -> kde -> w1, all KDE cells, {n_sample} W1 kernels")
     t = tracegen.make(name)
     c = t.cfg
     R, S, K, NS = c.n_ranks, c.n_steps, c.n_kernels, c.n_streams
@@ -215,21 +292,30 @@ def _full_size(name, n_sample):
     kd = pa.kde(ev, s, R, S, K, NS)
     gw = pa.w1(kd, R, S, K)
     torch.cuda.synchronize()
-    assert int(gw["dev_status"].item()) == 0
-    gw = {f: (v.cpu() if isinstance(v, torch.Tensor) else v) for f, v in gw.items() if f != "_workspace"}
+    assert int(kd["dev_status"].item()) == 0 and int(gw["dev_status"].item()) == 0
+    kd_h = {f: kd[f].cpu() for f in P.KDE_FIELDS}
+    ws = gw.pop("_workspace")
+    gw = {f: (v.cpu() if isinstance(v, torch.Tensor) else v) for f, v in gw.items()}
     del ev, s, kd
     gc.collect()
     torch.cuda.empty_cache()
     print(f"[gpu-case] {name}: GPU chain done, oracle KDE over {c.n_segments} segments", flush=True)
     ko = P.oracle_kde_segments(t, range(c.n_segments))
+    P.assert_kde_equal(kd_h, ko, f"{name} full-size KDE, every cell")
+    del kd_h
+    print(f"[gpu-case] {name}: all {c.n_segments * K} KDE cells agree", flush=True)
     rng = np.random.default_rng(5)
-    ks = np.sort(rng.choice(K, size=n_sample, replace=False))
-    sl = lambda x, w: np.ascontiguousarray(np.asarray(x).reshape(R, S, K, *w)[:, :, ks])  # noqa: E731
-    print(f"[gpu-case] {name}: oracle W1 on kernels {ks.tolist()}", flush=True)
-    ow = oracle.w1(sl(ko["n_clusters"], ()), sl(ko["count"], (MAXC,)), sl(ko["p50_ns"], (MAXC,)),
-                   sl(ko["p99_ns"], (MAXC,)), R, S, len(ks))
+    heavy = heaviest_ids(t, n_heavy)
+    rest = rng.choice(np.setdiff1d(np.arange(K), heavy), size=n_sample - len(heavy), replace=False)
+    ks = np.sort(np.concatenate([heavy, rest]))
+    print(f"[gpu-case] {name}: oracle W1 on kernels {ks.tolist()} (heaviest {sorted(heavy.tolist())})", flush=True)
+    ow = oracle_w1_kernels(ko, R, S, K, ks)
     n_amb = assert_w1_equal(gw, ow, R, S, K, f"{name} full", kernels=ks, max_ambiguous=2)
-    print(f"[gpu-case] {name}: sampled kernels agree ({n_amb} flags within rounding of the fence)", flush=True)
+    gw["_workspace"] = ws
+    n_q = check_cdf_values(gw, ko["n_clusters"], ko["count"], ko["p50_ns"], ko["p99_ns"], R, S, K, f"{name} full",
+                           n_points=20000, kernels=ks)
+    print(f"[gpu-case] {name}: sampled kernels agree ({n_amb} flags within rounding of the fence, "
+          f"{n_q} of 20000 CDF values one unit apart)", flush=True)
 
 
 @pytest.mark.timeout(900)
@@ -239,4 +325,9 @@ def test_w1_full_production():
 
 @pytest.mark.timeout(1100)
 def test_w1_full_cluster():
-    _full_size("cluster", 3)
+    _full_size("cluster", 64)
+
+
+@pytest.mark.timeout(1100)
+def test_w1_full_skew():
+    _full_size("skew", 64)
