@@ -46,6 +46,13 @@ constexpr uint32_t kBaseUnset = 0xFFu;
 constexpr uint32_t kStNone = 0, kStBusy = 0xFE, kStPoison = 0xFF;
 constexpr uint32_t kDone = 1u << 16;
 constexpr int kMapIds = 16384;  // ids per pass in mapped mode
+// Bound on the iterations of one claim wait, and on the passes over one key
+// range that may end with a wait cut short. A claim's owner publishes after
+// a fixed number of its own instructions, so no wait comes near the bound
+// unless the code around it is compiled wrongly; the bounds make the kernel
+// exit (and report) in that case instead of hanging.
+constexpr int kSpinCap = 1 << 16;
+constexpr int kMaxStuckPasses = 4;
 constexpr uint32_t kMapEmpty = 0xFFFF, kMapBusy = 0xFFFE, kMapDefer = 0xFFFD, kMapDone = 0xFFFC;
 
 // meta word of a slot: bits 0-7 window base bin (0xFF unset), bits 8-15
@@ -68,7 +75,7 @@ struct Smem {
   unsigned long long red_busy, red_wire;
   long long red_first, red_last;
   uint32_t red_valid, red_invalid;
-  uint32_t npool, poison, nslots;
+  uint32_t npool, poison, nslots, stuck;
 };
 
 struct Args {
@@ -119,7 +126,14 @@ struct Seg {
     uint32_t* w = &sm.map[lk >> 1];
     const int sh = (lk & 1) * 16;
     int res = -2;
-    while (true) {
+    // the trip count is the same for every lane (the loop exits on __any):
+    // the bound costs one scalar register
+    for (int it = 0;; ++it) {
+      if (res == -2 && it >= kSpinCap) {
+        // the wait is cut short: this event is dropped and the pass redone
+        lds_store(&sm.stuck, 1u);
+        res = -1;
+      }
       if (res == -2) {
         if (e < (uint32_t)NSLOT) {
           res = (int)e;
@@ -159,7 +173,11 @@ struct Seg {
   // one for the slot on first need (same exit discipline as map_claim).
   __device__ void pool_add(int slot, uint32_t m, int b) {
     bool pending = true;
-    while (true) {
+    for (int it = 0;; ++it) {
+      if (pending && it >= kSpinCap) {
+        lds_store(&sm.stuck, 1u);
+        pending = false;
+      }
       if (pending) {
         const uint32_t st = (m >> 8) & 0xFFu;
         if (st == kStPoison) {
@@ -180,7 +198,8 @@ struct Seg {
               fin = (m & ~0xFF00u) | (kStPoison << 8);
               lds_store(&sm.poison, 1u);
             }
-            atomicExch(&sm.meta[slot], fin);
+            // only the state field changes (it is ours while BUSY)
+            atomicXor(&sm.meta[slot], (fin ^ claim) & 0xFF00u);
             pending = false;
           } else {
             m = old;
@@ -338,6 +357,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
   unsigned long long busy = 0, wire = 0;
   long long tf = INT64_MAX, tl = INT64_MIN;
   bool first_scan = true;
+  int n_stuck = 0;  // passes of this segment that ended with a wait cut short
   constexpr int kRange = MAPPED ? kMapIds : NSLOT;
 
   for (int32_t kb = 0; kb < K; kb += kRange) {
@@ -355,6 +375,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         sm.npool = 0;
         sm.poison = 0;
         sm.nslots = 0;
+        sm.stuck = 0;
       }
       __syncthreads();
 
@@ -433,9 +454,20 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
       first_scan = false;
       __syncthreads();
 
+      // A claim wait cut short dropped an update: every kernel of this pass is
+      // redone (the per-segment aggregates were complete in the first scan).
+      // After kMaxStuckPasses such passes the results are flushed as they are
+      // and the condition is reported.
+      const bool stuck = sm.stuck != 0;
+      const bool redo_pass = stuck && n_stuck < kMaxStuckPasses;
+      if (stuck) {
+        if (!redo_pass && tid == 0 && a.dev_status) atomicOr(a.dev_status, (int32_t)ARGUS_DEV_SUMMARY_STALLED);
+        ++n_stuck;
+      }
+
       // flush: per-kernel scalars and wire size
       const int nslot = MAPPED ? (int)(sm.nslots < (uint32_t)NSLOT ? sm.nslots : NSLOT) : nk;
-      for (int s = tid; s < nslot; s += kThreads) {
+      for (int s = tid; s < (redo_pass ? 0 : nslot); s += kThreads) {
         const uint32_t m = sm.meta[s];
         const uint32_t pst = (m >> 8) & 0xFFu;
         if ((m & kDone) || pst == kStPoison) continue;
@@ -459,7 +491,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         if (cnt) wire += 33u + 5u * nnz;
       }
       // flush: histograms, four bins per thread, 16-byte stores
-      for (int it = tid; it < nslot * (NB / 4); it += kThreads) {
+      for (int it = tid; it < (redo_pass ? 0 : nslot) * (NB / 4); it += kThreads) {
         const int s = it >> 3, q = it & 7;
         const uint32_t m = sm.meta[s];
         const uint32_t pst = (m >> 8) & 0xFFu;
@@ -477,12 +509,12 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         *reinterpret_cast<uint4*>(a.hist + c * NB + 4 * q) = make_uint4(v[0], v[1], v[2], v[3]);
       }
       __syncthreads();
-      const bool again = sm.poison != 0;
+      const bool again = sm.poison != 0 || redo_pass;
       // mark what was written; kernels that ran out of room start over
       for (int s = tid; s < nslot; s += kThreads) {
         const uint32_t m = sm.meta[s];
         if (m & kDone) continue;
-        const bool redo = ((m >> 8) & 0xFFu) == kStPoison;
+        const bool redo = redo_pass || ((m >> 8) & 0xFFu) == kStPoison;
         if (MAPPED) {
           sg.map_set(sm.slot_kid[s], redo ? (uint16_t)kMapEmpty : (uint16_t)kMapDone);
         } else if (redo) {
