@@ -63,9 +63,46 @@ def measured_traffic(config: str):
     return traffic if sha == cur else None
 
 
+def host_record() -> dict:
+    """The host the CPU baselines ran on: usable cores, CPU model, RAM."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    ram = None
+    try:
+        for line in open("/proc/meminfo"):
+            if line.startswith("MemTotal:"):
+                ram = round(int(line.split()[1]) * 1024 / 2**30, 1)
+                break
+    except OSError:
+        pass
+    return {"nproc": len(os.sched_getaffinity(0)), "cpu_count": os.cpu_count(), "cpu_model": model,
+            "ram_gib": ram}
+
+
+class pinned_to_one_core:
+    """Pins the calling thread to one of its allowed cores for the duration
+    of a with-block (in-process; the oracle runs in the calling thread)."""
+
+    def __enter__(self):
+        self.old = os.sched_getaffinity(0)
+        self.core = max(self.old)
+        os.sched_setaffinity(0, {self.core})
+        return self
+
+    def __exit__(self, *exc):
+        os.sched_setaffinity(0, self.old)
+
+
 def cpu_baseline(trace, sample_ranks: int, gpu_sum: dict) -> dict:
-    """Oracle (single-threaded, as it stands) on the first sample_ranks ranks
-    of the same workload; also checks the GPU summaries of those ranks."""
+    """Oracle (single-threaded, as it stands, pinned to one core) on the
+    first sample_ranks ranks of the same workload; also checks the GPU
+    summaries of those ranks."""
     import oracle
     cfg = trace.cfg
     K, NS, S = cfg.n_kernels, cfg.n_streams, cfg.n_steps
@@ -79,9 +116,10 @@ def cpu_baseline(trace, sample_ranks: int, gpu_sum: dict) -> dict:
         g1 = min(g_end, g0 + chunk)
         ev = trace.fill_host(g0, g1, n_threads=os.cpu_count() or 1)
         n_ev += len(ev["kernel_id"])
-        t0 = time.perf_counter()
-        o = oracle.summarize(ev, K, NS)
-        t_oracle += time.perf_counter() - t0
+        with pinned_to_one_core() as pin:
+            t0 = time.perf_counter()
+            o = oracle.summarize(ev, K, NS)
+            t_oracle += time.perf_counter() - t0
         for f in ("count", "sum_ns", "min_ns", "max_ns", "hist"):
             ref = np.asarray(o[f]).reshape(-1)
             got = gpu_sum[f][g0 * K * (NB if f == "hist" else 1):g1 * K * (NB if f == "hist" else 1)]
@@ -93,14 +131,16 @@ def cpu_baseline(trace, sample_ranks: int, gpu_sum: dict) -> dict:
         sums.append(o["sum_ns"])
         steps.append(o["step_ns"])
     cnt, sm, st = np.concatenate(counts), np.concatenate(sums), np.concatenate(steps)
-    t0 = time.perf_counter()
-    oracle.cross_rank(cnt, sm, sample_ranks, S, K)
-    oracle.iter_windows(st, sample_ranks, S)
-    t_oracle += time.perf_counter() - t0
+    with pinned_to_one_core() as pin:
+        t0 = time.perf_counter()
+        oracle.cross_rank(cnt, sm, sample_ranks, S, K)
+        oracle.iter_windows(st, sample_ranks, S)
+        t_oracle += time.perf_counter() - t0
     return {"value": n_ev / t_oracle, "unit": "events/s", "cores": 1, "kind": "oracle",
             "sample": f"first {sample_ranks} ranks of the same workload ({n_ev} events): oracle summarize + "
-                      f"cross-rank + iter windows over the sample, single thread, generation excluded",
-            "seconds": round(t_oracle, 3), "_mismatches": mismatches}
+                      f"cross-rank + iter windows over the sample, single thread pinned to core {pin.core}, "
+                      f"generation excluded",
+            "seconds": round(t_oracle, 3), "host": host_record(), "_mismatches": mismatches}
 
 
 def cpu_baseline_sharded(trace, n_workers: int, seg_per_shard: int = 64) -> dict:
@@ -123,7 +163,20 @@ def cpu_baseline_sharded(trace, n_workers: int, seg_per_shard: int = 64) -> dict
     return {"value": n_ev / dt, "unit": "events/s", "cores": n, "kind": "oracle",
             "sample": f"{n} disjoint shards of {seg_per_shard} rank-steps ({n_ev} events) of the same workload, "
                       f"oracle summarize on each shard in its own thread at once, generation excluded",
-            "seconds": round(dt, 3)}
+            "seconds": round(dt, 3), "host": host_record()}
+
+
+def timed_calls(fn, reps: int, stream) -> list:
+    """Per-call times (ms) of reps back-to-back calls, from HIP events
+    recorded on the stream the calls launch on."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    ev[0].record(stream)
+    for i in range(reps):
+        fn()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    return [ev[i].elapsed_time(ev[i + 1]) for i in range(reps)]
 
 
 def main():
@@ -215,6 +268,7 @@ def main():
     present = int(np.count_nonzero(count_h))
     alg_bytes = algorithmic_summarize_bytes(trace.n_events, present, G, NS)
     sum_avg_ms = float(np.mean(sum_ms))
+    sum_med_ms = float(np.median(sum_ms))
     achieved = alg_bytes / (sum_avg_ms * 1e-3) / 1e9
     assert int(s["dev_status"].item()) == 0
 
@@ -236,10 +290,14 @@ def main():
         "dtype": "int64", "data": "synthetic (seeded counter-based generator, resident in HBM)",
         "config": {"workload": WORKLOADS[args.config], "n_ranks": R, "n_steps": S, "events": trace.n_events,
                    "n_kernels": K, "n_streams": NS, "input_bytes": 24 * trace.n_events},
+        "ms_per_step_median": float(np.median([a + b + c for a, b, c in zip(sum_ms, xr_ms, l1_ms)])),
         "summarize_ms": sum_avg_ms,
+        "summarize_ms_median": sum_med_ms,
         "summarize_events_per_s": trace.n_events / (sum_avg_ms * 1e-3),
         "hbm_frac_summarize": achieved / HBM_PEAK_GBS,
+        "hbm_frac_summarize_median": alg_bytes / (sum_med_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "cross_rank_ms_per_step": float(np.mean(xr_ms)) / S,
+        "cross_rank_ms_per_step_median": float(np.median(xr_ms)) / S,
         "iter_windows_ms": float(np.mean(l1_ms)),
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config),
@@ -333,20 +391,24 @@ def main():
         for _ in range(2):
             pa.kde(ev, s, R, S, K, NS, out=kde_out)
         torch.cuda.synchronize()
-        e0.record(stream)
-        for _ in range(args.kde_reps):
-            pa.kde(ev, s, R, S, K, NS, out=kde_out)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        kde_ms = e0.elapsed_time(e1) / args.kde_reps
+        kde_calls = timed_calls(lambda: pa.kde(ev, s, R, S, K, NS, out=kde_out), args.kde_reps, stream)
+        kde_ms = float(np.mean(kde_calls))
         assert int(kde_out["dev_status"].item()) == 0
         ncl = kde_out["n_clusters"].cpu().numpy()
         n_valid = int(s["n_valid"].cpu().numpy().view(np.uint32).astype(np.int64).sum())
         # summary record per present cell: kernel id 4 B + cluster count 1 B,
         # then (count 4, p50 8, p99 8) per cluster
         wire = int(5 * np.count_nonzero(ncl) + 20 * ncl.astype(np.int64).sum())
+        # algorithmic bytes: every event read once (24 B), each cell's count /
+        # min / max read (20 B) and its record written (n_clusters 1, count 16,
+        # p50 32, p99 32, bw 4 = 85 B); the bucketed durations the kernels
+        # write and re-read are the design's, not the operation's
+        kde_alg = 24 * trace.n_events + (20 + 85) * G * K
         result["kde"] = {
-            "ms": kde_ms, "events_per_s": trace.n_events / (kde_ms * 1e-3),
+            "ms": kde_ms, "ms_median": float(np.median(kde_calls)), "events_per_s": trace.n_events / (kde_ms * 1e-3),
+            "roofline": {"bound": "hbm", "achieved": kde_alg / (kde_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": kde_alg / (kde_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                         "algorithmic_bytes_per_call": kde_alg},
             "scatter_algorithmic_bytes": 24 * trace.n_events + 8 * n_valid + 8 * G * K,
             "cells": G * K, "present_cells": int(np.count_nonzero(ncl)),
             "mean_clusters_per_present_cell": float(ncl[ncl > 0].mean()) if (ncl > 0).any() else 0.0,
@@ -360,19 +422,22 @@ def main():
             w1_out = pa.alloc_w1(R, S, K, 64, dev)
             pa.w1(kde_out, R, S, K, out=w1_out)
             torch.cuda.synchronize()
-            e0.record(stream)
-            for _ in range(args.w1_reps):
-                pa.w1(kde_out, R, S, K, out=w1_out)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            w1_ms = e0.elapsed_time(e1) / args.w1_reps
+            w1_calls = timed_calls(lambda: pa.w1(kde_out, R, S, K, out=w1_out), args.w1_reps, stream)
+            w1_ms = float(np.mean(w1_calls))
             assert int(w1_out["dev_status"].item()) == 0
             wf = w1_out["flag"].cpu().numpy().reshape(R, S, K).astype(bool)
             pres = ncl.reshape(R, S, K) > 0
             strag = sorted(truth["stragglers"])
             others = np.setdiff1d(np.arange(R), strag)
+            # algorithmic bytes: each cell's cluster record read (81 B) and its
+            # score and flag written (9 B); per (step, kernel) 64 B of
+            # statistics. The 16-bit CDF table in the workspace is the design's.
+            w1_alg = 90 * G * K + 64 * S * K
             result["w1"] = {
-                "ms": w1_ms, "ms_per_step": w1_ms / S, "grid": 64,
+                "ms": w1_ms, "ms_median": float(np.median(w1_calls)), "ms_per_step": w1_ms / S, "grid": 64,
+                "roofline": {"bound": "hbm", "achieved": w1_alg / (w1_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                             "unit": "GB/s", "frac": w1_alg / (w1_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                             "algorithmic_bytes_per_call": w1_alg},
                 "kernel_steps": S * K, "present_cells": int(pres.sum()),
                 "straggler_cells_flagged_frac": float(wf[strag].sum() / max(1, pres[strag].sum())),
                 "other_cells_flagged_frac": float(wf[others].sum() / max(1, pres[others].sum())),
