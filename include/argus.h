@@ -43,7 +43,9 @@
  *     step times) are OR-ed as ARGUS_DEV_* bits into the optional device
  *     word *dev_status, which the call first resets to 0.
  *   - The library writes every element of every non-NULL output, including
- *     identity values for empty cells, so outputs need no pre-clearing.
+ *     identity values for empty cells, so outputs need no pre-clearing. The
+ *     one exception is argus_summarize (and _keyed): for an absent cell
+ *     (count 0) only the count is written, see there.
  *   - Calls keep no mutable global state and are safe from several host
  *     threads on different streams.
  *   - Integer outputs are exact and deterministic; float outputs are
@@ -120,6 +122,14 @@ const char* argus_status_string(int status);
  * A segment is malformed unless 0 <= seg_off[g] <= seg_off[g+1] <= n_events
  * and its length is below 2^32; a malformed segment is summarized as empty
  * and ARGUS_DEV_BAD_SEGMENT is raised. Sums wrap modulo 2^64.
+ *
+ * Written cells: count is written for every cell. sum_ns, min_ns, max_ns and
+ * hist are written only for present cells (count >= 1); for an absent cell
+ * they keep whatever the buffers held (a caller that wants the identity
+ * values 0 / INT64_MAX / INT64_MIN / 0 fills them beforehand). Large, sparse
+ * key spaces (most kernel ids absent from a rank-step) thus cost 4 bytes per
+ * absent cell instead of 156. Every consumer in this library (cross-rank, L2,
+ * KDE, compaction) reads a cell's other fields only when its count is >= 1.
  */
 typedef struct argus_events {
   const int32_t* kernel_id; /* [n_events] */
@@ -133,11 +143,11 @@ typedef struct argus_events {
 
 typedef struct argus_summary {
   /* per cell, [n_ranks][n_steps][n_kernels] (hist: [..][ARGUS_NBINS]) */
-  uint32_t* count;  /* valid events of the kernel */
-  int64_t* sum_ns;  /* sum of d */
-  int64_t* min_ns;  /* min d, INT64_MAX when count == 0 */
-  int64_t* max_ns;  /* max d, INT64_MIN when count == 0 */
-  uint32_t* hist;   /* octave histogram of d */
+  uint32_t* count;  /* valid events of the kernel (every cell) */
+  int64_t* sum_ns;  /* sum of d (present cells only) */
+  int64_t* min_ns;  /* min d (present cells only) */
+  int64_t* max_ns;  /* max d (present cells only) */
+  uint32_t* hist;   /* octave histogram of d (present cells only) */
   /* per segment, [n_ranks][n_steps] */
   uint32_t* n_valid;
   uint32_t* n_invalid;

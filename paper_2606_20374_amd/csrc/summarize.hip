@@ -28,8 +28,9 @@
 // * Per-segment aggregates (valid/invalid counts, first start, last end,
 //   busy time) are kept in registers and reduced once per segment; per-stream
 //   busy time uses LDS atomics.
-// * The flush writes every output element exactly once (identity values for
-//   absent kernels), coalesced, so outputs need no clearing.
+// * The flush writes each present cell once and the count of every cell
+//   (0 for absent kernels); an absent cell's other fields are not written,
+//   so a large, sparse key space costs 4 bytes per absent cell.
 #include <atomic>
 
 #include "argus_internal.h"
@@ -465,7 +466,8 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         ++n_stuck;
       }
 
-      // flush: per-kernel scalars and wire size
+      // flush: the count of every slot; sum, min, max and wire size of the
+      // present ones
       const int nslot = MAPPED ? (int)(sm.nslots < (uint32_t)NSLOT ? sm.nslots : NSLOT) : nk;
       for (int s = tid; s < (redo_pass ? 0 : nslot); s += kThreads) {
         const uint32_t m = sm.meta[s];
@@ -485,24 +487,27 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         }
         const int64_t c = g * K + kb + (MAPPED ? (int)sm.slot_kid[s] : s);
         a.count[c] = cnt;
-        a.sum_ns[c] = (int64_t)sm.sum[s];
-        a.min_ns[c] = sm.mm[s][0];
-        a.max_ns[c] = sm.mm[s][1];
-        if (cnt) wire += 33u + 5u * nnz;
+        if (cnt) {
+          a.sum_ns[c] = (int64_t)sm.sum[s];
+          a.min_ns[c] = sm.mm[s][0];
+          a.max_ns[c] = sm.mm[s][1];
+          wire += 33u + 5u * nnz;
+        }
       }
-      // flush: histograms, four bins per thread, 16-byte stores
+      // flush: histograms of the present slots (their window base is set),
+      // four bins per thread, 16-byte stores
       for (int it = tid; it < (redo_pass ? 0 : nslot) * (NB / 4); it += kThreads) {
         const int s = it >> 3, q = it & 7;
         const uint32_t m = sm.meta[s];
         const uint32_t pst = (m >> 8) & 0xFFu;
-        if ((m & kDone) || pst == kStPoison) continue;
         const int base = (int)(m & 0xFFu);
+        if ((m & kDone) || pst == kStPoison || base == (int)kBaseUnset) continue;
         uint32_t v[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int b = 4 * q + j;
           const int off = b - base;
-          v[j] = (base != (int)kBaseUnset && (unsigned)off < (unsigned)WIN) ? sm.win[s][off] : 0u;
+          v[j] = (unsigned)off < (unsigned)WIN ? sm.win[s][off] : 0u;
           if (pst != kStNone) v[j] += sm.pool[pst - 1][b];
         }
         const int64_t c = g * K + kb + (MAPPED ? (int)sm.slot_kid[s] : s);
@@ -529,8 +534,13 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
       __syncthreads();
       if (!again) break;
     }
-    // (mapped mode: ids of this range that never occurred keep the identity
-    // values written by identity_fill_kernel before this launch)
+    if (MAPPED) {
+      // keys of this range that never occurred: count 0 (their other fields
+      // are not written)
+      for (int i = tid; i < nk; i += kThreads)
+        if (sg.map_get(i) == kMapEmpty) a.count[g * K + kb + i] = 0;
+      __syncthreads();
+    }
   }
 
   // per-segment aggregates
@@ -591,25 +601,6 @@ hipError_t launch_t(const Args& args, int32_t n_seg, hipStream_t st) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Identity values of every cell (count 0, sum 0, min INT64_MAX, max
-// INT64_MIN, empty histogram), streamed with 16-byte stores. Used before the
-// mapped-mode kernel, which then writes only the cells of ids that occur:
-// for large, sparse id spaces most cells are absent, and one streaming pass
-// writes them far faster than per-segment bursts at the end of each scan.
-__global__ __launch_bounds__(256) void identity_fill_kernel(uint32_t* count, int64_t* sum, int64_t* mn, int64_t* mx,
-                                                            uint32_t* hist, int64_t cells) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  uint4* h4 = reinterpret_cast<uint4*>(hist);
-  for (int64_t i = t0; i < cells * (NB / 4); i += stride) h4[i] = make_uint4(0u, 0u, 0u, 0u);
-  for (int64_t c = t0; c < cells; c += stride) {
-    count[c] = 0;
-    sum[c] = 0;
-    mn[c] = INT64_MAX;
-    mx[c] = INT64_MIN;
-  }
-}
-
 }  // namespace
 
 hipError_t launch_summarize(const SummarizeLaunch& l, hipStream_t st) {
@@ -623,11 +614,6 @@ hipError_t launch_summarize(const SummarizeLaunch& l, hipStream_t st) {
   if (n_keys <= 64) return launch_t<64, 10, false>(a, l.n_seg, st);
   if (n_keys <= 512) return launch_t<512, 10, false>(a, l.n_seg, st);
   if (n_keys <= 2048) return launch_t<2048, 10, false>(a, l.n_seg, st);
-  const int64_t cells = (int64_t)l.n_seg * n_keys;
-  hipLaunchKernelGGL(identity_fill_kernel, dim3(4096), dim3(256), 0, st, l.count, l.sum_ns, l.min_ns, l.max_ns, l.hist,
-                     cells);
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
   return launch_t<2048, 6, true>(a, l.n_seg, st);
 }
 

@@ -222,9 +222,16 @@ def test_determinism():
     a = pa.run_step(ev, cfg.n_ranks, cfg.n_steps, cfg.n_kernels, cfg.n_streams)
     b = pa.run_step(ev, cfg.n_ranks, cfg.n_steps, cfg.n_kernels, cfg.n_streams)
     torch.cuda.synchronize()
+    pres = a[0]["count"] != 0
     for da, db in zip(a, b):
         for k in da:
-            if not k.startswith("_"):
+            if k.startswith("_"):
+                continue
+            if da is a[0] and k in P.PRESENT_ONLY:  # written for present cells only
+                per = da[k].numel() // pres.numel()
+                keep = pres.repeat_interleave(per)
+                assert torch.equal(da[k][keep], db[k][keep]), k
+            else:
                 assert torch.equal(da[k], db[k]), k
 
 
@@ -327,3 +334,32 @@ def test_l1_golden_and_random():
                 g = {k: v[:max(R, 0)] if k != "flags" else v[:0] for k, v in g.items()}
             P.assert_int_equal(g, o, P.L1_INT_FIELDS, f"l1 {R}x{S}")
             P.assert_float_close(g, o, ["cp_ratio"], f"l1 {R}x{S}")
+
+
+@pytest.mark.parametrize("K,keyed", [(64, False), (2048, False), (6000, False), (40_000, False), (300, True)])
+def test_absent_cells_keep_their_buffers(K, keyed):
+    """Only the count of an absent cell is written: its sum, min, max and
+    histogram keep what the caller's buffers held (a sentinel here), while
+    every present cell matches the oracle. Dense (K <= 2048), mapped
+    (larger K, one and several id ranges) and (kernel, stream) keys; half of
+    the ids never occur."""
+    _announce(f"absent cells untouched: K={K} keyed={keyed}")
+    NS = 4
+    ev = _random_events(40_000, K // 2, NS, seed=31 + K, seg_lengths=[25_000, 0, 15_000])
+    ev["stream"] = np.random.default_rng(K).integers(0, NS, size=40_000).astype(np.int32)
+    cells = 3 * K * (NS if keyed else 1)
+    out = pa.argus.alloc_summary(3, 1, K * (NS if keyed else 1), NS, DEV)
+    sentinel = {"sum_ns": 0x5A5A5A5A5A5A5A5A, "min_ns": 0x1234567812345678, "max_ns": -0x0F0F0F0F0F0F0F0F,
+                "hist": 0x3C3C3C3C}
+    for f, v in sentinel.items():
+        out[f].fill_(v)
+    g = pa.summarize(_dev_events(ev), 3, 1, K, NS, out=out, keyed=keyed)
+    torch.cuda.synchronize()
+    o = oracle.summarize(ev, K, NS, keyed=keyed)
+    P.assert_int_equal(g, o, P.SUM_INT_FIELDS, f"absent K={K} keyed={keyed}")
+    absent = np.asarray(o["count"]).reshape(-1) == 0
+    assert absent.sum() >= cells // 3, "the case needs absent cells"
+    for f, v in sentinel.items():
+        per = P.NB if f == "hist" else 1
+        got = P.to_np(g[f]).reshape(cells, per)[absent]
+        assert (got == v).all(), (f, "an absent cell's field was written")
