@@ -76,6 +76,7 @@ extern "C" {
 #define ARGUS_MAX_W1_STEPS 65535 /* argus_w1: n_steps limit */
 #define ARGUS_MAX_L2_RANKS 65536 /* argus_l2: n_ranks limit */
 #define ARGUS_MAX_L2_DIMS 16     /* argus_l2: parallelism dimensions limit */
+#define ARGUS_NOALLOC_SCRATCH_BYTES 256 /* argus_summarize_noalloc: static scratch per device */
 
 enum {
   ARGUS_OK = 0,
@@ -170,6 +171,20 @@ size_t argus_summarize_workspace(const argus_events_t* ev);
  * must be 16-byte aligned. workspace: see argus_summarize_workspace. */
 int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* workspace, size_t workspace_bytes,
                     void* stream);
+
+/* For callers that cannot allocate device memory or pass a workspace (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): argus_summarize with its scratch, the work-queue counter of
+ * its persistent workgroups, in a static device array of
+ * ARGUS_NOALLOC_SCRATCH_BYTES that the library holds on each device it runs
+ * on until the process ends. Arguments, outputs and status codes are those
+ * of argus_summarize; the call allocates nothing and frees nothing. It
+ * returns ARGUS_EINVAL when the call would need more scratch than the array
+ * holds (argus_summarize_workspace(ev) > ARGUS_NOALLOC_SCRATCH_BYTES). Every
+ * call on a device shares that device's array and resets it on its stream
+ * before use: calls that may overlap on one device (other streams, other
+ * host threads) race and must not be issued. */
+int argus_summarize_noalloc(const argus_events_t* ev, const argus_summary_t* out, void* stream);
 
 /* As argus_summarize, but cells are keyed by (kernel id, stream), the
  * grouping key of section 5.2: cells are [n_ranks][n_steps][n_kernels]

@@ -8,10 +8,10 @@ The Python layer only marshals arguments; see argus.py.
 """
 from .argus import (ArgusError, alloc_cross_rank, alloc_iter_windows, alloc_kde, alloc_l2, alloc_summary, alloc_w1,
                     compact, cross_rank, iter_windows, kde, kde_defaults, kde_workspace_bytes, l1_defaults, l2, l2_defaults,
-                    lib, summarize, w1, w1_defaults, xr_defaults)
+                    lib, summarize, summarize_noalloc, w1, w1_defaults, xr_defaults)
 
 __all__ = ["ArgusError", "alloc_cross_rank", "alloc_iter_windows", "alloc_kde", "alloc_summary", "cross_rank",
-           "iter_windows", "kde", "kde_defaults", "kde_workspace_bytes", "l1_defaults", "lib", "summarize",
+           "iter_windows", "kde", "kde_defaults", "kde_workspace_bytes", "l1_defaults", "lib", "summarize", "summarize_noalloc",
            "xr_defaults", "alloc_w1", "w1", "w1_defaults", "alloc_l2", "l2", "l2_defaults", "compact", "run_step"]
 
 

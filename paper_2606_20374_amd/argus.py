@@ -24,6 +24,7 @@ DEV_GROUPS_MALFORMED, DEV_GROUPS_DUPLICATE, DEV_L2_DOMAIN, DEV_COMPACT_CAPACITY 
 DEV_SUMMARY_STALLED = 256
 KDE_MAXC = 4
 MAX_W1_STEPS = 65535
+NOALLOC_SCRATCH_BYTES = 256
 
 V, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
 
@@ -118,6 +119,8 @@ def lib():
         L.argus_summarize.argtypes = [P(Events), P(Summary), V, ctypes.c_size_t, V]
         L.argus_summarize.restype = ctypes.c_int
         L.argus_summarize_keyed.argtypes = [P(Events), P(Summary), V, ctypes.c_size_t, V]
+        L.argus_summarize_noalloc.argtypes = [P(Events), P(Summary), V]
+        L.argus_summarize_noalloc.restype = ctypes.c_int
         L.argus_summarize_keyed.restype = ctypes.c_int
         L.argus_compact_workspace.argtypes = [I32, I32]
         L.argus_compact_workspace.restype = ctypes.c_size_t
@@ -234,6 +237,19 @@ def summarize(ev: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: i
     assert ws.numel() >= lib().argus_summarize_workspace(ctypes.byref(e))
     fn = lib().argus_summarize_keyed if keyed else lib().argus_summarize
     _check(fn(ctypes.byref(e), ctypes.byref(s), _ptr(ws), ws.numel(), _stream(dev)), "argus_summarize")
+    return out
+
+
+def summarize_noalloc(ev: dict, n_ranks: int, n_steps: int, n_kernels: int, n_streams: int,
+                      out: Optional[dict] = None) -> dict:
+    """argus_summarize_noalloc: argus_summarize with its scratch in the
+    library's static per-device array (no workspace argument)."""
+    dev = ev["kernel_id"].device
+    if out is None:
+        out = alloc_summary(n_ranks, n_steps, n_kernels, n_streams, dev)
+    e = _events(ev, n_ranks, n_steps, n_kernels, n_streams)
+    s = Summary(*[_ptr(out.get(f)) for f in SUMMARY_FIELDS])
+    _check(lib().argus_summarize_noalloc(ctypes.byref(e), ctypes.byref(s), _stream(dev)), "argus_summarize_noalloc")
     return out
 
 

@@ -32,6 +32,30 @@ int check_device() {
 
 int status_of(hipError_t e) { return e == hipSuccess ? ARGUS_OK : ARGUS_EHIP; }
 
+// Scratch of argus_summarize_noalloc: the work-queue counter of the
+// persistent summarize kernel, in device memory that the library never
+// allocates. Each device holds its own copy until the process ends; in host
+// code this name is only a handle, so kernels get the address that
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) uint8_t scratch[ARGUS_NOALLOC_SCRATCH_BYTES];
+
+// Device address of `scratch` per device, looked up on the first call on
+// that device (with it current).
+std::atomic<void*> g_scratch_ptr[64];
+
+int scratch_of_current_device(void** ptr) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ARGUS_EHIP;
+  if (dev < 0 || dev >= 64) return ARGUS_EUNSUPPORTED;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return ARGUS_EHIP;
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *ptr = p;
+  return ARGUS_OK;
+}
+
 }  // namespace
 
 hipError_t launch_clear(int32_t* dev_status, uint32_t* queue, hipStream_t st) {
@@ -102,6 +126,18 @@ int argus_summarize(const argus_events_t* ev, const argus_summary_t* out, void* 
 int argus_summarize_keyed(const argus_events_t* ev, const argus_summary_t* out, void* workspace,
                           size_t workspace_bytes, void* stream) {
   return summarize_impl(ev, out, workspace, workspace_bytes, stream, true);
+}
+
+int argus_summarize_noalloc(const argus_events_t* ev, const argus_summary_t* out, void* stream) {
+  if (!ev || !out) return ARGUS_EINVAL;
+  const size_t need = argus_summarize_workspace(ev);
+  if (need > ARGUS_NOALLOC_SCRATCH_BYTES) return ARGUS_EINVAL;  // scratch too small for this call
+  int rc = check_device();
+  if (rc != ARGUS_OK) return rc;
+  void* ws = nullptr;
+  rc = scratch_of_current_device(&ws);
+  if (rc != ARGUS_OK) return rc;
+  return summarize_impl(ev, out, ws, ARGUS_NOALLOC_SCRATCH_BYTES, stream, false);
 }
 
 void argus_xr_default(argus_xr_params_t* p) {

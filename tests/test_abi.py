@@ -212,3 +212,13 @@ def test_summarize_keyed_rejects_large_key_space():
     e = A.Events(0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 10, 2, 2, 4097, 16)  # 4097 x 16 > 65536 keys
     s = A.Summary(*([0x1000] * 12 + [None, None]))
     assert pa.lib().argus_summarize_keyed(ctypes.byref(e), ctypes.byref(s), 0x2000, 256, None) == A.EINVAL
+
+
+def test_summarize_noalloc_rejects_null_arguments():
+    L = pa.lib()
+    e = A.Events()
+    s = A.Summary()
+    assert L.argus_summarize_noalloc(None, ctypes.byref(s), None) == A.EINVAL
+    assert L.argus_summarize_noalloc(ctypes.byref(e), None, None) == A.EINVAL
+    # its scratch covers what argus_summarize asks for
+    assert L.argus_summarize_workspace(ctypes.byref(e)) <= A.NOALLOC_SCRATCH_BYTES
