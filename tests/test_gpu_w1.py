@@ -273,9 +273,9 @@ def oracle_w1_kernels(ko, R, S, K, ks, n_threads=None):
         parts = list(ex.map(one, [int(k) for k in ks]))
     out = {}
     for f in ("n_present", "lo_ns", "hi_ns", "q1", "q3", "fence", "n_flag"):
-        out[f] = np.stack([np.asarray(p[f]).reshape(S) for p in parts], axis=1)  # [S][nk]
+        out[f] = np.stack([np.asarray(p[f]).reshape(S) for p in parts], axis=1).reshape(-1)  # [S][nk]
     for f in ("score", "flag"):
-        out[f] = np.stack([np.asarray(p[f]).reshape(R, S) for p in parts], axis=2)  # [R][S][nk]
+        out[f] = np.stack([np.asarray(p[f]).reshape(R, S) for p in parts], axis=2).reshape(-1)  # [R][S][nk]
     return out
 
 
