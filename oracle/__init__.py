@@ -54,6 +54,14 @@ def lib():
         L.orc_kde_bin.argtypes = [ctypes.c_uint64, I32]
         L.orc_kde_bin.restype = ctypes.c_int
         L.orc_kde_group.argtypes = [I64, V] + [I32] * 4 + [V] * 8
+        L.orc_kde_weights.argtypes = [I64, I32, V]
+        L.orc_kde_pow_m02.argtypes = [I64]
+        L.orc_kde_pow_m02.restype = ctypes.c_double
+        L.orc_kde_bw_q8.argtypes = [ctypes.c_double, I64]
+        L.orc_kde_bw_q8.restype = I64
+        L.orc_kde_weights_many.argtypes = [V, V, I32, V]
+        L.orc_kde_pow_m02_many.argtypes = [V, I64, V]
+        L.orc_kde_bw_q8_many.argtypes = [V, V, I64, V]
         L.orc_kde.argtypes = [I64, I32, I32, I64] + [V] * 5 + [I32] * 4 + [V] * 5
         L.orc_kde.restype = I64
         L.orc_w1.argtypes = [I32, I32, I32] + [V] * 4 + [I32] * 3 + [V] * 9
@@ -204,6 +212,48 @@ def kde_group(durations, debug: bool = False, **params) -> dict:
         G = kde_bin(int(d.max()), p["sub_bits"]) - kde_bin(int(d.min()), p["sub_bits"]) + 1
         out["f"] = f[:G]
         out["cand"] = cand[:out["n_cand"]]
+    return out
+
+
+def kde_weights(H: int, nt: int) -> np.ndarray:
+    """The integer weights w(0 .. nt-1) of bandwidth H (1/256 grid steps)."""
+    w = np.empty(nt, np.uint32)
+    lib().orc_kde_weights(H, nt, _p(w))
+    return w
+
+
+def kde_pow_m02(n: int) -> float:
+    """n^-0.2 as the oracle's bandwidth takes it."""
+    return lib().orc_kde_pow_m02(n)
+
+
+def kde_bw_q8(var: float, n: int) -> int:
+    """The quantised bandwidth H of a group of n grid values of variance var."""
+    return lib().orc_kde_bw_q8(var, n)
+
+
+def kde_weights_many(H: np.ndarray, off: np.ndarray) -> np.ndarray:
+    """Weights of t = 0 .. off[i+1]-off[i]-1 for every bandwidth H[i], laid
+    out at w[off[i]:off[i+1]]."""
+    H = np.ascontiguousarray(H, dtype=np.int64)
+    off = np.ascontiguousarray(off, dtype=np.int64)
+    w = np.empty(int(off[-1]), np.uint32)
+    lib().orc_kde_weights_many(_p(H), _p(off), len(H), _p(w))
+    return w
+
+
+def kde_pow_m02_many(n: np.ndarray) -> np.ndarray:
+    n = np.ascontiguousarray(n, dtype=np.int64)
+    out = np.empty(n.size, np.float64)
+    lib().orc_kde_pow_m02_many(_p(n), n.size, _p(out))
+    return out
+
+
+def kde_bw_q8_many(var: np.ndarray, n: np.ndarray) -> np.ndarray:
+    var = np.ascontiguousarray(var, dtype=np.float64)
+    n = np.ascontiguousarray(n, dtype=np.int64)
+    out = np.empty(n.size, np.int64)
+    lib().orc_kde_bw_q8_many(_p(var), _p(n), n.size, _p(out))
     return out
 
 

@@ -24,6 +24,10 @@
  *  - sigma: sample standard deviation (n - 1) of the grid values x;
  *    h = (1.06 sqrt(var)) n^(-1/5) in grid steps, quantised to
  *    H = floor(256 h + 0.5) (units of 1/256 step); H = 0 means no valleys;
+ *    n^(-1/5) is the double nearest to the real fifth root, decided by exact
+ *    integer comparisons (a math library's pow(n, -0.2) takes the exponent
+ *    as the double nearest -0.2 and rounds differently from one library to
+ *    the next);
  *  - binned KDE with integer weights w(t) = floor(65536 exp(-t^2 / (2 (H/256)^2)) + 0.5)
  *    for grid distance t; f(j) = sum_b c(b) w(|j - b|) over the histogram c
  *    (the 1/(n h sqrt(2 pi)) factor does not move minima);
@@ -97,6 +101,116 @@ static int cmp_u64(const void* a, const void* b) {
   return x < y ? -1 : x > y;
 }
 
+/* ---- n^(-1/5), the double nearest to the real value ----------------------
+ * Whether the fifth root z = n^(-1/5) lies above or below a dyadic number
+ * m = c 2^k (c odd) is decided exactly: z < m iff c^5 n > 2^(-5k). The product
+ * is formed in 32-bit limbs (c < 2^55, n < 2^33: under 320 bits). */
+#define MP_LIMBS 12
+
+/* a *= m (a: MP_LIMBS little-endian 32-bit limbs) */
+static void mp_mul_u32(uint32_t* a, uint32_t m) {
+  uint64_t carry = 0;
+  for (int i = 0; i < MP_LIMBS; i++) {
+    uint64_t v = (uint64_t)a[i] * m + carry;
+    a[i] = (uint32_t)v;
+    carry = v >> 32;
+  }
+}
+
+/* a *= m for a 64-bit m: a * lo + (a * hi) << 32 */
+static void mp_mul_u64(uint32_t* a, uint64_t m) {
+  uint32_t lo[MP_LIMBS], hi[MP_LIMBS];
+  memcpy(lo, a, sizeof(lo));
+  memcpy(hi, a, sizeof(hi));
+  mp_mul_u32(lo, (uint32_t)m);
+  mp_mul_u32(hi, (uint32_t)(m >> 32));
+  uint64_t carry = 0;
+  for (int i = 0; i < MP_LIMBS; i++) {
+    uint64_t v = (uint64_t)lo[i] + (i > 0 ? hi[i - 1] : 0) + carry;
+    a[i] = (uint32_t)v;
+    carry = v >> 32;
+  }
+}
+
+/* sign of c^5 n - 2^e: 1, 0 or -1 (c, n >= 1, 0 <= e < 32 MP_LIMBS) */
+static int fifth_cmp(uint64_t c, uint64_t n, int e) {
+  uint32_t a[MP_LIMBS] = {0};
+  a[0] = 1;
+  for (int r = 0; r < 5; r++) mp_mul_u64(a, c);
+  mp_mul_u64(a, n);
+  int top = MP_LIMBS - 1;
+  while (top > 0 && a[top] == 0) top--;
+  int bits = 32 * top + (a[top] ? 32 - __builtin_clz(a[top]) : 0);
+  if (bits != e + 1) return bits > e + 1 ? 1 : -1; /* 2^e has e + 1 bits */
+  for (int i = 0; i < MP_LIMBS; i++) {             /* same length: equal iff only the top bit is set */
+    uint32_t want = i == e / 32 ? (1u << (e % 32)) : 0u;
+    if (a[i] != want) return 1;
+  }
+  return 0;
+}
+
+/* The double nearest to n^(-1/5) for 1 <= n < 2^33. y = M 2^q with M in
+ * [2^52, 2^53); its rounding interval is bounded by the midpoints to its
+ * neighbours, (2M + 1) 2^(q-1) above and (2M - 1) 2^(q-1) below, or
+ * (4M - 1) 2^(q-2) below when M = 2^52 (the neighbour below lies in the next
+ * lower binade). z is irrational or a reciprocal integer, never a midpoint. */
+static double kde_pw(int64_t n) {
+  double y = pow((double)n, -0.2); /* a start within a few units in the last place */
+  for (;;) {
+    int q;
+    double f = frexp(y, &q); /* y = f 2^q, f in [0.5, 1) */
+    uint64_t M = (uint64_t)ldexp(f, 53);
+    q -= 53;
+    /* z < upper midpoint: (2M + 1)^5 n > 2^(5 (1 - q)) */
+    if (fifth_cmp(2 * M + 1, (uint64_t)n, 5 * (1 - q)) <= 0) {
+      y = nextafter(y, INFINITY);
+      continue;
+    }
+    /* z > lower midpoint: (2M - 1)^5 n < 2^(5 (1 - q)), or (4M - 1)^5 n < 2^(5 (2 - q)) */
+    int below = M == (1ull << 52) ? fifth_cmp(4 * M - 1, (uint64_t)n, 5 * (2 - q))
+                                  : fifth_cmp(2 * M - 1, (uint64_t)n, 5 * (1 - q));
+    if (below >= 0) {
+      y = nextafter(y, 0.0);
+      continue;
+    }
+    return y;
+  }
+}
+
+/* Step 2's bandwidth: H = floor(256 h + 0.5) with h = 1.06 sqrt(var) n^(-1/5)
+ * in grid steps, n^(-1/5) the double nearest to the real value. */
+static int64_t kde_bw_q8(double var, int64_t n) {
+  double h = 1.06 * sqrt(var) * kde_pw(n);
+  return (int64_t)floor(h * 256.0 + 0.5);
+}
+
+/* Step 3's integer Gaussian weight of grid distance t for bandwidth H. */
+static uint32_t kde_weight(int64_t t, int64_t H) {
+  double a = (double)(32768LL * t * t) / (double)(H * H);
+  return (uint32_t)floor(65536.0 * exp(-a) + 0.5);
+}
+
+/* Test access to the floating-point steps: the weights of t = 0 .. nt-1 for
+ * bandwidth H, n^-0.2, and H from (var, n). */
+void orc_kde_weights(int64_t H, int32_t nt, uint32_t* w) {
+  for (int32_t t = 0; t < nt; t++) w[t] = kde_weight(t, H);
+}
+double orc_kde_pow_m02(int64_t n) { return kde_pw(n); }
+int64_t orc_kde_bw_q8(double var, int64_t n) { return kde_bw_q8(var, n); }
+
+/* The same over arrays: weights of t = 0 .. off[i+1]-off[i]-1 for each H[i]
+ * into w[off[i] ..]; n^-0.2 and H of (var[i], n[i]). */
+void orc_kde_weights_many(const int64_t* H, const int64_t* off, int32_t nH, uint32_t* w) {
+  for (int32_t i = 0; i < nH; i++)
+    for (int64_t t = 0; t < off[i + 1] - off[i]; t++) w[off[i] + t] = kde_weight(t, H[i]);
+}
+void orc_kde_pow_m02_many(const int64_t* n, int64_t m, double* out) {
+  for (int64_t i = 0; i < m; i++) out[i] = kde_pw(n[i]);
+}
+void orc_kde_bw_q8_many(const double* var, const int64_t* n, int64_t m, int64_t* out) {
+  for (int64_t i = 0; i < m; i++) out[i] = kde_bw_q8(var[i], n[i]);
+}
+
 /* Remove valley i from the position / value lists of length *m. */
 static void drop(int32_t* pos, uint64_t* val, int32_t* m, int32_t i) {
   for (int32_t q = i; q + 1 < *m; q++) {
@@ -143,8 +257,7 @@ static void kde_group(int64_t n, const uint64_t* d, int32_t s, int32_t frac_pm, 
   if (n >= 2) {
     u128 V = (u128)n * s2 - (u128)s1 * s1;
     double var = (double)V / ((double)n * (double)(n - 1));
-    double h = 1.06 * sqrt(var) * pow((double)n, -0.2);
-    H = (int64_t)floor(h * 256.0 + 0.5);
+    H = kde_bw_q8(var, n);
   }
   *bw_q8 = (int32_t)H;
 
@@ -156,8 +269,7 @@ static void kde_group(int64_t n, const uint64_t* d, int32_t s, int32_t frac_pm, 
     uint32_t* w = malloc((size_t)G * sizeof(uint32_t));
     int32_t T = -1;
     for (int32_t t = 0; t < G; t++) {
-      double a = (double)(32768LL * t * t) / (double)(H * H);
-      uint32_t wt = (uint32_t)floor(65536.0 * exp(-a) + 0.5);
+      uint32_t wt = kde_weight(t, H);
       if (wt == 0) break;
       w[t] = wt;
       T = t;

@@ -77,6 +77,26 @@ def _spikes(*pairs):
     return out
 
 
+def nearest_fifth_root_recip(n: int) -> float:
+    """The double nearest to n^(-1/5), from 60-digit decimal arithmetic
+    (Decimal -> float rounds to nearest)."""
+    from decimal import Decimal, localcontext
+    with localcontext() as ctx:
+        ctx.prec = 60
+        return float(Decimal(n) ** (Decimal(-1) / Decimal(5)))
+
+
+def test_fifth_root_is_the_nearest_double():
+    # the bandwidth's n^(-1/5): every n to 20,000, random n to 2^33, perfect
+    # fifth powers and powers of two, against exact decimal arithmetic
+    rng = np.random.default_rng(9)
+    ns = np.concatenate([np.arange(1, 20_001), rng.integers(20_001, 2**33, size=5000),
+                         np.array([k**5 for k in range(2, 80)] + [2**k for k in range(33)])]).astype(np.int64)
+    got = oracle.kde_pow_m02_many(ns)
+    want = np.array([nearest_fifth_root_recip(int(n)) for n in ns])
+    assert np.array_equal(got, want), ns[got != want][:5]
+
+
 @pytest.mark.parametrize("na,nb,octaves", [(100, 100, 2), (1000, 300, 5), (7, 9, 3)])
 def test_bandwidth_two_spikes(na, nb, octaves):
     # grid values 64*20 and 64*(20 + octaves): exact powers of two
@@ -84,7 +104,7 @@ def test_bandwidth_two_spikes(na, nb, octaves):
     r = oracle.kde_group(_spikes((2**20, na), (2**(20 + octaves), nb)))
     n = na + nb
     var = na * nb * D * D / (n * (n - 1))  # closed form of the sample variance
-    h = 1.06 * math.sqrt(var) * n ** -0.2
+    h = 1.06 * math.sqrt(var) * nearest_fifth_root_recip(n)
     assert r["bw_q8"] == math.floor(h * 256 + 0.5)
 
 
