@@ -337,7 +337,8 @@ int argus_iter_windows(const int64_t* step_ns, int32_t n_ranks, int32_t n_steps,
  *     The group's grid is every integer from x(min) to x(max), G points.
  *  2. Bandwidth (Scott's rule as the paper prints it, in grid steps):
  *     var = (n * sum x^2 - (sum x)^2) / (n (n - 1)) evaluated in double from
- *     exact integer sums, h = (1.06 * sqrt(var)) * n^-0.2,
+ *     exact integer sums, h = (1.06 * sqrt(var)) * n^(-1/5) with n^(-1/5) the
+ *     double nearest to the real value (decided exactly, no math library),
  *     H = floor(256 h + 0.5); n < 2 gives H = 0. Reported as bw_q8.
  *  3. Density: w(t) = floor(65536 exp(-32768 t^2 / H^2) + 0.5) (double),
  *     f(j) = sum_b c(b) w(|j - b|) over the group's grid histogram c.
@@ -361,9 +362,13 @@ int argus_iter_windows(const int64_t* step_ns, int32_t n_ranks, int32_t n_steps,
  * the weights are 16-bit integers. Against Eq. 1 evaluated exactly (raw logs,
  * unrounded bandwidth, float64 Gaussian) the tested groups keep the same
  * number of clusters, with at most 6.5e-4 of the samples in another cluster.
- * The only floating-point steps are sqrt, n^-0.2 and exp in step 2 and 3;
- * integer outputs follow from them exactly. Thresholds and tie rules are
- * this library's readings: the paper names the filters but gives no values.
+ * The only floating-point steps are sqrt and exp in step 2 and 3 (n^(-1/5)
+ * is exact by construction); integer outputs follow from them exactly. sqrt
+ * and exp are the device's; the weights and bandwidths they give equal those
+ * of the host C library on their reachable domain as tested: every weight of
+ * every H up to 2^17 and H for 2^22 random (var, n). Thresholds and tie rules
+ * are this library's readings: the paper names the filters but gives no
+ * values.
  *
  * Inputs: the events (same rules as argus_summarize) and the count, min_ns
  * and max_ns outputs of argus_summarize over those same events. If they do

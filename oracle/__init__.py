@@ -55,12 +55,12 @@ def lib():
         L.orc_kde_bin.restype = ctypes.c_int
         L.orc_kde_group.argtypes = [I64, V] + [I32] * 4 + [V] * 8
         L.orc_kde_weights.argtypes = [I64, I32, V]
-        L.orc_kde_pow_m02.argtypes = [I64]
-        L.orc_kde_pow_m02.restype = ctypes.c_double
+        L.orc_kde_root5.argtypes = [I64]
+        L.orc_kde_root5.restype = ctypes.c_double
         L.orc_kde_bw_q8.argtypes = [ctypes.c_double, I64]
         L.orc_kde_bw_q8.restype = I64
         L.orc_kde_weights_many.argtypes = [V, V, I32, V]
-        L.orc_kde_pow_m02_many.argtypes = [V, I64, V]
+        L.orc_kde_root5_many.argtypes = [V, I64, V]
         L.orc_kde_bw_q8_many.argtypes = [V, V, I64, V]
         L.orc_kde.argtypes = [I64, I32, I32, I64] + [V] * 5 + [I32] * 4 + [V] * 5
         L.orc_kde.restype = I64
@@ -222,9 +222,9 @@ def kde_weights(H: int, nt: int) -> np.ndarray:
     return w
 
 
-def kde_pow_m02(n: int) -> float:
-    """n^-0.2 as the oracle's bandwidth takes it."""
-    return lib().orc_kde_pow_m02(n)
+def kde_root5(n: int) -> float:
+    """n^(-1/5) as the oracle's bandwidth takes it (the nearest double)."""
+    return lib().orc_kde_root5(n)
 
 
 def kde_bw_q8(var: float, n: int) -> int:
@@ -242,10 +242,10 @@ def kde_weights_many(H: np.ndarray, off: np.ndarray) -> np.ndarray:
     return w
 
 
-def kde_pow_m02_many(n: np.ndarray) -> np.ndarray:
+def kde_root5_many(n: np.ndarray) -> np.ndarray:
     n = np.ascontiguousarray(n, dtype=np.int64)
     out = np.empty(n.size, np.float64)
-    lib().orc_kde_pow_m02_many(_p(n), n.size, _p(out))
+    lib().orc_kde_root5_many(_p(n), n.size, _p(out))
     return out
 
 

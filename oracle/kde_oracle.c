@@ -195,7 +195,7 @@ static uint32_t kde_weight(int64_t t, int64_t H) {
 void orc_kde_weights(int64_t H, int32_t nt, uint32_t* w) {
   for (int32_t t = 0; t < nt; t++) w[t] = kde_weight(t, H);
 }
-double orc_kde_pow_m02(int64_t n) { return kde_pw(n); }
+double orc_kde_root5(int64_t n) { return kde_pw(n); }
 int64_t orc_kde_bw_q8(double var, int64_t n) { return kde_bw_q8(var, n); }
 
 /* The same over arrays: weights of t = 0 .. off[i+1]-off[i]-1 for each H[i]
@@ -204,7 +204,7 @@ void orc_kde_weights_many(const int64_t* H, const int64_t* off, int32_t nH, uint
   for (int32_t i = 0; i < nH; i++)
     for (int64_t t = 0; t < off[i + 1] - off[i]; t++) w[off[i] + t] = kde_weight(t, H[i]);
 }
-void orc_kde_pow_m02_many(const int64_t* n, int64_t m, double* out) {
+void orc_kde_root5_many(const int64_t* n, int64_t m, double* out) {
   for (int64_t i = 0; i < m; i++) out[i] = kde_pw(n[i]);
 }
 void orc_kde_bw_q8_many(const double* var, const int64_t* n, int64_t m, int64_t* out) {

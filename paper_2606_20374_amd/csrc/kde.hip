@@ -21,7 +21,7 @@
 //   kde_block_kernel     one 128-thread workgroup per cell of 2,048 or more
 //                        durations.
 //   kde_cell_kernel<0>   one wavefront per cell, cells claimed 64 at a time
-//                        with their summaries, n^-0.2 and (for cells of up to
+//                        with their summaries, n^(-1/5) and (for cells of up to
 //                        256 durations) the next cell's durations prefetched
 //                        while the current cell is processed: grid histogram
 //                        in LDS, exact bandwidth, integer-weight density
@@ -38,6 +38,7 @@
 #include <vector>
 
 #include "argus_internal.h"
+#include "kde_math.h"
 
 namespace argus {
 namespace {
@@ -49,7 +50,7 @@ constexpr int kScatterThreads = 512;
 constexpr int kWave = 64;
 constexpr int kMaxC = ARGUS_KDE_MAXC;
 constexpr int kMaxT = 2 * kMaxC;  // selection targets: p50 and p99 per cluster
-constexpr int kPowTab = 65536;    // n^-0.2 for n below this, from the host libm
+constexpr int kPowTab = 65536;    // n^(-1/5) tabulated for n below this
 constexpr int kRegVals = 4;       // cells of up to 256 durations stay in registers
 constexpr int kDigit = 6;         // radix-selection digit width (64 counters per target)
 
@@ -72,12 +73,9 @@ struct Tier<2> {
   static constexpr int kWords = 20688, kCand = 2047;
 };
 
-// n^-0.2 for small n, filled once per device from the host's pow().
+// n^(-1/5) for small n (kde_pw), filled once per device.
 __device__ double g_kde_pow[kPowTab];
 
-// n^-0.2 for the rare cells of kPowTab or more durations, out of line: inlined,
-// pow's constants are hoisted into the cell loops' registers and spilled there
-__device__ __attribute__((noinline)) double pow_m02(double n) { return pow(n, -0.2); }
 
 struct KdeArgs {
   const int32_t* kernel_id;
@@ -634,7 +632,7 @@ struct CellMeta {
   uint32_t n;
   int64_t mn, mx;
   int64_t off;  // first duration in the bucket, or -1 when the summary does not match
-  double pw;    // n^-0.2 from the table (0 when n is outside it)
+  double pw;    // n^(-1/5) from the table (0 when n is outside it)
 };
 
 template <int TIER>
@@ -803,9 +801,15 @@ __device__ bool kde_analyze(const KdeArgs& a, CellLds<TIER>& L, const CellMeta& 
     if (!__builtin_mul_overflow((uint64_t)n, s2, &ns2) && s1 < (1ull << 32)) vnum = (double)(ns2 - s1 * s1);
     else vnum = u128_to_f64((unsigned __int128)n * s2 - (unsigned __int128)s1 * s1);
     const double var = vnum / ((double)n * (double)(n - 1));
-    const double pw = n < (uint32_t)kPowTab ? cm.pw : pow_m02((double)n);
-    const double h = 1.06 * sqrt(var) * pw;
-    H = (int64_t)floor(h * 256.0 + 0.5);
+    double pw = cm.pw;
+    if (n >= (uint32_t)kPowTab) {
+      // tier 0 is routed fewer than 2,048 durations; should a larger cell come
+      // here, it goes on to tier 1 rather than carry the exact root's
+      // registers in the hottest kernel
+      if (TIER == 0) return false;
+      pw = kde_pw(n);
+    }
+    H = kde_bw_q8(var, pw);
   }
 
   // 3-4. weights, density and valleys
@@ -824,7 +828,7 @@ __device__ bool kde_analyze(const KdeArgs& a, CellLds<TIER>& L, const CellMeta& 
     for (int tb = 0; tb <= C; tb += kWave) {
       const int t = tb + l;
       uint32_t wt = 0;
-      if (!past && t < G) wt = (uint32_t)floor(65536.0 * exp(-(double)(32768ll * t * t) / H2) + 0.5);
+      if (!past && t < G) wt = kde_weight(t, H2);
       const int cnt = __popcll(__ballot(wt != 0));  // weights are non-increasing in t
       if (!past) T = tb + cnt - 1;
       past = past || cnt < kWave;
@@ -1701,8 +1705,7 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
       s2 += k * (uint64_t)j * (uint64_t)j;
     }
     const double var = (double)(n * s2 - s1 * s1) / ((double)n * (double)(n - 1));
-    const double h = 1.06 * sqrt(var) * cm.pw;
-    H = (int64_t)floor(h * 256.0 + 0.5);
+    H = kde_bw_q8(var, cm.pw);
   }
 
   // 3-4. weights, then the density in one pass with its valleys: a run of
@@ -1713,7 +1716,7 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
     const double H2 = (double)(H * H);
     int T = -1;
     for (int t = 0; t < G; ++t) {
-      const uint32_t wt = (uint32_t)floor(65536.0 * exp(-(double)(32768ll * t * t) / H2) + 0.5);
+      const uint32_t wt = kde_weight(t, H2);
       if (wt == 0) break;
       if (t == kLaneT) return false;  // kernel wider than the lane's weight table
       L.w[t][l] = wt;
@@ -2129,7 +2132,12 @@ const uint32_t* thresholds() {
   return th;
 }
 
-// Fill g_kde_pow on the current device once.
+__global__ void kde_pow_table_kernel() {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n < kPowTab) g_kde_pow[n] = n > 0 ? kde_pw((uint64_t)n) : 0.0;
+}
+
+// Fill g_kde_pow on the current device once (before its first KDE call).
 hipError_t ensure_pow_table() {
   static std::mutex mu;
   static bool done[64];
@@ -2139,10 +2147,9 @@ hipError_t ensure_pow_table() {
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
   std::lock_guard<std::mutex> lock(mu);
   if (done[dev]) return hipSuccess;
-  std::vector<double> tab(kPowTab);
-  tab[0] = 0.0;
-  for (int n = 1; n < kPowTab; ++n) tab[n] = std::pow((double)n, -0.2);
-  e = hipMemcpyToSymbol(HIP_SYMBOL(g_kde_pow), tab.data(), sizeof(double) * kPowTab);
+  hipLaunchKernelGGL(kde_pow_table_kernel, dim3(kPowTab / 256), dim3(256), 0, nullptr);
+  e = hipGetLastError();
+  if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e == hipSuccess) done[dev] = true;
   return e;
 }

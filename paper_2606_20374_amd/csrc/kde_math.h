@@ -1,0 +1,80 @@
+// The floating-point steps of the KDE clustering definition (section 5.2,
+// Eq. 1: Gaussian kernel, bandwidth 1.06 sigma n^(-1/5)), one copy for every
+// cell tier. The integer outputs follow from these results exactly. n^(-1/5)
+// is decided exactly (no math library involved); sqrt is correctly rounded;
+// exp enters the weights, and a GPU test evaluates these same functions over
+// their whole reachable domain against the host C library's.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace argus {
+
+// Sign of c^5 n - 2^e, exactly (c < 2^55, n < 2^33, so the product has at
+// most 308 bits: six 64-bit limbs).
+__device__ inline int kde_fifth_cmp(uint64_t c, uint64_t n, int e) {
+  uint64_t a[6] = {1, 0, 0, 0, 0, 0};
+#pragma unroll 1
+  for (int r = 0; r < 6; ++r) {
+    const uint64_t m = r < 5 ? c : n;
+    unsigned __int128 carry = 0;
+#pragma unroll
+    for (int i = 0; i < 6; ++i) {
+      const unsigned __int128 v = (unsigned __int128)a[i] * m + carry;
+      a[i] = (uint64_t)v;
+      carry = v >> 64;
+    }
+  }
+  int top = 5;
+  while (top > 0 && a[top] == 0) --top;
+  const int bits = 64 * top + (a[top] ? 64 - __builtin_clzll(a[top]) : 0);
+  if (bits != e + 1) return bits > e + 1 ? 1 : -1;
+  for (int i = 0; i < 6; ++i)
+    if (a[i] != (i == e / 64 ? (1ull << (e % 64)) : 0ull)) return 1;
+  return 0;
+}
+
+// n^(-1/5) for the bandwidth: the double nearest to the real value, for
+// 1 <= n < 2^33. Starting from the device pow (a few units in the last place
+// off), the candidate y = M 2^q (M in [2^52, 2^53)) moves one unit at a time
+// until z = n^(-1/5) lies between the midpoints to its neighbours; z < c 2^k
+// iff c^5 n > 2^(-5k). Below a power of two the lower neighbour is half a
+// unit away, so that midpoint is (4M - 1) 2^(q-2). Out of line: the cell
+// kernels call it only for cells of 65,536 or more durations (the others
+// read a table this function filled).
+__device__ __attribute__((noinline)) inline double kde_pw(uint64_t n) {
+  double y = pow((double)n, -0.2);
+  for (int it = 0; it < 64; ++it) {
+    const uint64_t bits = (uint64_t)__double_as_longlong(y);
+    const uint64_t M = (bits & ((1ull << 52) - 1)) | (1ull << 52);
+    const int q = (int)(bits >> 52) - 1075;
+    if (kde_fifth_cmp(2 * M + 1, n, 5 * (1 - q)) <= 0) {  // z above the upper midpoint
+      y = __longlong_as_double((long long)(bits + 1));
+      continue;
+    }
+    const int below = M == (1ull << 52) ? kde_fifth_cmp(4 * M - 1, n, 5 * (2 - q))
+                                        : kde_fifth_cmp(2 * M - 1, n, 5 * (1 - q));
+    if (below >= 0) {  // z below the lower midpoint
+      y = __longlong_as_double((long long)(bits - 1));
+      continue;
+    }
+    break;
+  }
+  return y;
+}
+
+// Quantised bandwidth H = floor(256 h + 0.5), h = 1.06 sqrt(var) n^(-1/5),
+// in 1/256 grid steps; pw = kde_pw(n).
+__device__ __forceinline__ int64_t kde_bw_q8(double var, double pw) {
+  const double h = 1.06 * sqrt(var) * pw;
+  return (int64_t)floor(h * 256.0 + 0.5);
+}
+
+// Integer Gaussian weight of grid distance t for bandwidth H (H2 = H * H as
+// a double): floor(65536 exp(-t^2 / (2 (H / 256)^2)) + 0.5).
+__device__ __forceinline__ uint32_t kde_weight(int t, double H2) {
+  return (uint32_t)floor(65536.0 * exp(-(double)(32768ll * t * t) / H2) + 0.5);
+}
+
+}  // namespace argus

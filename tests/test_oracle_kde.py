@@ -92,7 +92,7 @@ def test_fifth_root_is_the_nearest_double():
     rng = np.random.default_rng(9)
     ns = np.concatenate([np.arange(1, 20_001), rng.integers(20_001, 2**33, size=5000),
                          np.array([k**5 for k in range(2, 80)] + [2**k for k in range(33)])]).astype(np.int64)
-    got = oracle.kde_pow_m02_many(ns)
+    got = oracle.kde_root5_many(ns)
     want = np.array([nearest_fifth_root_recip(int(n)) for n in ns])
     assert np.array_equal(got, want), ns[got != want][:5]
 
