@@ -313,10 +313,7 @@ def main():
     # L1 iteration windows on a long series: 10,240 ranks x 1,000 steps of
     # step times (seeded: 4% noise, a 1.5x regression on every 7th rank from
     # step 600, a 3x spike on every 11th rank at step 300)
-    rng = np.random.default_rng(7)
-    y = (10**9 * (1 + 0.04 * rng.standard_normal((10_240, 1000)))).astype(np.int64)
-    y[::7, 600:] = y[::7, 600:] * 3 // 2
-    y[::11, 300] *= 3
+    y = tracegen.l1_series(10_240, 1000)
     y_d = torch.from_numpy(y.reshape(-1)).to(dev)
     l1_out = pa.alloc_iter_windows(10_240, 1000, dev)
     for _ in range(2):

@@ -6,8 +6,11 @@ The oracle regenerates every segment on the host and summarizes it with the
 unmodified single-threaded code on disjoint chunks in parallel; its
 summaries (never the GPU's) feed the oracle's cross-rank and L1 steps.
 Everything is compared element by element; float32 fields within 1e-5
-relative. Planted faults must be recovered exactly. The group-aware L2 step
-runs over the same summaries with the workload's parallel layout.
+relative. Planted faults must be recovered exactly. The upload record stream
+(argus_compact) of every segment is compared byte for byte, and the
+group-aware L2 step runs over the same summaries with the workload's
+parallel layout. L1 also runs on the long-series shape the benchmark times
+(10,240 ranks x 1,000 steps).
 """
 import gc
 
@@ -62,6 +65,15 @@ def _full_parity(name: str, chunk_segments: int = 512):
                 raise AssertionError(f"{name} {f} segments {g0}-{g1}: {len(bad)} mismatches at {bad[:5]}")
     P.assert_int_equal(s, so, ["n_valid", "n_invalid", "t_first", "t_last", "step_ns", "busy_ns",
                                "stream_busy_ns", "wire_bytes"], name)
+    # the upload record stream of every segment, byte for byte
+    gc_ = pa.compact(s, R, S, K, 0)
+    torch.cuda.synchronize()
+    assert int(gc_["dev_status"].item()) == 0
+    ob, ooff = oracle.compact(so, G, K, 0)
+    assert np.array_equal(gc_["seg_byte_off"].cpu().numpy(), ooff), (name, "record offsets")
+    assert np.array_equal(gc_["bytes"][:len(ob)].cpu().numpy(), ob), (name, "records")
+    print(f"[gpu-case] {name}: {len(ob)} record bytes identical", flush=True)
+    del gc_, ob, ooff
     hist = so.pop("hist")
     del hist
     xo = oracle.cross_rank(so["count"], so["sum_ns"], R, S, K)
@@ -114,3 +126,27 @@ def test_full_cluster():
 @pytest.mark.timeout(1200)
 def test_full_skew():
     _full_parity("skew")
+
+
+def test_l1_long_series():
+    """L1 windows and change points on the benchmark's 10,240 x 1,000 step
+    series (every 7th rank regresses 1.5x at step 600, every 11th spikes 3x at
+    step 300), every rank against the oracle."""
+    print("\n[gpu-case] L1 on 10,240 ranks x 1,000 steps", flush=True)
+    y = tracegen.l1_series(10_240, 1000)
+    g = pa.iter_windows(torch.from_numpy(y.reshape(-1)).to(DEV), 10_240, 1000)
+    torch.cuda.synchronize()
+    o = oracle.iter_windows(y.reshape(-1), 10_240, 1000)
+    P.assert_int_equal(g, o, P.L1_INT_FIELDS, "l1 long series")
+    P.assert_float_close(g, o, ["cp_ratio"], "l1 long series")
+    # planted faults: every 11th rank is jitter; every 7th rank that is not
+    # also an 11th regresses at step 600 (on the multiples of 77 the spike at
+    # step 300 lifts the left side's relative std past the 10% bound, so no
+    # split qualifies); no other rank is flagged
+    cls, cp = P.to_np(g["cls"]), P.to_np(g["cp"])
+    r = np.arange(10_240)
+    reg = (r % 7 == 0) & (r % 11 != 0)
+    assert (cp[reg] == 600).all() and (cls[reg] & 2).all()
+    assert (cls[r % 11 == 0] & 1).all()
+    clean = (r % 7 != 0) & (r % 11 != 0)
+    assert (cls[clean] == 0).all()

@@ -443,3 +443,17 @@ def workload_groups(name: str, n_ranks: int, n_events: int, seed: int = 0):
     tp, pp, ep = LAYOUTS[name]
     off, mem, _ = parallel_groups(n_ranks, tp, pp, ep)
     return event_routes(n_events, seed), off, mem
+
+
+def l1_series(n_ranks: int = 10_240, n_steps: int = 1000, seed: int = 7) -> np.ndarray:
+    """Seeded per-rank step times [n_ranks][n_steps] (int64 ns) for the L1
+    iteration-window path at long series: 1 s steps with 4% Gaussian noise,
+    a 1.5x regression from step 600 on every 7th rank, a 3x spike at step 300
+    on every 11th rank."""
+    rng = np.random.default_rng(seed)
+    y = (10**9 * (1 + 0.04 * rng.standard_normal((n_ranks, n_steps)))).astype(np.int64)
+    if n_steps > 600:
+        y[::7, 600:] = y[::7, 600:] * 3 // 2
+    if n_steps > 300:
+        y[::11, 300] *= 3
+    return y
