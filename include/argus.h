@@ -394,7 +394,7 @@ typedef struct argus_kde_out {
 
 void argus_kde_default(argus_kde_params_t* p);
 
-/* Workspace bytes: 8 per event plus 14 per cell plus a fixed part. */
+/* Workspace bytes: 8 per event plus 14 per cell plus 1 per rank-step plus a fixed part. */
 size_t argus_kde_workspace(const argus_events_t* ev);
 
 /* ev: as for argus_summarize, n_kernels <= ARGUS_MAX_KDE_KERNELS.

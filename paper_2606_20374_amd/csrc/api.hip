@@ -228,7 +228,8 @@ void argus_kde_default(argus_kde_params_t* p) {
 
 size_t argus_kde_workspace(const argus_events_t* ev) {
   if (!ev || ev->n_ranks < 0 || ev->n_steps < 0 || ev->n_kernels < 0 || ev->n_events < 0) return 0;
-  return kde_workspace_bytes(ev->n_events, (int64_t)ev->n_ranks * ev->n_steps * ev->n_kernels);
+  return kde_workspace_bytes(ev->n_events, (int64_t)ev->n_ranks * ev->n_steps,
+                             (int64_t)ev->n_ranks * ev->n_steps * ev->n_kernels);
 }
 
 int argus_kde(const argus_events_t* ev, const argus_summary_t* sum, const argus_kde_params_t* params,

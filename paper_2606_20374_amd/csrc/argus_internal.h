@@ -134,10 +134,10 @@ struct KdeLaunch {
   const int64_t* max_ns;
   argus_kde_params_t p;
   argus_kde_out_t o;
-  void* workspace;  // kde_workspace_bytes(n_events, n_seg * n_kernels), 256-byte aligned
+  void* workspace;  // kde_workspace_bytes(n_events, n_seg, n_seg * n_kernels), 256-byte aligned
 };
 hipError_t launch_kde(const KdeLaunch& a, hipStream_t st);
-size_t kde_workspace_bytes(int64_t n_events, int64_t cells);
+size_t kde_workspace_bytes(int64_t n_events, int64_t n_seg, int64_t cells);
 
 struct W1Launch {
   const uint8_t* n_clusters;

@@ -100,7 +100,9 @@ struct KdeArgs {
   // [8] wide lane pass queue, [9] wide list length, [10] workgroup tier queue, [11] heavy list length,
   // [12] lane list length
   uint32_t* counters;
-  uint64_t* bucket;    // [n_events]: segment g's durations at seg_off[g] + local position
+  uint64_t* bucket;    // [n_events]: segment g's durations from byte 8 seg_off[g], one record per
+                       // local position, of 4 bytes (seg_w4[g] = 1) or 8
+  uint8_t* seg_w4;     // [n_seg]
   uint32_t* cell_end;  // [cells]: local end offset of each cell's durations
   uint32_t* list1;     // [cells]: the cells of the wide lane pass (from the bottom) and of the
                        // first lane pass (from the top), each in cost-class order; later
@@ -222,6 +224,7 @@ __global__ __launch_bounds__(kScatterThreads) void kde_scatter_kernel(KdeArgs a)
     __syncthreads();
     const uint32_t g = claim;
     if (g >= (uint32_t)a.n_seg) break;
+    if (tid == 0) a.seg_w4[g] = 0;  // 8-byte records
     // cursors = exclusive prefix of the segment's per-kernel counts
     const uint32_t* cnt = a.count + (int64_t)g * K;
     const int k0 = tid * per, k1 = min(K, k0 + per);
@@ -292,59 +295,79 @@ __global__ __launch_bounds__(kScatterThreads) void kde_scatter_kernel(KdeArgs a)
 
 // ----------------------------------------------------------- staged scatter
 // For id spaces of up to kStageK kernel ids. Scattering each duration with
-// its own 8-byte store leaves partly written cache lines for the many rare
-// kernel ids, and HBM then writes about twice the durations' bytes. Here
-// each kernel id keeps a window of kStageW positions, [done, done + 8), in
-// LDS; a duration whose position falls inside the window is staged, any
-// later one (a frequent id within one round) is stored directly. After each
-// round of 8,192 events the workgroup writes out the staged positions up to
-// the last complete aligned group of 8 (64 bytes), or all of them when the
-// id overflowed its window, and advances the window. The rule that decides
-// staged or direct reads only the window start, which changes between
-// rounds, so the result does not depend on when the flushes happen. The
-// workgroup shares only LDS state, so its barriers order LDS alone and the
-// next round's loads stay in flight across them.
+// its own store leaves partly written cache lines for the many rare kernel
+// ids, and HBM then writes about twice the durations' bytes. Here each kernel
+// id keeps a window of one 64-byte group of positions (W = 8 records of 8
+// bytes or 16 of 4), [done, done + W), in LDS; a duration whose position
+// falls inside the window is staged, any later one (a frequent id within one
+// round) is stored directly. After each round of 8,192 events the workgroup
+// writes out the staged positions up to the last complete aligned 64-byte
+// group, or all of them when the id overflowed its window, and advances the
+// window. The rule that decides staged or direct reads only the window start,
+// which changes between rounds, so the result does not depend on when the
+// flushes happen. The workgroup shares only LDS state, so its barriers order
+// LDS alone and the next round's loads stay in flight across them.
+//
+// Record width: a segment's durations are stored in 4 bytes when the segment
+// takes the buffer path below and every present cell's summarized maximum is
+// below 2^31, else in 8. A 4-byte record saturates at 2^32 - 1. A duration of
+// 2^31 or more in such a segment can only come from summaries that do not
+// match the events; it lies in a higher octave than its cell's summarized
+// maximum, so on a grid of any resolution the cells' range check reports it.
 constexpr int kStageThreads = 1024;
 constexpr int kStageK = 2048;
-constexpr int kStageW = 8;
 constexpr int kStageD = 2;  // groups of four events per thread and round
+constexpr uint64_t kW4Max = 0xFFFFFFFFull;  // saturation of a 4-byte record
+constexpr uint64_t kW4Lim = 1ull << 31;     // summarized maxima below this allow 4-byte records
 
+template <typename R>
 struct StageCtx {
-  uint64_t (*stage)[kStageW];
+  static constexpr int W = 64 / (int)sizeof(R);  // positions per 64-byte group
+  R (*stage)[W];
   uint32_t* cur;
   const uint32_t* done;
-  uint64_t* out;
-  uint32_t len, lo7;  // segment length; lo mod 8, the global alignment of local position 0
+  R* out;
+  uint32_t len, al;  // segment length; position of local 0 in its 64-byte group (in records)
   int32_t K, NS;
 };
 
-__device__ __forceinline__ void stage_one(const StageCtx& s, int32_t kid, int32_t st, int64_t t0, int64_t t1) {
+template <typename R>
+__device__ __forceinline__ R to_record(uint64_t d) {
+  if constexpr (sizeof(R) == 8) return d;
+  else return (R)(d < kW4Max ? d : kW4Max);
+}
+
+template <typename R>
+__device__ __forceinline__ void stage_one(const StageCtx<R>& s, int32_t kid, int32_t st, int64_t t0, int64_t t1) {
+  constexpr int W = StageCtx<R>::W;
   if (kid >= 0 && kid < s.K && st >= 0 && st < s.NS && t0 >= 0 && t1 >= t0) {
     const uint32_t p = atomicAdd(&s.cur[kid], 1u);
-    const uint64_t d = (uint64_t)t1 - (uint64_t)t0;
-    if (p - s.done[kid] < (uint32_t)kStageW) s.stage[kid][(p + s.lo7) & (kStageW - 1)] = d;
+    const R d = to_record<R>((uint64_t)t1 - (uint64_t)t0);
+    if (p - s.done[kid] < (uint32_t)W) s.stage[kid][(p + s.al) & (W - 1)] = d;
     else if (p < s.len) s.out[p] = d;
   }
 }
 
 // Write out kernel id k's staged positions: up to the last complete aligned
 // group, everything when the window overflowed, or everything (final).
-__device__ __forceinline__ void stage_flush(const StageCtx& s, uint32_t* done, int k, bool final) {
+template <typename R>
+__device__ __forceinline__ void stage_flush(const StageCtx<R>& s, uint32_t* done, int k, bool final) {
+  constexpr int W = StageCtx<R>::W;
   const uint32_t c = s.cur[k], dn = done[k];
   if (c == dn) return;
   uint32_t e, nd;
-  if (c - dn > (uint32_t)kStageW) {
-    e = dn + kStageW;
+  if (c - dn > (uint32_t)W) {
+    e = dn + W;
     nd = c;
   } else if (final) {
     e = nd = c;
   } else {
-    const int64_t al = (int64_t)((c + s.lo7) & ~(uint32_t)(kStageW - 1)) - (int64_t)s.lo7;
+    const int64_t al = (int64_t)((c + s.al) & ~(uint32_t)(W - 1)) - (int64_t)s.al;
     if (al <= (int64_t)dn) return;
     e = nd = (uint32_t)al;
   }
   for (uint32_t p = dn; p < e; ++p)
-    if (p < s.len) s.out[p] = s.stage[k][(p + s.lo7) & (kStageW - 1)];
+    if (p < s.len) s.out[p] = s.stage[k][(p + s.al) & (W - 1)];
   done[k] = nd;
 }
 
@@ -364,16 +387,22 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, int
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-__device__ __forceinline__ void buf_store_u64(__amdgpu_buffer_rsrc_t r, uint32_t off, uint64_t v) {
+__device__ __forceinline__ void buf_store(__amdgpu_buffer_rsrc_t r, uint32_t off, uint64_t v) {
   __builtin_amdgcn_raw_buffer_store_b64(v2u{(uint32_t)v, (uint32_t)(v >> 32)}, r, (int)off, 0, 0);
+}
+
+__device__ __forceinline__ void buf_store(__amdgpu_buffer_rsrc_t r, uint32_t off, uint32_t v) {
+  __builtin_amdgcn_raw_buffer_store_b32(v, r, (int)off, 0, 0);
 }
 
 // Four events at once. Every lane takes a cursor for all four before any
 // result is used, so the four LDS round trips overlap: an event that is not
 // valid (or past the end) counts on the spare slot kStageK, which no flush
 // reads, and stores nothing.
-__device__ __forceinline__ void stage_four_buf(const StageCtx& s, __amdgpu_buffer_rsrc_t ro, bool ok, v4i k4, v4i s4,
-                                               v2l x0, v2l x1, v2l y0, v2l y1) {
+template <typename R>
+__device__ __forceinline__ void stage_four_buf(const StageCtx<R>& s, __amdgpu_buffer_rsrc_t ro, bool ok, v4i k4,
+                                               v4i s4, v2l x0, v2l x1, v2l y0, v2l y1) {
+  constexpr int W = StageCtx<R>::W;
   const int32_t kid[4] = {k4.x, k4.y, k4.z, k4.w}, st[4] = {s4.x, s4.y, s4.z, s4.w};
   const int64_t t0[4] = {x0.x, x0.y, x1.x, x1.y}, t1[4] = {y0.x, y0.y, y1.x, y1.y};
   bool val[4];
@@ -389,13 +418,13 @@ __device__ __forceinline__ void stage_four_buf(const StageCtx& s, __amdgpu_buffe
   for (int i = 0; i < 4; ++i) dn[i] = s.done[slot[i]];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const uint64_t d = (uint64_t)t1[i] - (uint64_t)t0[i];
+    const R d = to_record<R>((uint64_t)t1[i] - (uint64_t)t0[i]);
     uint32_t off = kOob;
     if (val[i]) {
-      if (p[i] - dn[i] < (uint32_t)kStageW) s.stage[slot[i]][(p[i] + s.lo7) & (kStageW - 1)] = d;
-      else if (p[i] < s.len) off = p[i] * 8u;
+      if (p[i] - dn[i] < (uint32_t)W) s.stage[slot[i]][(p[i] + s.al) & (W - 1)] = d;
+      else if (p[i] < s.len) off = p[i] * (uint32_t)sizeof(R);
     }
-    buf_store_u64(ro, off, d);
+    buf_store(ro, off, d);
   }
 }
 
@@ -403,27 +432,29 @@ __device__ __forceinline__ void stage_four_buf(const StageCtx& s, __amdgpu_buffe
 // positions to write (as stage_flush decides) takes an entry of an LDS list
 // of kFlushCap; ids that find the list full keep their positions staged for
 // a later round (the staging rule allows any flush time). Write: one lane
-// per (entry, position), kFlushCap * kStageW / kStageThreads stores per
-// thread whether used or not.
+// per (entry, position), kFlushCap * W / kStageThreads stores per thread
+// whether used or not.
 constexpr int kFlushCap = 512;
 
 struct FlushEntry {
   uint32_t k, dn, e, nd;
 };
 
-__device__ __forceinline__ void stage_plan(const StageCtx& s, const uint32_t* done, int k, FlushEntry* list,
+template <typename R>
+__device__ __forceinline__ void stage_plan(const StageCtx<R>& s, const uint32_t* done, int k, FlushEntry* list,
                                            uint32_t* n_list) {
+  constexpr int W = StageCtx<R>::W;
   uint32_t dn = 0, e = 0, nd = 0;
   bool act = false;
   if (k < s.K) {
     const uint32_t c = s.cur[k];
     dn = done[k];
-    if (c - dn > (uint32_t)kStageW) {
-      e = dn + kStageW;
+    if (c - dn > (uint32_t)W) {
+      e = dn + W;
       nd = c;
       act = true;
     } else if (c != dn) {
-      const int64_t al = (int64_t)((c + s.lo7) & ~(uint32_t)(kStageW - 1)) - (int64_t)s.lo7;
+      const int64_t al = (int64_t)((c + s.al) & ~(uint32_t)(W - 1)) - (int64_t)s.al;
       if (al > (int64_t)dn) {
         e = nd = (uint32_t)al;
         act = true;
@@ -440,52 +471,180 @@ __device__ __forceinline__ void stage_plan(const StageCtx& s, const uint32_t* do
   if (act && idx < (uint32_t)kFlushCap) list[idx] = FlushEntry{(uint32_t)k, dn, e, nd};
 }
 
-__device__ __forceinline__ void stage_write(const StageCtx& s, __amdgpu_buffer_rsrc_t ro, uint32_t* done,
+template <typename R>
+__device__ __forceinline__ void stage_write(const StageCtx<R>& s, __amdgpu_buffer_rsrc_t ro, uint32_t* done,
                                             const FlushEntry* list, uint32_t n_list, int tid) {
+  constexpr int W = StageCtx<R>::W;
   const uint32_t n = n_list < (uint32_t)kFlushCap ? n_list : (uint32_t)kFlushCap;
 #pragma unroll
-  for (int j = 0; j < kFlushCap * kStageW / kStageThreads; ++j) {
+  for (int j = 0; j < kFlushCap * W / kStageThreads; ++j) {
     const uint32_t slot = (uint32_t)(j * kStageThreads + tid);
-    const uint32_t ent = slot / kStageW, i = slot % kStageW;
+    const uint32_t ent = slot / W, i = slot % W;
     uint32_t off = kOob;
-    uint64_t v = 0;
+    R v = 0;
     if (ent < n) {
       const FlushEntry f = list[ent];
       const uint32_t p = f.dn + i;
       if (p < f.e && p < s.len) {
-        off = p * 8u;
-        v = s.stage[f.k][(p + s.lo7) & (kStageW - 1)];
+        off = p * (uint32_t)sizeof(R);
+        v = s.stage[f.k][(p + s.al) & (W - 1)];
       }
       if (i == 0) done[f.k] = f.nd;
     }
-    buf_store_u64(ro, off, v);
+    buf_store(ro, off, v);
   }
 }
 
-__global__ __launch_bounds__(kStageThreads) void kde_scatter_staged_kernel(KdeArgs a) {
-  __shared__ uint64_t stage[kStageK][kStageW];
-  __shared__ uint32_t cur[kStageK + 1], done[kStageK + 1];  // + the spare slot
-  __shared__ uint32_t wave_tot[kStageThreads / kWave];
-  __shared__ uint32_t claim, n_list;
-  __shared__ FlushEntry list[kFlushCap];
-  const int tid = threadIdx.x, K = a.K;
-  const int per = (K + kStageThreads - 1) / kStageThreads;
+// One well-formed segment [lo, hi) of the staged scatter, the cursors set up;
+// returns with every staged position written out.
+template <typename R>
+__device__ void stage_segment(const KdeArgs& a, const StageCtx<R>& s, uint32_t* done, FlushEntry* list,
+                              uint32_t* n_list, int64_t lo, int64_t hi, int tid) {
   const v4i* K4 = reinterpret_cast<const v4i*>(a.kernel_id);
   const v4i* S4 = reinterpret_cast<const v4i*>(a.stream);
   const v2l* T0 = reinterpret_cast<const v2l*>(a.start_ns);
   const v2l* T1 = reinterpret_cast<const v2l*>(a.end_ns);
+  int64_t a4 = hi, b4 = hi;  // aligned body [a4, b4) in groups of four events
+  if (a.vec_ok) {
+    const int64_t up = (lo + 3) & ~(int64_t)3, dn = hi & ~(int64_t)3;
+    a4 = up < hi ? up : hi;
+    b4 = dn > a4 ? dn : a4;
+  }
+  // head [lo, a4) (the whole segment without aligned arrays) and tail [b4, hi)
+  for (int64_t i = lo + tid; i < a4; i += kStageThreads)
+    stage_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
+  for (int64_t i = b4 + tid; i < hi; i += kStageThreads)
+    stage_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
+  const int64_t qa = a4 >> 2, qb = b4 >> 2;
+  if (hi - lo <= kBufEvents) {
+    // rounds of kStageD groups of four events per thread with the next
+    // round's groups in flight, every step the same memory instructions;
+    // staged windows are flushed after every round
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the head / tail stores above are done
+    const int64_t ng = qb - qa;
+    const __amdgpu_buffer_rsrc_t rk = buf_rsrc(a.kernel_id + a4, ng * 16), rs = buf_rsrc(a.stream + a4, ng * 16);
+    const __amdgpu_buffer_rsrc_t r0 = buf_rsrc(a.start_ns + a4, ng * 32), r1 = buf_rsrc(a.end_ns + a4, ng * 32);
+    const __amdgpu_buffer_rsrc_t ro = buf_rsrc(s.out, (int64_t)s.len * (int64_t)sizeof(R));
+    v4u bk[kStageD], bs[kStageD], ba0[kStageD], ba1[kStageD], bb0[kStageD], bb1[kStageD];
+    auto load = [&](int d, int64_t rq) {
+      const uint32_t o16 = rq < ng ? (uint32_t)rq * 16u : kOob, o32 = rq < ng ? (uint32_t)rq * 32u : kOob;
+      bk[d] = __builtin_amdgcn_raw_buffer_load_b128(rk, (int)o16, 0, 0);
+      bs[d] = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)o16, 0, 0);
+      ba0[d] = __builtin_amdgcn_raw_buffer_load_b128(r0, (int)o32, 0, 0);
+      ba1[d] = __builtin_amdgcn_raw_buffer_load_b128(r0, (int)(o32 + 16u), 0, 0);
+      bb0[d] = __builtin_amdgcn_raw_buffer_load_b128(r1, (int)o32, 0, 0);
+      bb1[d] = __builtin_amdgcn_raw_buffer_load_b128(r1, (int)(o32 + 16u), 0, 0);
+    };
+#pragma unroll
+    for (int d = 0; d < kStageD; ++d) load(d, tid + (int64_t)d * kStageThreads);
+    for (int64_t rb = 0; rb < ng; rb += (int64_t)kStageD * kStageThreads) {
+#pragma unroll
+      for (int d = 0; d < kStageD; ++d) {
+        const int64_t rq = rb + tid + (int64_t)d * kStageThreads;
+        const v4i k4 = __builtin_bit_cast(v4i, bk[d]), s4 = __builtin_bit_cast(v4i, bs[d]);
+        const v2l x0 = __builtin_bit_cast(v2l, ba0[d]), x1 = __builtin_bit_cast(v2l, ba1[d]);
+        const v2l y0 = __builtin_bit_cast(v2l, bb0[d]), y1 = __builtin_bit_cast(v2l, bb1[d]);
+        load(d, rq + (int64_t)kStageD * kStageThreads);
+        stage_four_buf(s, ro, rq < ng, k4, s4, x0, x1, y0, y1);
+      }
+      if (tid == 0) *n_list = 0;
+      lds_barrier();
+#pragma unroll
+      for (int kk = 0; kk < kStageK / kStageThreads; ++kk) stage_plan(s, done, tid + kk * kStageThreads, list, n_list);
+      lds_barrier();
+      stage_write(s, ro, done, list, *n_list, tid);
+      lds_barrier();
+    }
+  } else {
+    if constexpr (sizeof(R) == 8) {
+      // segments too long for 32-bit buffer offsets (8-byte records only): the
+      // same rounds with global loads and stores
+      v4i bk[kStageD], bs[kStageD];
+      v2l ba0[kStageD], ba1[kStageD], bb0[kStageD], bb1[kStageD];
+#pragma unroll
+      for (int d = 0; d < kStageD; ++d) {
+        const int64_t q = qa + tid + (int64_t)d * kStageThreads;
+        bk[d] = bs[d] = 0;
+        ba0[d] = ba1[d] = bb0[d] = bb1[d] = 0;
+        if (q < qb) {
+          bk[d] = __builtin_nontemporal_load(K4 + q);
+          bs[d] = __builtin_nontemporal_load(S4 + q);
+          ba0[d] = __builtin_nontemporal_load(T0 + 2 * q);
+          ba1[d] = __builtin_nontemporal_load(T0 + 2 * q + 1);
+          bb0[d] = __builtin_nontemporal_load(T1 + 2 * q);
+          bb1[d] = __builtin_nontemporal_load(T1 + 2 * q + 1);
+        }
+      }
+      for (int64_t r0 = qa; r0 < qb; r0 += (int64_t)kStageD * kStageThreads) {
+#pragma unroll
+        for (int d = 0; d < kStageD; ++d) {
+          const int64_t q = r0 + tid + (int64_t)d * kStageThreads;
+          const v4i k4 = bk[d], s4 = bs[d];
+          const v2l x0 = ba0[d], x1 = ba1[d], y0 = bb0[d], y1 = bb1[d];
+          const int64_t qn = q + (int64_t)kStageD * kStageThreads;
+          if (qn < qb) {
+            bk[d] = __builtin_nontemporal_load(K4 + qn);
+            bs[d] = __builtin_nontemporal_load(S4 + qn);
+            ba0[d] = __builtin_nontemporal_load(T0 + 2 * qn);
+            ba1[d] = __builtin_nontemporal_load(T0 + 2 * qn + 1);
+            bb0[d] = __builtin_nontemporal_load(T1 + 2 * qn);
+            bb1[d] = __builtin_nontemporal_load(T1 + 2 * qn + 1);
+          }
+          if (q < qb) {
+            stage_one(s, k4.x, s4.x, x0.x, y0.x);
+            stage_one(s, k4.y, s4.y, x0.y, y0.y);
+            stage_one(s, k4.z, s4.z, x1.x, y1.x);
+            stage_one(s, k4.w, s4.w, x1.y, y1.y);
+          }
+        }
+        lds_barrier();
+        for (int k = tid; k < s.K; k += kStageThreads) stage_flush(s, done, k, false);
+        lds_barrier();
+      }
+    }
+  }
+  // every staging write and cursor increment of the segment (the head and
+  // tail, and the element-wise path, run without a round barrier after them)
+  lds_barrier();
+  for (int k = tid; k < s.K; k += kStageThreads) stage_flush(s, done, k, true);
+}
+
+union StageLds {
+  uint64_t w8[kStageK][8];
+  uint32_t w4[kStageK][16];
+};
+
+__global__ __launch_bounds__(kStageThreads) void kde_scatter_staged_kernel(KdeArgs a) {
+  __shared__ StageLds stage;
+  __shared__ uint32_t cur[kStageK + 1], done[kStageK + 1];  // + the spare slot
+  __shared__ uint32_t wave_tot[kStageThreads / kWave];
+  __shared__ uint32_t claim, n_list, wide;
+  __shared__ FlushEntry list[kFlushCap];
+  const int tid = threadIdx.x, K = a.K;
+  const int per = (K + kStageThreads - 1) / kStageThreads;
   while (true) {
-    if (tid == 0) claim = atomicAdd(&a.counters[0], 1u);
+    if (tid == 0) {
+      claim = atomicAdd(&a.counters[0], 1u);
+      wide = 0;
+    }
     lds_barrier();
     const uint32_t g = claim;
     if (g >= (uint32_t)a.n_seg) break;
-    // cursors = exclusive prefix of the segment's per-kernel counts
+    // cursors = exclusive prefix of the segment's per-kernel counts; any
+    // present cell's maximum at or above kW4Lim asks for 8-byte records
     const uint32_t* cnt = a.count + (int64_t)g * K;
+    const int64_t* mx = a.max_ns + (int64_t)g * K;
     const int k0 = tid * per, k1 = min(K, k0 + per);
     uint32_t own = 0;
-    for (int k = k0; k < k1; ++k) own += cnt[k];
+    bool big = false;
+    for (int k = k0; k < k1; ++k) {
+      const uint32_t n = cnt[k];
+      own += n;
+      big |= n != 0 && (uint64_t)mx[k] >= kW4Lim;
+    }
     const uint32_t incl = wave_incl_scan(own);
     if (lane_id() == kWave - 1) wave_tot[tid / kWave] = incl;
+    if (__any(big) && lane_id() == 0) wide = 1;
     lds_barrier();
     uint32_t base = incl - own;
     for (int w = 0; w < tid / kWave; ++w) base += wave_tot[w];
@@ -493,114 +652,21 @@ __global__ __launch_bounds__(kStageThreads) void kde_scatter_staged_kernel(KdeAr
       cur[k] = done[k] = base;
       base += cnt[k];
     }
-    lds_barrier();
     const int64_t lo = a.seg_off[g], hi = a.seg_off[g + 1];
     const bool bad = !(lo >= 0 && lo <= hi && hi <= a.n_events && hi - lo <= (int64_t)UINT32_MAX);
-    const StageCtx s{stage, cur, done, a.bucket + (bad ? 0 : lo), bad ? 0u : (uint32_t)(hi - lo),
-                     bad ? 0u : (uint32_t)(lo & 7), K, a.NS};
-    if (!bad) {
-      int64_t a4 = hi, b4 = hi;  // aligned body [a4, b4) in groups of four events
-      if (a.vec_ok) {
-        const int64_t up = (lo + 3) & ~(int64_t)3, dn = hi & ~(int64_t)3;
-        a4 = up < hi ? up : hi;
-        b4 = dn > a4 ? dn : a4;
-      }
-      // head [lo, a4) (the whole segment without aligned arrays) and tail [b4, hi)
-      for (int64_t i = lo + tid; i < a4; i += kStageThreads)
-        stage_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
-      for (int64_t i = b4 + tid; i < hi; i += kStageThreads)
-        stage_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
-      const int64_t qa = a4 >> 2, qb = b4 >> 2;
-      if (hi - lo <= kBufEvents) {
-        // rounds of kStageD groups of four events per thread with the next
-        // round's groups in flight, every step the same memory instructions;
-        // staged windows are flushed after every round
-        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): the head / tail stores above are done
-        const int64_t ng = qb - qa;
-        const __amdgpu_buffer_rsrc_t rk = buf_rsrc(a.kernel_id + a4, ng * 16), rs = buf_rsrc(a.stream + a4, ng * 16);
-        const __amdgpu_buffer_rsrc_t r0 = buf_rsrc(a.start_ns + a4, ng * 32), r1 = buf_rsrc(a.end_ns + a4, ng * 32);
-        const __amdgpu_buffer_rsrc_t ro = buf_rsrc(s.out, (int64_t)s.len * 8);
-        v4u bk[kStageD], bs[kStageD], ba0[kStageD], ba1[kStageD], bb0[kStageD], bb1[kStageD];
-        auto load = [&](int d, int64_t rq) {
-          const uint32_t o16 = rq < ng ? (uint32_t)rq * 16u : kOob, o32 = rq < ng ? (uint32_t)rq * 32u : kOob;
-          bk[d] = __builtin_amdgcn_raw_buffer_load_b128(rk, (int)o16, 0, 0);
-          bs[d] = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)o16, 0, 0);
-          ba0[d] = __builtin_amdgcn_raw_buffer_load_b128(r0, (int)o32, 0, 0);
-          ba1[d] = __builtin_amdgcn_raw_buffer_load_b128(r0, (int)(o32 + 16u), 0, 0);
-          bb0[d] = __builtin_amdgcn_raw_buffer_load_b128(r1, (int)o32, 0, 0);
-          bb1[d] = __builtin_amdgcn_raw_buffer_load_b128(r1, (int)(o32 + 16u), 0, 0);
-        };
-#pragma unroll
-        for (int d = 0; d < kStageD; ++d) load(d, tid + (int64_t)d * kStageThreads);
-        for (int64_t rb = 0; rb < ng; rb += (int64_t)kStageD * kStageThreads) {
-#pragma unroll
-          for (int d = 0; d < kStageD; ++d) {
-            const int64_t rq = rb + tid + (int64_t)d * kStageThreads;
-            const v4i k4 = __builtin_bit_cast(v4i, bk[d]), s4 = __builtin_bit_cast(v4i, bs[d]);
-            const v2l x0 = __builtin_bit_cast(v2l, ba0[d]), x1 = __builtin_bit_cast(v2l, ba1[d]);
-            const v2l y0 = __builtin_bit_cast(v2l, bb0[d]), y1 = __builtin_bit_cast(v2l, bb1[d]);
-            load(d, rq + (int64_t)kStageD * kStageThreads);
-            stage_four_buf(s, ro, rq < ng, k4, s4, x0, x1, y0, y1);
-          }
-          if (tid == 0) n_list = 0;
-          lds_barrier();
-#pragma unroll
-          for (int kk = 0; kk < kStageK / kStageThreads; ++kk) stage_plan(s, done, tid + kk * kStageThreads, list, &n_list);
-          lds_barrier();
-          stage_write(s, ro, done, list, n_list, tid);
-          lds_barrier();
-        }
-      } else {
-        // segments too long for 32-bit buffer offsets: the same rounds with
-        // global loads and stores
-        v4i bk[kStageD], bs[kStageD];
-        v2l ba0[kStageD], ba1[kStageD], bb0[kStageD], bb1[kStageD];
-#pragma unroll
-        for (int d = 0; d < kStageD; ++d) {
-          const int64_t q = qa + tid + (int64_t)d * kStageThreads;
-          bk[d] = bs[d] = 0;
-          ba0[d] = ba1[d] = bb0[d] = bb1[d] = 0;
-          if (q < qb) {
-            bk[d] = __builtin_nontemporal_load(K4 + q);
-            bs[d] = __builtin_nontemporal_load(S4 + q);
-            ba0[d] = __builtin_nontemporal_load(T0 + 2 * q);
-            ba1[d] = __builtin_nontemporal_load(T0 + 2 * q + 1);
-            bb0[d] = __builtin_nontemporal_load(T1 + 2 * q);
-            bb1[d] = __builtin_nontemporal_load(T1 + 2 * q + 1);
-          }
-        }
-        for (int64_t r0 = qa; r0 < qb; r0 += (int64_t)kStageD * kStageThreads) {
-#pragma unroll
-          for (int d = 0; d < kStageD; ++d) {
-            const int64_t q = r0 + tid + (int64_t)d * kStageThreads;
-            const v4i k4 = bk[d], s4 = bs[d];
-            const v2l x0 = ba0[d], x1 = ba1[d], y0 = bb0[d], y1 = bb1[d];
-            const int64_t qn = q + (int64_t)kStageD * kStageThreads;
-            if (qn < qb) {
-              bk[d] = __builtin_nontemporal_load(K4 + qn);
-              bs[d] = __builtin_nontemporal_load(S4 + qn);
-              ba0[d] = __builtin_nontemporal_load(T0 + 2 * qn);
-              ba1[d] = __builtin_nontemporal_load(T0 + 2 * qn + 1);
-              bb0[d] = __builtin_nontemporal_load(T1 + 2 * qn);
-              bb1[d] = __builtin_nontemporal_load(T1 + 2 * qn + 1);
-            }
-            if (q < qb) {
-              stage_one(s, k4.x, s4.x, x0.x, y0.x);
-              stage_one(s, k4.y, s4.y, x0.y, y0.y);
-              stage_one(s, k4.z, s4.z, x1.x, y1.x);
-              stage_one(s, k4.w, s4.w, x1.y, y1.y);
-            }
-          }
-          lds_barrier();
-          for (int k = tid; k < K; k += kStageThreads) stage_flush(s, done, k, false);
-          lds_barrier();
-        }
-      }
-    }
-    // every staging write and cursor increment of the segment (the head and
-    // tail, and the element-wise path, run without a round barrier after them)
+    const bool w4 = !bad && hi - lo <= kBufEvents && !wide;
+    if (tid == 0) a.seg_w4[g] = w4 ? 1 : 0;
     lds_barrier();
-    for (int k = tid; k < K; k += kStageThreads) stage_flush(s, done, k, true);
+    if (w4) {
+      const StageCtx<uint32_t> s{stage.w4, cur, done, reinterpret_cast<uint32_t*>(a.bucket + lo),
+                                 (uint32_t)(hi - lo), (uint32_t)((2 * lo) & 15), K, a.NS};
+      stage_segment(a, s, done, list, &n_list, lo, hi, tid);
+    } else if (!bad) {
+      const StageCtx<uint64_t> s{stage.w8, cur, done, a.bucket + lo, (uint32_t)(hi - lo), (uint32_t)(lo & 7), K,
+                                 a.NS};
+      stage_segment(a, s, done, list, &n_list, lo, hi, tid);
+    }
+    lds_barrier();
     uint32_t* ends = a.cell_end + (int64_t)g * K;
     for (int k = tid; k < K; k += kStageThreads) ends[k] = cur[k];
     lds_barrier();
@@ -630,10 +696,47 @@ struct CellLds {
 // One cell's inputs, checked against the bucketed durations.
 struct CellMeta {
   uint32_t n;
+  uint32_t w4;  // records of 4 bytes (1) or 8 (0)
   int64_t mn, mx;
-  int64_t off;  // first duration in the bucket, or -1 when the summary does not match
+  int64_t off;  // byte offset of the first duration in the bucket, or -1 when the summary does not match
   double pw;    // n^(-1/5) from the table (0 when n is outside it)
 };
+
+// A cell's bucketed durations, records of 4 or 8 bytes. Reads take the
+// width's own loads (one branch per group of loads, uniform when the
+// wavefront works on one cell).
+struct Durs {
+  const void* p;
+  bool w4;
+  // v[u] = record i0 + u * stride where that is below n, else dflt
+  template <int N>
+  __device__ __forceinline__ void get(uint64_t i0, uint32_t stride, uint32_t n, uint64_t (&v)[N],
+                                      uint64_t dflt) const {
+    if (w4) {
+      const uint32_t* q = static_cast<const uint32_t*>(p);
+#pragma unroll
+      for (int u = 0; u < N; ++u) {
+        const uint64_t i = i0 + (uint64_t)u * stride;
+        v[u] = i < n ? (uint64_t)q[i] : dflt;
+      }
+    } else {
+      const uint64_t* q = static_cast<const uint64_t*>(p);
+#pragma unroll
+      for (int u = 0; u < N; ++u) {
+        const uint64_t i = i0 + (uint64_t)u * stride;
+        v[u] = i < n ? q[i] : dflt;
+      }
+    }
+  }
+  __device__ __forceinline__ uint64_t nt(uint32_t i) const {  // streaming (nontemporal) read
+    return w4 ? (uint64_t)__builtin_nontemporal_load(static_cast<const uint32_t*>(p) + i)
+              : __builtin_nontemporal_load(static_cast<const uint64_t*>(p) + i);
+  }
+};
+
+__device__ __forceinline__ Durs durs_of(const KdeArgs& a, const CellMeta& m) {
+  return Durs{reinterpret_cast<const char*>(a.bucket) + m.off, m.w4 != 0};
+}
 
 template <int TIER>
 __device__ void remove_valley(CellLds<TIER>& L, int idx, int m) {
@@ -672,10 +775,11 @@ __device__ void write_empty(const KdeArgs& a, int64_t c) {
 __device__ __forceinline__ void load_small(const KdeArgs& a, const CellMeta& m, uint64_t (&rv)[kRegVals]) {
   const int l = lane_id();
   const bool small = m.off >= 0 && m.n <= (uint32_t)(kWave * kRegVals);
+  const Durs vals = durs_of(a, m);
 #pragma unroll
   for (int r = 0; r < kRegVals; ++r) {
     const uint32_t i = (uint32_t)(l + r * kWave);
-    rv[r] = small && i < m.n ? __builtin_nontemporal_load(a.bucket + m.off + i) : 0ull;
+    rv[r] = small && i < m.n ? vals.nt(i) : 0ull;
   }
 }
 
@@ -1050,7 +1154,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
   constexpr int WORDS = CellLds<TIER>::W;
   const int l = lane_id();
   const uint32_t n = cm.n;
-  const uint64_t* vals = a.bucket + cm.off;
+  const Durs vals = durs_of(a, cm);
   const int sh = 6 - a.sub_bits;
   const int lo = grid64((uint64_t)cm.mn, L.th) >> sh;
   const int G = (grid64((uint64_t)cm.mx, L.th) >> sh) - lo + 1;
@@ -1076,8 +1180,7 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
     // four loads in flight per lane
     for (uint64_t i0 = l; i0 < n; i0 += 4 * kWave) {
       uint64_t v[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = i0 + u * kWave < n ? vals[i0 + u * kWave] : 0ull;
+      vals.get(i0, kWave, n, v, 0ull);
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         if (i0 + u * kWave >= n) break;
@@ -1139,10 +1242,10 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
         for (uint64_t i0 = l; i0 < n; i0 += 4 * kWave) {
           uint64_t v[4];
           bool ok[4];
+          vals.get(i0, kWave, n, v, 0ull);
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
             ok[u] = i0 + u * kWave < n;
-            v[u] = ok[u] ? vals[i0 + u * kWave] : 0ull;
           }
           gather4(v, ok);
         }
@@ -1213,10 +1316,10 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
       for (uint64_t i0 = l; i0 < n; i0 += 4 * kWave) {
         uint64_t v[4];
         bool ok[4];
+        vals.get(i0, kWave, n, v, 0ull);
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           ok[u] = i0 + u * kWave < n;
-          v[u] = ok[u] ? vals[i0 + u * kWave] : 0ull;
         }
         consider4(v, ok);
       }
@@ -1271,8 +1374,9 @@ __device__ CellMeta load_meta(const KdeArgs& a, int64_t c) {
   const int64_t g = c / a.K;
   const int64_t lo = a.seg_off[g], hi = a.seg_off[g + 1];
   const bool seg_ok = lo >= 0 && lo <= hi && hi <= a.n_events && hi - lo <= (int64_t)UINT32_MAX;
+  m.w4 = a.seg_w4[g];
   if (seg_ok && end >= m.n && end - m.n == prev && (int64_t)end <= hi - lo && m.mn >= 0 && m.mn <= m.mx)
-    m.off = lo + (end - m.n);
+    m.off = 8 * lo + (int64_t)(end - m.n) * (m.w4 ? 4 : 8);
   m.pw = m.n < (uint32_t)kPowTab ? g_kde_pow[m.n] : 0.0;
   return m;
 }
@@ -1280,6 +1384,7 @@ __device__ CellMeta load_meta(const KdeArgs& a, int64_t c) {
 __device__ CellMeta meta_from_lane(const CellMeta& m, int i) {
   CellMeta r;
   r.n = __builtin_amdgcn_readlane(m.n, i);
+  r.w4 = __builtin_amdgcn_readlane(m.w4, i);
   r.mn = (int64_t)readlane64((uint64_t)m.mn, i);
   r.mx = (int64_t)readlane64((uint64_t)m.mx, i);
   r.off = (int64_t)readlane64((uint64_t)m.off, i);
@@ -1412,7 +1517,7 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
     const int64_t c = (int64_t)__builtin_amdgcn_readfirstlane(a.list2[cells - 1 - (int64_t)claim]);
     const CellMeta cm = load_meta(a, c);  // checked when the cell was listed: off >= 0, n >= kBlockMin
     const uint64_t n = cm.n;
-    const uint64_t* vals = a.bucket + cm.off;
+    const Durs vals = durs_of(a, cm);
     const int lo = grid64((uint64_t)cm.mn, L.th) >> sh;
     const int G = (grid64((uint64_t)cm.mx, L.th) >> sh) - lo + 1;
     if (G > Tier<1>::kWords) {
@@ -1427,8 +1532,7 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
     bool out_of_range = false;
     for (uint64_t i0 = tid; i0 < n; i0 += kBlockDepth * kBlockThreads) {
       uint64_t v[kBlockDepth];
-#pragma unroll
-      for (int u = 0; u < kBlockDepth; ++u) v[u] = i0 + u * kBlockThreads < n ? vals[i0 + u * kBlockThreads] : 0ull;
+      vals.get(i0, kBlockThreads, n, v, 0ull);
 #pragma unroll
       for (int u = 0; u < kBlockDepth; ++u) {
         if (i0 + u * kBlockThreads >= n) break;
@@ -1510,8 +1614,7 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
       };
       for (uint64_t i0 = tid; i0 < n; i0 += kBlockDepth * kBlockThreads) {
         uint64_t v[kBlockDepth];
-#pragma unroll
-        for (int u = 0; u < kBlockDepth; ++u) v[u] = i0 + u * kBlockThreads < n ? vals[i0 + u * kBlockThreads] : 0ull;
+        vals.get(i0, kBlockThreads, n, v, 0ull);
 #pragma unroll
         for (int u = 0; u < kBlockDepth; ++u)
           if (i0 + u * kBlockThreads < n) consider(v[u]);
@@ -1665,7 +1768,7 @@ template <int GC>
 __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const CellMeta& cm) {
   const int l = lane_id();
   const uint32_t n = cm.n;
-  const uint64_t* vals = a.bucket + cm.off;
+  const Durs vals = durs_of(a, cm);
   const int sh = 6 - a.sub_bits;
   const int lo = grid64((uint64_t)cm.mn, L.th) >> sh;
   const int G = (grid64((uint64_t)cm.mx, L.th) >> sh) - lo + 1;
@@ -1676,8 +1779,7 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
   bool out_of_range = false;
   for (uint32_t i0 = 0; i0 < n; i0 += 8) {
     uint64_t d[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) d[u] = i0 + u < n ? vals[i0 + u] : 0ull;
+    vals.get(i0, 1, n, d, 0ull);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if (i0 + u >= n) break;
@@ -1832,8 +1934,7 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
       uint32_t got0 = 0, got1 = same ? k[1] : 0u;
       for (uint32_t i0 = 0; i0 < n && (got0 < k[0] || got1 < k[1]); i0 += 8) {
         uint64_t d[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) d[u] = i0 + u < n ? vals[i0 + u] : ~0ull;
+        vals.get(i0, 1, n, d, ~0ull);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           if (d[u] >= lb[0] && d[u] < ub[0] && got0 < k[0]) L.w[got0++][l] = (uint32_t)(d[u] - lb[0]);
@@ -1859,8 +1960,7 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
         uint32_t got = 0;
         for (uint32_t i0 = 0; i0 < n && got < k[t2]; i0 += 8) {
           uint64_t d[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) d[u] = i0 + u < n ? vals[i0 + u] : ~0ull;
+          vals.get(i0, 1, n, d, ~0ull);
 #pragma unroll
           for (int u = 0; u < 8; ++u) {
             if (d[u] >= lb[t2] && d[u] < ub[t2] && got < k[t2]) {
@@ -2175,9 +2275,9 @@ size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
-size_t kde_workspace_bytes(int64_t n_events, int64_t cells) {
+size_t kde_workspace_bytes(int64_t n_events, int64_t n_seg, int64_t cells) {
   return 256 + al256((size_t)n_events * 8) + 3 * al256((size_t)cells * 4) + al256((size_t)cells * 2) +
-         al256((size_t)2 * kClasses * 4);
+         al256((size_t)2 * kClasses * 4) + al256((size_t)n_seg);
 }
 
 hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
@@ -2222,6 +2322,8 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   a.lane_key = reinterpret_cast<uint16_t*>(ws + off);
   off += al256((size_t)cells * 2);
   a.lane_cls = reinterpret_cast<uint32_t*>(ws + off);
+  off += al256((size_t)2 * kClasses * 4);
+  a.seg_w4 = reinterpret_cast<uint8_t*>(ws + off);
   const uint32_t* th = thresholds();
   for (int t = 0; t < 64; ++t) a.theta[t] = th[t];
 

@@ -45,11 +45,11 @@ def test_workspace_sizes():
     assert pa.lib().argus_iter_windows_workspace(10, 10) == 0
     e = A.Events(0, 0, 0, 0, 0, 0, 1, 1, 1, 1)
     assert pa.lib().argus_summarize_workspace(ctypes.byref(e)) == 256
-    # 256 fixed + 8 B per event + 3 x 4 B + 2 B per cell + 8 KB of class counters,
-    # each part 256-byte aligned
+    # 256 fixed + 8 B per event + 3 x 4 B + 2 B per cell + 8 KB of class counters
+    # + 1 B per rank-step (record width), each part 256-byte aligned
     assert pa.kde_workspace_bytes(4_096_000_000, 10240, 1, 2048) == (
-        256 + 4_096_000_000 * 8 + 3 * 10240 * 2048 * 4 + 10240 * 2048 * 2 + 8192)
-    assert pa.kde_workspace_bytes(10, 1, 1, 3) == 256 + 256 + 3 * 256 + 256 + 8192
+        256 + 4_096_000_000 * 8 + 3 * 10240 * 2048 * 4 + 10240 * 2048 * 2 + 8192 + 10240)
+    assert pa.kde_workspace_bytes(10, 1, 1, 3) == 256 + 256 + 3 * 256 + 256 + 8192 + 256
 
 
 @pytest.mark.parametrize("mutate", [

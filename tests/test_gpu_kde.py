@@ -6,8 +6,9 @@ Cases: the seeded tiny and medium traces (multimodal kernels), parameter
 variants, ragged / corrupted / malformed segments, hand-built groups that
 exercise every filter rule and both LDS paths (cells whose grid, kernel or
 valley list do not fit the fast path are finished by the large-LDS path),
-summaries that do not match the events, and full-size workloads (sampled
-segments checked against the oracle).
+summaries that do not match the events, segments of 4-byte and 8-byte
+bucket records in one call, and full-size workloads (sampled segments checked
+against the oracle).
 """
 import gc
 
@@ -244,6 +245,62 @@ def test_kde_summary_mismatch_in_large_cells():
     assert nc[0] == 0 and nc[2] == 0
     keep = np.array([1, 3])
     P.assert_kde_equal(k, {f: np.asarray(o[f])[keep] for f in P.KDE_FIELDS}, "large mismatch", rows=keep)
+
+
+def _segments_to_events(segs, K, NS, seed=0):
+    """Several segments in order; segs[g] is a list of duration arrays, array i
+    of a segment -> kernel id i."""
+    parts = [_groups_to_events(groups, K, NS, seed + g) for g, groups in enumerate(segs)]
+    ev = {f: np.concatenate([q[f] for q in parts]) for f in ("kernel_id", "stream", "start_ns", "end_ns")}
+    ev["seg_off"] = np.concatenate([[0], np.cumsum([len(q["kernel_id"]) for q in parts])]).astype(np.int64)
+    return ev
+
+
+def _record_widths(k, n_events, n_seg, cells):
+    """Per-segment record width flags from the workspace (its layout, each part
+    256-byte aligned: 256 B of counters, 8 B per event, 3 x 4 B and 2 B per
+    cell, 8 KiB of class counters, then one byte per segment)."""
+    al = lambda n: (n + 255) // 256 * 256  # noqa: E731
+    off = 256 + al(8 * n_events) + 3 * al(4 * cells) + al(2 * cells) + al(8192)
+    return k["_workspace"][off:off + n_seg].cpu().numpy()
+
+
+def test_kde_record_widths_mixed():
+    _announce("kde segments of 4-byte and 8-byte duration records in one call")
+    rng = np.random.default_rng(21)
+
+    def cells(top):
+        # cells for every tier (60 to 40,000 durations); the last one's largest
+        # duration is top
+        gs = [np.exp(rng.normal(np.log(c), 0.2, n)).astype(np.uint64)
+              for c, n in ((3e4, 60), (9e4, 250), (2e5, 1500), (5e5, 6000), (1e6, 40_000))]
+        body = np.minimum(np.exp(rng.normal(np.log(1e9), 0.4, 500)), top - 1).astype(np.uint64)
+        gs.append(np.concatenate([body, np.array([top], np.uint64)]))
+        return gs
+
+    # 4-byte records need every present maximum below 2^31
+    tops = [2**31 - 1, 2**31, 2**31 - 1, 5 * 10**9, 2**31 - 1, 2**32]
+    R, S, K, NS = 3, 2, 8, 3
+    ev = _segments_to_events([cells(t) for t in tops], K, NS)
+    n = len(ev["kernel_id"])
+    k, o = _both(ev, R, S, K, NS, "mixed widths")
+    assert list(_record_widths(k, n, R * S, R * S * K)) == [1, 0, 1, 0, 1, 0]
+    assert (o["n_clusters"][np.arange(R * S) * K + 5] >= 1).all()
+
+    # summaries that understate a maximum: segment 5 now looks 4-byte, its
+    # durations from 2^31 up (the largest, 2^32, saturated) lie above the
+    # stated maximum's octave, and only that cell is reported
+    ev_d = _dev(ev)
+    s = pa.summarize(ev_d, R, S, K, NS)
+    bad = 5 * K + 5
+    s["max_ns"][bad] = 2**31 - 1
+    k2 = pa.kde(ev_d, s, R, S, K, NS)
+    torch.cuda.synchronize()
+    assert int(k2["dev_status"].item()) == pa.argus.DEV_KDE_SUMMARY
+    assert list(_record_widths(k2, n, R * S, R * S * K)) == [1, 0, 1, 0, 1, 1]
+    assert int(k2["n_clusters"][bad].item()) == 0
+    keep = np.setdiff1d(np.arange(R * S * K), [bad])
+    P.assert_kde_equal(k2, {f: np.asarray(o[f])[keep] for f in P.KDE_FIELDS}, "understated maximum", rows=keep)
 
 
 @pytest.mark.parametrize("name,n_check", [("production", 96), ("cluster", 48), ("skew", 48)])
