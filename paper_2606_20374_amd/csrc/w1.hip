@@ -205,11 +205,16 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
     uint32_t nc;
     uint64_t tot;
     if (cell_state(a, c, nc, tot) <= 0) continue;
-    double mu[kMaxC], den[kMaxC], isg[kMaxC], wt[kMaxC];
+    double lnlo, du;
+    grid_of(a, sk, lnlo, du);
+    // per cluster: the table coordinate sx = kPhiSteps (z + kPhiZ) of grid
+    // point g is sx0 + g dsx (its rounding differs from the direct form's by
+    // far less than the band below allows for)
+    double mu[kMaxC], den[kMaxC], wt[kMaxC], sx0[kMaxC], dsx[kMaxC];
     bool spread[kMaxC];
 #pragma unroll
     for (int cl = 0; cl < kMaxC; ++cl) {
-      mu[cl] = den[cl] = isg[cl] = wt[cl] = 0.0;
+      mu[cl] = den[cl] = wt[cl] = sx0[cl] = dsx[cl] = 0.0;
       spread[cl] = false;
       if ((uint32_t)cl >= nc) continue;
       const int64_t p = a.p50[c * kMaxC + cl], t = a.p99[c * kMaxC + cl];
@@ -220,17 +225,18 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
       const double sigma = (log(y) - mu[cl]) / kZ99;
       spread[cl] = sigma > 0.0;
       den[cl] = sigma * kSqrt2;
-      isg[cl] = spread[cl] ? 1.0 / sigma : 0.0;
+      const double isg = spread[cl] ? 1.0 / sigma : 0.0;
+      sx0[cl] = fma((lnlo - mu[cl]) * isg, (double)kPhiSteps, kPhiZ * (double)kPhiSteps);
+      dsx[cl] = du * isg * (double)kPhiSteps;
       wt[cl] = (double)a.cnt[c * kMaxC + cl] / (double)tot;
     }
-    double lnlo, du;
-    grid_of(a, sk, lnlo, du);
     uint16_t* out = a.q + (sk * a.G) * a.R + r;
     for (int gb = 0; gb < a.G; gb += 64) {
       const int gn = a.G - gb < 64 ? a.G - gb : 64;
       uint64_t unsure = 0;
       for (int gi = 0; gi < gn; ++gi) {
-        const double u = lnlo + (double)(gb + gi) * du;
+        const double gd = (double)(gb + gi);
+        const double u = lnlo + gd * du;
         double F = 0.0;
 #pragma unroll
         for (int cl = 0; cl < kMaxC; ++cl) {
@@ -239,15 +245,14 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
           if (!spread[cl]) {
             ph = u >= mu[cl] ? 1.0 : 0.0;
           } else {
-            const double z = (u - mu[cl]) * isg[cl];
-            if (z <= -kPhiZ) {
+            const double sx = fma(gd, dsx[cl], sx0[cl]);
+            if (sx <= 0.0) {
               ph = 0.0;
-            } else if (z >= kPhiZ) {
+            } else if (sx >= (double)kPhiN) {
               ph = 1.0;
             } else {
               // fused multiply-adds: their rounding differs from separate
               // operations by far less than the band below allows for
-              const double sx = fma(z, (double)kPhiSteps, kPhiZ * (double)kPhiSteps);
               int i = (int)sx;
               i = i < kPhiN - 1 ? i : kPhiN - 1;
               const double t = sx - (double)i;
@@ -257,10 +262,14 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
           }
           F = fma(wt[cl], ph, F);
         }
-        const double v = F * 65536.0;
-        const uint32_t qa = quant16(v - kBand), qb = quant16(v + kBand);
-        if (qa == qb) out[(int64_t)(gb + gi) * a.R] = (uint16_t)qa;
-        else unsure |= 1ull << gi;
+        // quant16(v - kBand) == quant16(v + kBand), decided from one floor:
+        // both ends below 1 (q = 0), both at or above 65535, or one integer part
+        const double v = F * 65536.0, vlo = v - kBand, vhi = v + kBand;
+        const double fh = floor(vhi);
+        if (vhi < 1.0 || vlo >= fh || vlo >= 65535.0)
+          out[(int64_t)(gb + gi) * a.R] = (uint16_t)(vhi < 1.0 ? 0u : (fh >= 65535.0 ? 65535u : (uint32_t)fh));
+        else
+          unsure |= 1ull << gi;
       }
       // grid points near a quantisation step: the defining erfc form
       while (unsure) {
