@@ -234,8 +234,9 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
     for (int gb = 0; gb < a.G; gb += 64) {
       const int gn = a.G - gb < 64 ? a.G - gb : 64;
       uint64_t unsure = 0;
-      for (int gi = 0; gi < gn; ++gi) {
-        const double gd = (double)(gb + gi);
+      // the mixture at grid point g: two points per step, so that the two
+      // dependent chains of table evaluations overlap
+      auto mix = [&](double gd) -> double {
         const double u = lnlo + gd * du;
         double F = 0.0;
 #pragma unroll
@@ -262,15 +263,25 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
           }
           F = fma(wt[cl], ph, F);
         }
-        // quant16(v - kBand) == quant16(v + kBand), decided from one floor:
-        // both ends below 1 (q = 0), both at or above 65535, or one integer part
+        return F;
+      };
+      // quant16(v - kBand) == quant16(v + kBand), decided from one floor:
+      // both ends below 1 (q = 0), both at or above 65535, or one integer part
+      auto emit = [&](int gi, double F) {
         const double v = F * 65536.0, vlo = v - kBand, vhi = v + kBand;
         const double fh = floor(vhi);
         if (vhi < 1.0 || vlo >= fh || vlo >= 65535.0)
           out[(int64_t)(gb + gi) * a.R] = (uint16_t)(vhi < 1.0 ? 0u : (fh >= 65535.0 ? 65535u : (uint32_t)fh));
         else
           unsure |= 1ull << gi;
+      };
+      int gi = 0;
+      for (; gi + 1 < gn; gi += 2) {
+        const double F0 = mix((double)(gb + gi)), F1 = mix((double)(gb + gi + 1));
+        emit(gi, F0);
+        emit(gi + 1, F1);
       }
+      if (gi < gn) emit(gi, mix((double)(gb + gi)));
       // grid points near a quantisation step: the defining erfc form
       while (unsure) {
         const int gi = __builtin_ctzll(unsure);
