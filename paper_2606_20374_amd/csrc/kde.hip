@@ -1720,7 +1720,10 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
 // at the same step touch consecutive words. A lane that finds more valleys
 // than kLaneCand, or more durations in a target grid bin than kLaneList,
 // writes nothing and hands its cell to the wavefront tiers, like every cell
-// outside these limits.
+// outside these limits. The per-lane arrays are kept small (weights and
+// target-bin offsets in 16 bits where they fit) because the lane passes are
+// latency bound: every kilobyte of LDS per wavefront is resident wavefronts
+// per CU.
 constexpr int kLaneN = 255;     // durations per cell (counts fit in 8 bits, densities in 24)
 constexpr int kLaneG = 64;      // grid points per cell, first lane pass (over every cell)
 constexpr int kLaneGW = 256;    // grid points per cell, second lane pass (listed wide cells)
@@ -1732,7 +1735,15 @@ static_assert(2 * kLaneList <= kLaneT, "two target lists in the weight words");
 template <int GC>
 struct LaneLds {
   alignas(4) uint8_t cp[GC][kWave];  // grid counts, then inclusive prefix counts (8 bits: n <= 255)
-  uint32_t w[kLaneT][kWave];       // kernel weights; later the durations of one target bin (lo, hi words)
+  // kernel weights w(t) for 1 <= t < kLaneT (w(0) = 65536 is implicit; a cell
+  // whose w(1) needs 17 bits goes to the wavefront tiers); later the
+  // durations of a cluster's target bins as offsets from the bin start: two
+  // bins of 16-bit offsets, or one bin of 32-bit offsets
+  union {
+    uint16_t w[kLaneT][kWave];
+    uint16_t off16[2 * kLaneList][kWave];
+    uint32_t off32[kLaneList][kWave];
+  };
   uint32_t cand[kLaneCand][kWave]; // valleys: density << 8 | grid index
   uint32_t th[64];
 };
@@ -1821,21 +1832,27 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
       const uint32_t wt = kde_weight(t, H2);
       if (wt == 0) break;
       if (t == kLaneT) return false;  // kernel wider than the lane's weight table
-      L.w[t][l] = wt;
+      if (t > 0) {
+        if (wt > 0xFFFFu) return false;  // w(1) = 65536: a bandwidth far beyond the table's reach
+        L.w[t][l] = (uint16_t)wt;
+      }
       T = t;
     }
     uint32_t v = 0, pv = 0;
     int r0 = 0;
     for (int j = 0; j < G; ++j) {
       const int b0 = j - T > 0 ? j - T : 0, b1 = j + T < G - 1 ? j + T : G - 1;
-      // left of j the distance falls to 0, right of it it rises from 1: two
-      // loops walk the weight column by pointer (counts < 256, weights <= 2^16)
+      // left of j the distance falls to 1, right of it it rises from 1: two
+      // loops walk the weight column by pointer (counts < 256, weights
+      // < 2^16); j itself weighs w(0) = 65536
       uint32_t f = 0;
-      const uint32_t* wl = &L.w[j - b0][l];
+      const uint16_t* wl = &L.w[j - b0][l];
       const uint8_t* cl = &L.cp[b0][l];
 #pragma unroll 4
-      for (int b = b0; b <= j; ++b, wl -= kWave, cl += kWave) f += __umul24(*cl, *wl);
-      const uint32_t* wr = &L.w[1][l];
+      for (int b = b0; b < j; ++b, wl -= kWave, cl += kWave) f += __umul24(*cl, *wl);
+      f += (uint32_t)*cl << 16;
+      cl += kWave;
+      const uint16_t* wr = &L.w[1][l];
 #pragma unroll 4
       for (int b = j + 1; b <= b1; ++b, wr += kWave, cl += kWave) f += __umul24(*cl, *wr);
       if (j == 0) {
@@ -1903,9 +1920,10 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
   // 8. per cluster: count, then p50 / p99 as the element of the wanted rank
   // inside its grid bin, found among the bin's durations gathered in LDS. The
   // targets' ranks increase, so the bin search goes on from the last bin. A
-  // cluster's two bins are gathered in one pass over the durations, as 32-bit
-  // offsets from the bin start (16 words each), when both bins are narrower
-  // than 2^32 ns; otherwise one bin per pass as 64-bit values (32 words).
+  // cluster's two bins are gathered in one pass over the durations, as 16-bit
+  // offsets from the bin start, when both bins are at most 2^16 ns wide (bins
+  // of durations below about 6 ms); otherwise one bin per pass as 32-bit
+  // offsets, and bins wider than 2^32 ns hand the cell to the wavefront tiers.
   const int ncl = m + 1;
   uint32_t before = 0;
   int jc = 0;
@@ -1925,30 +1943,31 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
       rr[t2] = r - below;
       lb[t2] = grid64_lb((lo + jc) << sh, L.th);
       ub[t2] = grid64_lb((lo + jc + 1) << sh, L.th);
-      narrow = narrow && ub[t2] - lb[t2] <= (1ull << 32);
+      narrow = narrow && ub[t2] - lb[t2] <= (1ull << 16);
     }
     const bool same = lb[1] == lb[0];
     uint64_t pick[2] = {0, 0};
     if (narrow) {
-      // list t at words [16 t, 16 t + k[t]): offsets from lb[t]
+      // list t at entries [16 t, 16 t + k[t]): 16-bit offsets from lb[t]
       uint32_t got0 = 0, got1 = same ? k[1] : 0u;
       for (uint32_t i0 = 0; i0 < n && (got0 < k[0] || got1 < k[1]); i0 += 8) {
         uint64_t d[8];
         vals.get(i0, 1, n, d, ~0ull);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-          if (d[u] >= lb[0] && d[u] < ub[0] && got0 < k[0]) L.w[got0++][l] = (uint32_t)(d[u] - lb[0]);
-          if (!same && d[u] >= lb[1] && d[u] < ub[1] && got1 < k[1]) L.w[kLaneList + got1++][l] = (uint32_t)(d[u] - lb[1]);
+          if (d[u] >= lb[0] && d[u] < ub[0] && got0 < k[0]) L.off16[got0++][l] = (uint16_t)(d[u] - lb[0]);
+          if (!same && d[u] >= lb[1] && d[u] < ub[1] && got1 < k[1])
+            L.off16[kLaneList + got1++][l] = (uint16_t)(d[u] - lb[1]);
         }
       }
       for (int t2 = 0; t2 < 2; ++t2) {
         const int base = same ? 0 : t2 * kLaneList;
         uint32_t off = 0;
         for (uint32_t i = 0; i < k[t2]; ++i) {
-          const uint32_t e = L.w[base + i][l];
+          const uint32_t e = L.off16[base + i][l];
           uint32_t rank = 0;
           for (uint32_t x = 0; x < k[t2]; ++x) {
-            const uint32_t y = L.w[base + x][l];
+            const uint32_t y = L.off16[base + x][l];
             rank += (y < e || (y == e && x < i)) ? 1u : 0u;
           }
           if (rank == rr[t2]) off = e;
@@ -1957,28 +1976,26 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
       }
     } else {
       for (int t2 = 0; t2 < 2; ++t2) {
+        if (ub[t2] - lb[t2] > (1ull << 32)) return false;
         uint32_t got = 0;
         for (uint32_t i0 = 0; i0 < n && got < k[t2]; i0 += 8) {
           uint64_t d[8];
           vals.get(i0, 1, n, d, ~0ull);
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            if (d[u] >= lb[t2] && d[u] < ub[t2] && got < k[t2]) {
-              L.w[2 * got][l] = (uint32_t)d[u];
-              L.w[2 * got + 1][l] = (uint32_t)(d[u] >> 32);
-              ++got;
-            }
-          }
+          for (int u = 0; u < 8; ++u)
+            if (d[u] >= lb[t2] && d[u] < ub[t2] && got < k[t2]) L.off32[got++][l] = (uint32_t)(d[u] - lb[t2]);
         }
+        uint32_t off = 0;
         for (uint32_t i = 0; i < k[t2]; ++i) {
-          const uint64_t e = ((uint64_t)L.w[2 * i + 1][l] << 32) | L.w[2 * i][l];
+          const uint32_t e = L.off32[i][l];
           uint32_t rank = 0;
           for (uint32_t x = 0; x < k[t2]; ++x) {
-            const uint64_t y = ((uint64_t)L.w[2 * x + 1][l] << 32) | L.w[2 * x][l];
+            const uint32_t y = L.off32[x][l];
             rank += (y < e || (y == e && x < i)) ? 1u : 0u;
           }
-          if (rank == rr[t2]) pick[t2] = e;
+          if (rank == rr[t2]) off = e;
         }
+        pick[t2] = lb[t2] + off;
       }
     }
     for (int qq = 0; qq < kMaxC; ++qq) {
