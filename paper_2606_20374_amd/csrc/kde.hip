@@ -702,6 +702,10 @@ struct CellMeta {
   double pw;    // n^(-1/5) from the table (0 when n is outside it)
 };
 
+typedef unsigned v4u_a4 __attribute__((ext_vector_type(4), aligned(4)));
+typedef unsigned long long v2ul __attribute__((ext_vector_type(2)));
+typedef unsigned long long v2ul_a8 __attribute__((ext_vector_type(2), aligned(8)));
+
 // A cell's bucketed durations, records of 4 or 8 bytes. Reads take the
 // width's own loads (one branch per group of loads, uniform when the
 // wavefront works on one cell).
@@ -725,6 +729,28 @@ struct Durs {
       for (int u = 0; u < N; ++u) {
         const uint64_t i = i0 + (uint64_t)u * stride;
         v[u] = i < n ? q[i] : dflt;
+      }
+    }
+  }
+  // v[u] = record i0 + u (u < 8) where that is below n, else dflt: one lane's
+  // run of eight records in 16-byte loads. The loads may reach up to seven
+  // records past the cell; those bytes lie inside the workspace (a segment of
+  // 4-byte records fills half its area, and the bucket is followed by the
+  // cell-end array) and are discarded.
+  __device__ __forceinline__ void run8(uint32_t i0, uint32_t n, uint64_t (&v)[8], uint64_t dflt) const {
+    if (w4) {
+      const v4u_a4* q = reinterpret_cast<const v4u_a4*>(static_cast<const uint32_t*>(p) + i0);
+      const v4u x = q[0], y = q[1];
+      const uint32_t r[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = i0 + u < n ? (uint64_t)r[u] : dflt;
+    } else {
+      const v2ul_a8* q = reinterpret_cast<const v2ul_a8*>(static_cast<const uint64_t*>(p) + i0);
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const v2ul x = q[h];
+        v[2 * h] = i0 + 2 * h < n ? (uint64_t)x.x : dflt;
+        v[2 * h + 1] = i0 + 2 * h + 1 < n ? (uint64_t)x.y : dflt;
       }
     }
   }
@@ -1790,7 +1816,7 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
   bool out_of_range = false;
   for (uint32_t i0 = 0; i0 < n; i0 += 8) {
     uint64_t d[8];
-    vals.get(i0, 1, n, d, 0ull);
+    vals.run8(i0, n, d, 0ull);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if (i0 + u >= n) break;
@@ -1952,7 +1978,7 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
       uint32_t got0 = 0, got1 = same ? k[1] : 0u;
       for (uint32_t i0 = 0; i0 < n && (got0 < k[0] || got1 < k[1]); i0 += 8) {
         uint64_t d[8];
-        vals.get(i0, 1, n, d, ~0ull);
+        vals.run8(i0, n, d, ~0ull);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           if (d[u] >= lb[0] && d[u] < ub[0] && got0 < k[0]) L.off16[got0++][l] = (uint16_t)(d[u] - lb[0]);
@@ -1980,7 +2006,7 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
         uint32_t got = 0;
         for (uint32_t i0 = 0; i0 < n && got < k[t2]; i0 += 8) {
           uint64_t d[8];
-          vals.get(i0, 1, n, d, ~0ull);
+          vals.run8(i0, n, d, ~0ull);
 #pragma unroll
           for (int u = 0; u < 8; ++u)
             if (d[u] >= lb[t2] && d[u] < ub[t2] && got < k[t2]) L.off32[got++][l] = (uint32_t)(d[u] - lb[t2]);
