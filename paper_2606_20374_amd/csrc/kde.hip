@@ -1623,27 +1623,27 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
       for (int i = tid; i < kMaxT * kSelRegion; i += kBlockThreads) L.buf[i] = 0;
       if (tid < kMaxT) L.tcnt[tid] = 0;
       __syncthreads();
-      auto consider = [&](uint64_t v) {
-#pragma unroll
-        for (int t = 0; t < kMaxT; ++t) {
-          const uint64_t u = v - tlo[t];
-          if (u < twd[t]) {
-            if (tsh[t] < 0) {
-              const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
-              if (slot < (uint32_t)kSelCap)
-                reinterpret_cast<uint64_t*>(L.buf + t * kSelRegion)[slot] = v;
-            } else {
-              atomicAdd(&L.buf[t * kSelRegion + (int)(u >> tsh[t])], 1u);
-            }
-          }
-        }
-      };
+      // live targets outer (a uniform test each), the loaded durations inner
       for (uint64_t i0 = tid; i0 < n; i0 += kBlockDepth * kBlockThreads) {
         uint64_t v[kBlockDepth];
         vals.get(i0, kBlockThreads, n, v, 0ull);
 #pragma unroll
-        for (int u = 0; u < kBlockDepth; ++u)
-          if (i0 + u * kBlockThreads < n) consider(v[u]);
+        for (int t = 0; t < kMaxT; ++t) {
+          if (!((live >> t) & 1u)) continue;
+#pragma unroll
+          for (int k = 0; k < kBlockDepth; ++k) {
+            const uint64_t u = v[k] - tlo[t];
+            if (i0 + k * kBlockThreads < n && u < twd[t]) {
+              if (tsh[t] < 0) {
+                const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
+                if (slot < (uint32_t)kSelCap)
+                  reinterpret_cast<uint64_t*>(L.buf + t * kSelRegion)[slot] = v[k];
+              } else {
+                atomicAdd(&L.buf[t * kSelRegion + (int)(u >> tsh[t])], 1u);
+              }
+            }
+          }
+        }
       }
       __syncthreads();
       // wavefront wv resolves targets wv, wv + kBlockWaves, ...
