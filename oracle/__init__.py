@@ -62,6 +62,7 @@ def lib():
         L.orc_kde_weights_many.argtypes = [V, V, I32, V]
         L.orc_kde_root5_many.argtypes = [V, I64, V]
         L.orc_kde_bw_q8_many.argtypes = [V, V, I64, V]
+        L.orc_kde_bin_many.argtypes = [V, I64, V]
         L.orc_kde.argtypes = [I64, I32, I32, I64] + [V] * 5 + [I32] * 4 + [V] * 5
         L.orc_kde.restype = I64
         L.orc_w1.argtypes = [I32, I32, I32] + [V] * 4 + [I32] * 3 + [V] * 9
@@ -180,6 +181,14 @@ def kde_thresholds() -> np.ndarray:
 
 def kde_bin(d: int, sub_bits: int = 6) -> int:
     return lib().orc_kde_bin(d, sub_bits)
+
+
+def kde_bin_many(d: np.ndarray) -> np.ndarray:
+    """kde_bin(d, 6) for an array of durations (uint64)."""
+    d = np.ascontiguousarray(d, dtype=np.uint64)
+    out = np.empty(d.size, np.int32)
+    lib().orc_kde_bin_many(_p(d), d.size, _p(out))
+    return out
 
 
 def _kde_params(params: dict) -> dict:

@@ -96,6 +96,13 @@ int orc_kde_bin(uint64_t d, int32_t sub_bits) {
   return kde_bin64(d, th) >> (6 - sub_bits);
 }
 
+/* orc_kde_bin at full resolution (64 grid points per octave) for m durations. */
+void orc_kde_bin_many(const uint64_t* d, int64_t m, int32_t* out) {
+  uint32_t th[64];
+  kde_thresholds(th);
+  for (int64_t i = 0; i < m; i++) out[i] = kde_bin64(d[i], th);
+}
+
 static int cmp_u64(const void* a, const void* b) {
   uint64_t x = *(const uint64_t*)a, y = *(const uint64_t*)b;
   return x < y ? -1 : x > y;

@@ -118,18 +118,8 @@ struct KdeArgs {
 
 // ----------------------------------------------------------------- helpers
 
-// floor(64 log2 d') with d' the 24 leading significant bits of d: a hardware
-// log2 estimate, corrected against the exact mantissa thresholds.
-__device__ __forceinline__ int grid64(uint64_t d, const uint32_t* th) {
-  if (d < 2) return 0;
-  const int e = 63 - __builtin_clzll(d);
-  const uint32_t m = e >= 23 ? (uint32_t)(d >> (e - 23)) : (uint32_t)(d << (23 - e));
-  int t = (int)((__log2f((float)m) - 23.0f) * 64.0f);
-  t = t < 0 ? 0 : (t > 63 ? 63 : t);
-  while (t > 0 && m < th[t]) --t;
-  while (t < 63 && m >= th[t + 1]) ++t;
-  return e * 64 + t;
-}
+// the grid index of a duration (kde_math.h)
+__device__ __forceinline__ int grid64(uint64_t d, const uint32_t* th) { return kde_grid64(d, th); }
 
 // Smallest duration whose 64-per-octave grid value is >= b.
 __device__ __forceinline__ uint64_t grid64_lb(int b, const uint32_t* th) {
@@ -2236,45 +2226,6 @@ __global__ __launch_bounds__(kWave) void kde_lane_kernel(KdeArgs a) {
 
 // ---------------------------------------------------------------- host side
 
-// Exact thresholds ceil(2^(23 + t/64)): the smallest m with
-// floor(log2(m^64)) >= 1472 + t, found by bisection with big-integer powers.
-int bitlen_pow64(uint32_t m) {
-  std::vector<uint32_t> x{m};
-  for (int s = 0; s < 6; ++s) {
-    std::vector<uint32_t> r(2 * x.size(), 0u);
-    for (size_t i = 0; i < x.size(); ++i) {
-      uint64_t carry = 0;
-      for (size_t j = 0; j < x.size(); ++j) {
-        const uint64_t t = (uint64_t)x[i] * x[j] + r[i + j] + carry;
-        r[i + j] = (uint32_t)t;
-        carry = t >> 32;
-      }
-      r[i + x.size()] = (uint32_t)carry;
-    }
-    while (r.size() > 1 && r.back() == 0) r.pop_back();
-    x.swap(r);
-  }
-  return (int)(x.size() - 1) * 32 + (32 - __builtin_clz(x.back()));
-}
-
-const uint32_t* thresholds() {
-  static uint32_t th[64];
-  static std::once_flag once;
-  std::call_once(once, [] {
-    th[0] = 1u << 23;
-    for (int t = 1; t < 64; ++t) {
-      uint32_t lo = 1u << 23, hi = (1u << 24) - 1;
-      while (lo < hi) {
-        const uint32_t mid = lo + (hi - lo) / 2;
-        if (bitlen_pow64(mid) - 1 >= 1472 + t) hi = mid;
-        else lo = mid + 1;
-      }
-      th[t] = lo;
-    }
-  });
-  return th;
-}
-
 __global__ void kde_pow_table_kernel() {
   const int n = blockIdx.x * blockDim.x + threadIdx.x;
   if (n < kPowTab) g_kde_pow[n] = n > 0 ? kde_pw((uint64_t)n) : 0.0;
@@ -2367,7 +2318,7 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   a.lane_cls = reinterpret_cast<uint32_t*>(ws + off);
   off += al256((size_t)2 * kClasses * 4);
   a.seg_w4 = reinterpret_cast<uint8_t*>(ws + off);
-  const uint32_t* th = thresholds();
+  const uint32_t* th = kde_thresholds();
   for (int t = 0; t < 64; ++t) a.theta[t] = th[t];
 
   hipLaunchKernelGGL(kde_clear_kernel, dim3(1), dim3(256), 0, st, a.counters, a.lane_cls, a.dev_status);

@@ -1,15 +1,83 @@
-// The floating-point steps of the KDE clustering definition (section 5.2,
-// Eq. 1: Gaussian kernel, bandwidth 1.06 sigma n^(-1/5)), one copy for every
-// cell tier. The integer outputs follow from these results exactly. n^(-1/5)
-// is decided exactly (no math library involved); sqrt is correctly rounded;
-// exp enters the weights, and a GPU test evaluates these same functions over
-// their whole reachable domain against the host C library's.
+// The log grid and the floating-point steps of the KDE clustering definition
+// (section 5.2, Eq. 1: log-duration grid, Gaussian kernel, bandwidth 1.06
+// sigma n^(-1/5)), one copy for every cell tier. The integer outputs follow
+// from these results exactly. The grid index and n^(-1/5) are decided
+// exactly (no math library involved); sqrt is correctly rounded; exp enters
+// the weights, and a GPU test evaluates these same functions over their
+// whole reachable domain against the oracle and the host C library.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+#include <vector>
+
 namespace argus {
+
+// ------------------------------------------------------------ the log grid
+// Bit length of m^64, exactly (big-integer squaring, six times).
+inline int kde_bitlen_pow64(uint32_t m) {
+  std::vector<uint32_t> x{m};
+  for (int s = 0; s < 6; ++s) {
+    std::vector<uint32_t> r(2 * x.size(), 0u);
+    for (size_t i = 0; i < x.size(); ++i) {
+      uint64_t carry = 0;
+      for (size_t j = 0; j < x.size(); ++j) {
+        const uint64_t t = (uint64_t)x[i] * x[j] + r[i + j] + carry;
+        r[i + j] = (uint32_t)t;
+        carry = t >> 32;
+      }
+      r[i + x.size()] = (uint32_t)carry;
+    }
+    while (r.size() > 1 && r.back() == 0) r.pop_back();
+    x.swap(r);
+  }
+  return 32 * (int)(x.size() - 1) + (32 - __builtin_clz(x.back()));
+}
+
+// The 64 mantissa thresholds ceil(2^(23 + t/64)) of the grid (host, computed
+// once): the smallest m with floor(log2(m^64)) >= 1472 + t, by bisection.
+inline const uint32_t* kde_thresholds() {
+  static uint32_t th[64];
+  static std::once_flag once;
+  std::call_once(once, [] {
+    th[0] = 1u << 23;
+    for (int t = 1; t < 64; ++t) {
+      uint32_t lo = 1u << 23, hi = (1u << 24) - 1;
+      while (lo < hi) {
+        const uint32_t mid = lo + (hi - lo) / 2;
+        if (kde_bitlen_pow64(mid) - 1 >= 1472 + t) hi = mid;
+        else lo = mid + 1;
+      }
+      th[t] = lo;
+    }
+  });
+  return th;
+}
+
+// Grid index floor(64 log2 d') of a duration d >= 2, with d' its 24 leading
+// significant bits (exact below 2^24 ns); 0 for d < 2. A hardware log2
+// estimate is checked against the exact thresholds th (kde_thresholds): the
+// estimate's bracket [th[t], th[t + 1]) is read at once, a result equal to
+// the estimate is proved by those two comparisons, and only an estimate off
+// by a step (a mantissa next to a threshold) walks the table to the exact
+// index.
+__device__ __forceinline__ int kde_grid64(uint64_t d, const uint32_t* th) {
+  if (d < 2) return 0;
+  const int e = 63 - __builtin_clzll(d);
+  const uint32_t m = e >= 23 ? (uint32_t)(d >> (e - 23)) : (uint32_t)(d << (23 - e));
+  int t0 = (int)((__log2f((float)m) - 23.0f) * 64.0f);
+  t0 = t0 < 0 ? 0 : (t0 > 63 ? 63 : t0);
+  const uint32_t a0 = th[t0], a1 = th[t0 < 63 ? t0 + 1 : 63];
+  int t = t0 - 1 + (m >= a0 ? 1 : 0) + (t0 < 63 && m >= a1 ? 1 : 0);
+  if (t != t0) {
+    t = t < 0 ? 0 : t;
+    while (t > 0 && m < th[t]) --t;
+    while (t < 63 && m >= th[t + 1]) ++t;
+  }
+  return e * 64 + t;
+}
 
 // Sign of c^5 n - 2^e, exactly (c < 2^55, n < 2^33, so the product has at
 // most 308 bits: six 64-bit limbs).

@@ -1,6 +1,7 @@
-// Test probe (not part of libargus): evaluates the KDE's floating-point steps
-// through the very functions the cell kernels call (kde_math.h) on given
-// arguments, so a GPU test can compare them with the host C library's.
+// Test probe (not part of libargus): evaluates the KDE's grid index and
+// floating-point steps through the very functions the cell kernels call
+// (kde_math.h) on given arguments, so a GPU test can compare them with the
+// oracle's and the host C library's.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -31,6 +32,20 @@ __global__ void bw_kernel(const double* var, const int64_t* n, const double* pw_
   out[i] = argus::kde_bw_q8(var[i], pw);
 }
 
+// Grid index of each duration, with the thresholds in LDS as the cell
+// kernels hold them.
+struct Thresholds {
+  uint32_t th[64];
+};
+
+__global__ void grid_kernel(const uint64_t* d, int64_t m, Thresholds t, int32_t* out) {
+  __shared__ uint32_t th[64];
+  if (threadIdx.x < 64) th[threadIdx.x] = t.th[threadIdx.x];
+  __syncthreads();
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < m) out[i] = argus::kde_grid64(d[i], th);
+}
+
 int status(hipError_t e) { return e == hipSuccess ? 0 : -3; }
 
 }  // namespace
@@ -46,6 +61,15 @@ int probe_kde_weights(const int64_t* H, const int64_t* off, int32_t nH, uint32_t
 int probe_kde_root5(const int64_t* n, int64_t m, double* out, void* stream) {
   if (m <= 0) return 0;
   hipLaunchKernelGGL(pow_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, (hipStream_t)stream, n, m, out);
+  return status(hipGetLastError());
+}
+
+int probe_kde_grid(const uint64_t* d, int64_t m, int32_t* out, void* stream) {
+  if (m <= 0) return 0;
+  Thresholds t;
+  const uint32_t* th = argus::kde_thresholds();
+  for (int i = 0; i < 64; ++i) t.th[i] = th[i];
+  hipLaunchKernelGGL(grid_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, (hipStream_t)stream, d, m, t, out);
   return status(hipGetLastError());
 }
 

@@ -16,6 +16,10 @@ they must equal the oracle's bit for bit:
 * n^(-1/5): every n from 1 to 2^22 and 2^20 random n up to 2^33;
 * H: 2^22 random (var, n) pairs, var from exact integer moment quotients as
   the kernels form them and log-uniform doubles.
+The grid index of a duration (an integer result that a hardware log2
+estimate only starts) must equal the oracle's exact one for every duration
+below 2^20, every threshold of every octave and its two neighbours, and 2^22
+log-uniform random durations.
 The full-size KDE parity tests compare the bandwidth and clusters of every
 cell of the benchmarked workloads on top of this.
 """
@@ -43,6 +47,7 @@ def _probe():
     L.probe_kde_weights.argtypes = [V, V, ctypes.c_int32, V, V]
     L.probe_kde_root5.argtypes = [V, ctypes.c_int64, V, V]
     L.probe_kde_bw_q8.argtypes = [V, V, V, ctypes.c_int64, V, V]
+    L.probe_kde_grid.argtypes = [V, ctypes.c_int64, V, V]
     return L
 
 
@@ -113,3 +118,30 @@ def test_bandwidth_matches_the_host():
     want = oracle.kde_bw_q8_many(var, n)
     bad = np.nonzero(got != want)[0]
     assert bad.size == 0, (bad.size, var[bad[:5]], n[bad[:5]], got[bad[:5]], want[bad[:5]])
+
+
+def test_grid_index_matches_the_oracle():
+    print("\n[gpu-case] kde grid index: d < 2^20, every threshold of every octave +-1, 2^22 random", flush=True)
+    th = oracle.kde_thresholds().astype(np.uint64)
+    parts = [np.arange(1 << 20, dtype=np.uint64)]
+    # every threshold of every octave and its neighbours: for octaves below
+    # 2^23 the threshold's duration is the smallest d whose shifted mantissa
+    # reaches it
+    for e in range(20, 63):
+        if e >= 23:
+            b = th << np.uint64(e - 23)
+        else:
+            sh = np.uint64(23 - e)
+            b = (th + (np.uint64(1) << sh) - np.uint64(1)) >> sh
+        parts += [b - np.uint64(1), b, b + np.uint64(1)]
+    rng = np.random.default_rng(17)
+    parts.append(np.exp2(rng.uniform(1.0, 62.99, 1 << 22)).astype(np.uint64))
+    parts.append(np.array([2**63 - 1, 2**63 - 2, 2**62, 2**62 - 1], np.uint64))
+    d = np.unique(np.concatenate(parts))
+    want = oracle.kde_bin_many(d)
+    out = torch.empty(d.size, dtype=torch.int32, device=DEV)
+    assert _probe().probe_kde_grid(_dev(d.view(np.int64)).data_ptr(), d.size, out.data_ptr(), _stream()) == 0
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, (bad.size, d[bad[:5]], got[bad[:5]], want[bad[:5]])
