@@ -497,9 +497,9 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
 #pragma unroll
     for (int j = 0; j < V; ++j) {
       if (present(j)) {
-        const int64_t clt = (cl2[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
-        const int64_t S =
-            (int64_t)(qt[j] & 0xFFFFu) * (2 * clt - (int64_t)n) + (int64_t)T - 2 * (int64_t)fine[clt];
+        // S <= (n - 1) 65535 < 2^32: the sum is exact modulo 2^32
+        const uint32_t clt = (cl2[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
+        const uint32_t S = (qt[j] & 0xFFFFu) * (2u * clt - n) + T - 2u * fine[clt];
         acc[j] += wg * (double)S;
       }
       qt[j] = (qn2[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
