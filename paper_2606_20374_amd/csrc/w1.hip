@@ -12,9 +12,10 @@
 //   w1_cdf      one lane per rank (64 ranks of one kernel id per wavefront,
 //               eight kernel ids per wavefront): the count-weighted lognormal
 //               mixture of Eq. 2 at every grid point, quantised to 16 bits,
-//               into a [S][K][G][R] workspace (ranks contiguous, so the
-//               writes and the next kernel's reads are coalesced). Phi comes
-//               from a cubic Hermite table (error below 2e-10); a grid point
+//               into a [S][K][G][R'] workspace (R' = R rounded up to even;
+//               ranks contiguous, so the writes and the next kernel's reads
+//               are coalesced). Phi comes from a cubic Hermite table (error
+//               below 2e-10); a grid point
 //               whose quantised value is not settled by that bound (within
 //               1e-4 of a step of 2^-16) is recomputed with erfc in double,
 //               the defining formula, so every output equals the erfc form.
@@ -71,8 +72,12 @@ struct W1Args {
   const int64_t* p99;
   int32_t R, S, K, G, min_ranks, alpha_pm;
   argus_w1_out_t o;
-  uint16_t* q;  // workspace [S][K][G][R]
+  uint16_t* q;  // workspace [S][K][G][R rounded up to even]
 };
+
+// Workspace row stride: the rank count rounded up to even, so that the
+// values of ranks 2p and 2p + 1 share one aligned 32-bit word.
+__device__ __forceinline__ int64_t row_stride(const W1Args& a) { return (int64_t)(a.R + (a.R & 1)); }
 
 __device__ __forceinline__ int64_t cell_of(const W1Args& a, int r, int s, int k) {
   return ((int64_t)r * a.S + s) * a.K + k;
@@ -230,7 +235,8 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
       dsx[cl] = du * isg * (double)kPhiSteps;
       wt[cl] = (double)a.cnt[c * kMaxC + cl] / (double)tot;
     }
-    uint16_t* out = a.q + (sk * a.G) * a.R + r;
+    const int64_t rs = row_stride(a);
+    uint16_t* out = a.q + (sk * a.G) * rs + r;
     for (int gb = 0; gb < a.G; gb += 64) {
       const int gn = a.G - gb < 64 ? a.G - gb : 64;
       uint64_t unsure = 0;
@@ -271,7 +277,7 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
         const double v = F * 65536.0, vlo = v - kBand, vhi = v + kBand;
         const double fh = floor(vhi);
         if (vhi < 1.0 || vlo >= fh || vlo >= 65535.0)
-          out[(int64_t)(gb + gi) * a.R] = (uint16_t)(vhi < 1.0 ? 0u : (fh >= 65535.0 ? 65535u : (uint32_t)fh));
+          out[(int64_t)(gb + gi) * rs] = (uint16_t)(vhi < 1.0 ? 0u : (fh >= 65535.0 ? 65535u : (uint32_t)fh));
         else
           unsure |= 1ull << gi;
       };
@@ -294,7 +300,7 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
           const double phi = spread[cl] ? 0.5 * erfc((mu[cl] - u) / den[cl]) : (u >= mu[cl] ? 1.0 : 0.0);
           F += wt[cl] * phi;
         }
-        out[(int64_t)(gb + gi) * a.R] = (uint16_t)quant16(F * 65536.0);
+        out[(int64_t)(gb + gi) * rs] = (uint16_t)quant16(F * 65536.0);
       }
     }
   }
@@ -336,9 +342,19 @@ __device__ __forceinline__ uint32_t claim_bin(uint32_t* fine, uint32_t v, bool a
   return (atomicAdd(&fine[v >> 1], 1u << shv) >> shv) & 0xFFFFu;
 }
 
+// Rank of slot j of thread tid: slots come in pairs of neighbouring ranks,
+// 2 (tid + m NT) and 2 (tid + m NT) + 1 for pair m, whose two 16-bit values
+// are one aligned 32-bit word of a workspace row.
+template <int NT>
+__device__ __forceinline__ int slot_rank(int tid, int j) {
+  return 2 * (tid + (j >> 1) * NT) + (j & 1);
+}
+
 template <int NT, int V>
 __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
   constexpr int NW = NT / 64;
+  constexpr int V2 = (V + 1) / 2;  // slot pairs per thread
+  constexpr int VS = 2 * V2;       // slots per thread
   __shared__ uint32_t fine[kFineWords];  // bin counters, then the sorted values and their prefix sums
   __shared__ double wts[ARGUS_MAX_W1_GRID];  // trapezoid weights
   __shared__ uint32_t bcnt[256], bexcl[256];
@@ -353,8 +369,8 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
 
   if (!evaluated(a, n)) {
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
-      const int r = tid + j * NT;
+    for (int j = 0; j < VS; ++j) {
+      const int r = slot_rank<NT>(tid, j);
       if (r >= a.R) break;
       const int64_t c = cell_of(a, r, s, k);
       a.o.score[c] = 0.0;
@@ -369,10 +385,10 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
     return;
   }
 
-  uint32_t pm = 0;  // bit j: slot j (rank tid + j NT) is present
+  uint32_t pm = 0;  // bit j: slot j is present
 #pragma unroll
-  for (int j = 0; j < V; ++j) {
-    const int r = tid + j * NT;
+  for (int j = 0; j < VS; ++j) {
+    const int r = slot_rank<NT>(tid, j);
     if (r >= a.R) break;
     uint32_t nc;
     uint64_t tot;
@@ -381,7 +397,15 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
   double lnlo, du;
   grid_of(a, sk, lnlo, du);
   const int G = a.G;
-  const uint16_t* qrow = a.q + sk * (int64_t)G * a.R;
+  const int64_t rs = row_stride(a);
+  // this kernel's rows as a buffer: the word of pair m in row g is at byte
+  // 2 rs g + 4 (tid + m NT); words of pairs past the ranks are never used,
+  // and those past the last row read 0 (buffer range check)
+  const __amdgpu_buffer_rsrc_t qbuf =
+      __builtin_amdgcn_make_buffer_rsrc(a.q + sk * (int64_t)G * rs, (short)0, (int)(2 * rs * G), 0x00020000);
+  auto pair_word = [&](int g, int m) -> uint32_t {
+    return __builtin_amdgcn_raw_buffer_load_b32(qbuf, (int)(2u * (uint32_t)rs * (uint32_t)g + 4u * (uint32_t)(tid + m * NT)), 0, 0);
+  };
   // w_g = (x_{min(g+1,G-1)} - x_{max(g-1,0)}) / 2, x_i = exp(lnlo + i du)
   for (int g = tid; g < G; g += NT)
     wts[g] = (exp(lnlo + (double)(g + 1 < G ? g + 1 : G - 1) * du) - exp(lnlo + (double)(g > 0 ? g - 1 : 0) * du)) /
@@ -389,18 +413,19 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
 
   // per slot: acc = weighted sum; qt = q | (rank among equal values) << 16;
   // cl2 / qn2: values below q / the next grid point's q, 16 bits each, two
-  // slots to a word (keeps the 16-slot variant in registers)
-  constexpr int V2 = (V + 1) / 2;
-  double acc[V];
-  uint32_t qt[V], cl2[V2], qn2[V2];
+  // slots to a word (keeps the 16-slot variant in registers). A slot that is
+  // not present may hold any value; every use is masked by present().
+  double acc[VS];
+  uint32_t qt[VS], cl2[V2], qn2[V2];
   auto present = [&](int j) { return ((pm >> j) & 1u) != 0; };
 #pragma unroll
-  for (int j = 0; j < V; ++j) {
-    acc[j] = 0.0;
-    qt[j] = present(j) ? qrow[(uint32_t)(tid + j * NT)] : 0u;
+  for (int m = 0; m < V2; ++m) {
+    const uint32_t w = pair_word(0, m);
+    qt[2 * m] = w & 0xFFFFu;
+    qt[2 * m + 1] = w >> 16;
+    acc[2 * m] = acc[2 * m + 1] = 0.0;
+    cl2[m] = qn2[m] = 0;
   }
-#pragma unroll
-  for (int j = 0; j < V2; ++j) cl2[j] = qn2[j] = 0;
   if (tid < 256) bcnt[tid] = 0;
   if (tid == 0) {
     mn_sh = ~0ull;
@@ -411,19 +436,10 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
 
   const int E = ((int)n + NT - 1) / NT;  // sorted values per thread in the prefix sum
   for (int g = 0; g < G; ++g) {
-    if (g + 1 < G) {
-      const uint16_t* nrow = qrow + (int64_t)(g + 1) * a.R;  // uniform row base, 32-bit lane offsets
-#pragma unroll
-      for (int j = 0; j < V; j += 2) {
-        const uint32_t lo = present(j) ? nrow[(uint32_t)(tid + j * NT)] : 0u;
-        const uint32_t hi = j + 1 < V && present(j + 1) ? nrow[(uint32_t)(tid + (j + 1) * NT)] : 0u;
-        qn2[j >> 1] = lo | (hi << 16);
-      }
-    }
     // 1. bucket (high byte) counts
 #pragma unroll
-    for (int j = 0; j < V; ++j) hist_add<1>(bcnt, (qt[j] & 0xFFFFu) >> 8, present(j));
-    __syncthreads();
+    for (int j = 0; j < VS; ++j) hist_add<1>(bcnt, (qt[j] & 0xFFFFu) >> 8, present(j));
+    lds_barrier();
     // 2. bucket scan, first half; clear the bins of the occupied buckets
     uint32_t bc = 0, binc = 0;
     if (tid < 256) {
@@ -431,9 +447,12 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
       binc = wave_incl_scan(bc);
       if (lane == 63) wtot[wv] = binc;
     }
+    // (not unrolled: unrolled, its per-iteration addresses stay live across
+    // the loop over grid points and push other values out of registers)
+#pragma unroll 1
     for (int ch = tid; ch < kFineWords / 4; ch += NT)
       if (bcnt[ch >> 5]) *reinterpret_cast<uint4*>(&fine[ch * 4]) = make_uint4(0, 0, 0, 0);
-    __syncthreads();
+    lds_barrier();
     // 3. bucket exclusive prefix; per-value claims (rank among equal values)
     if (tid < 256) {
       uint32_t base = 0;
@@ -441,11 +460,20 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
       bexcl[tid] = base + binc - bc;
     }
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
+    for (int j = 0; j < VS; ++j) {
       const uint32_t v = qt[j] & 0xFFFFu;
       qt[j] = v | (claim_bin(fine, v, present(j)) << 16);
     }
-    __syncthreads();
+    lds_barrier();
+    // the next point's words, one load per pair with no arithmetic on the
+    // result: the loads stay in flight until step 8 (the barriers of the
+    // steps in between order LDS only). Issued here, after the last reload
+    // of spilled registers before step 8 (loads complete in order, so a
+    // reload waits for every load issued before it).
+    if (g + 1 < G) {
+#pragma unroll
+      for (int m = 0; m < V2; ++m) qn2[m] = pair_word(g + 1, m);
+    }
     // 4. exclusive prefix over the 256 bins of each occupied bucket
     for (int h = wv; h < 256; h += NW) {
       if (bcnt[h] == 0) continue;
@@ -456,29 +484,29 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
       const uint32_t e0 = wave_incl_scan(t) - t, e1 = e0 + b0, e2 = e1 + b1, e3 = e2 + b2;
       *p = make_uint2(e0 | (e1 << 16), e2 | (e3 << 16));
     }
-    __syncthreads();
+    lds_barrier();
     // 5. values below q: bucket prefix + bin prefix
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
+    for (int j = 0; j < VS; ++j) {
       const uint32_t v = qt[j] & 0xFFFFu;
       const uint32_t clt = present(j) ? bexcl[v >> 8] + ((fine[v >> 1] >> ((v & 1u) * 16u)) & 0xFFFFu) : 0u;
       cl2[j >> 1] = (j & 1) ? (cl2[j >> 1] & 0xFFFFu) | (clt << 16) : (cl2[j >> 1] & 0xFFFF0000u) | clt;
     }
-    __syncthreads();
+    lds_barrier();
     // 6. counting-sort scatter to position (values below) + (rank among
     //    equal values); clear the bucket counts for the next point
 #pragma unroll
-    for (int j = 0; j < V; ++j)
+    for (int j = 0; j < VS; ++j)
       if (present(j)) fine[((cl2[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu) + (qt[j] >> 16)] = qt[j] & 0xFFFFu;
     if (tid < 256) bcnt[tid] = 0;
-    __syncthreads();
+    lds_barrier();
     // 7. exclusive prefix sums of the sorted values, in place
     const int i0 = tid * E, i1 = i0 + E < (int)n ? i0 + E : (int)n;
     uint32_t loc = 0;
     for (int i = i0; i < i1; ++i) loc += fine[i];
     const uint32_t linc = wave_incl_scan(loc);
     if (lane == 63) wtot[wv] = linc;
-    __syncthreads();
+    lds_barrier();
     uint32_t run = linc - loc, T = 0;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
@@ -491,11 +519,11 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
       fine[i] = run;
       run += x;
     }
-    __syncthreads();
+    lds_barrier();
     // 8. S_a = q (2 c - n) + T - 2 P, weighted by the trapezoid rule
     const double wg = wts[g];
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
+    for (int j = 0; j < VS; ++j) {
       if (present(j)) {
         // S <= (n - 1) 65535 < 2^32: the sum is exact modulo 2^32
         const uint32_t clt = (cl2[j >> 1] >> ((j & 1) * 16)) & 0xFFFFu;
@@ -509,10 +537,10 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
   // deviation scores; quartiles by radix selection on their bit patterns
   // (the scores are kept only as their bits, offset by the minimum)
   const double norm = 65536.0 * (double)(n - 1);
-  uint64_t key[V];
+  uint64_t key[VS];
   unsigned long long mn = ~0ull, mx = 0;
 #pragma unroll
-  for (int j = 0; j < V; ++j) {
+  for (int j = 0; j < VS; ++j) {
     key[j] = (uint64_t)__double_as_longlong(acc[j] / norm);
     if (present(j)) {
       mn = key[j] < mn ? key[j] : mn;
@@ -531,19 +559,19 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
   __syncthreads();
   const uint64_t kmin = mn_sh, kmax = mx_sh;
 #pragma unroll
-  for (int j = 0; j < V; ++j) key[j] = present(j) ? key[j] - kmin : 0;
+  for (int j = 0; j < VS; ++j) key[j] = present(j) ? key[j] - kmin : 0;
   const uint32_t nm1 = n - 1;
   const uint32_t ranks[2] = {nm1 / 4, (uint32_t)((3ull * nm1) / 4)};
   uint64_t qs[2];
-  select_ranks<NT, V, 2>(key, (uint64_t)pm, kmax - kmin, ranks, qs, sel);
+  select_ranks<NT, VS, 2>(key, (uint64_t)pm, kmax - kmin, ranks, qs, sel);
   const double a1 = __longlong_as_double((long long)(kmin + qs[0]));
   const double a3 = __longlong_as_double((long long)(kmin + qs[1]));
   const double fence = a3 + (double)a.alpha_pm * (a3 - a1) / 1000.0;
 
   uint32_t nf = 0;
 #pragma unroll
-  for (int j = 0; j < V; ++j) {
-    const int r = tid + j * NT;
+  for (int j = 0; j < VS; ++j) {
+    const int r = slot_rank<NT>(tid, j);
     if (r >= a.R) break;
     const bool p = present(j);
     const double sc = __longlong_as_double((long long)(kmin + key[j]));
@@ -601,7 +629,7 @@ hipError_t ensure_phi_table() {
 
 size_t w1_workspace_bytes(int32_t R, int32_t S, int32_t K, int32_t G) {
   if (R < 0 || S < 0 || K < 0 || G < 0) return 0;
-  return (size_t)S * (size_t)K * (size_t)G * (size_t)R * sizeof(uint16_t);
+  return (size_t)S * (size_t)K * (size_t)G * (size_t)(R + (R & 1)) * sizeof(uint16_t);
 }
 
 hipError_t launch_w1(const W1Launch& l, hipStream_t st) {

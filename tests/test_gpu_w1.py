@@ -119,7 +119,8 @@ def check_cdf_values(gw, ncl, cnt, a, b, R, S, K, what, n_points=4000, seed=0, k
         r = int(rng.integers(R))
         if 1 <= ncl[r, s, k] <= MAXC and cnt[r, s, k, :ncl[r, s, k]].sum() > 0:
             pts.append((s, k, int(rng.integers(G)), r))
-    idx = torch.tensor([((s * K + k) * G + g) * R + r for s, k, g, r in pts], dtype=torch.int64)
+    Rp = R + (R & 1)  # workspace rows: the rank count rounded up to even
+    idx = torch.tensor([((s * K + k) * G + g) * Rp + r for s, k, g, r in pts], dtype=torch.int64)
     ws = gw["_workspace"].view(torch.int16)
     got = ws[idx.to(ws.device)].cpu().numpy().view(np.uint16).astype(np.int64)
     want = np.array([oracle.w1_cdf_q_grid(cnt[r, s, k, :ncl[r, s, k]], a[r, s, k, :ncl[r, s, k]],
