@@ -447,11 +447,18 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
       binc = wave_incl_scan(bc);
       if (lane == 63) wtot[wv] = binc;
     }
-    // (not unrolled: unrolled, its per-iteration addresses stay live across
-    // the loop over grid points and push other values out of registers)
+    // (16-bin chunks tid + i NT, 32 to a bucket: their buckets' counts are
+    // read together, then the chunks of occupied buckets cleared one by one;
+    // unrolled, the stores' addresses would stay live across the loop over
+    // grid points and push other values out of registers)
+    constexpr int kChunks = kFineWords / 4 / NT;
+    static_assert(kChunks <= 32, "chunk mask");
+    uint32_t occ = 0;
+#pragma unroll
+    for (int i = 0; i < kChunks; ++i) occ |= (bcnt[(tid + i * NT) >> 5] != 0 ? 1u : 0u) << i;
 #pragma unroll 1
-    for (int ch = tid; ch < kFineWords / 4; ch += NT)
-      if (bcnt[ch >> 5]) *reinterpret_cast<uint4*>(&fine[ch * 4]) = make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < kChunks; ++i)
+      if ((occ >> i) & 1u) *reinterpret_cast<uint4*>(&fine[(tid + i * NT) * 4]) = make_uint4(0, 0, 0, 0);
     lds_barrier();
     // 3. bucket exclusive prefix; per-value claims (rank among equal values)
     if (tid < 256) {
@@ -473,10 +480,17 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
     if (g + 1 < G) {
 #pragma unroll
       for (int m = 0; m < V2; ++m) qn2[m] = pair_word(g + 1, m);
+      // keeps the compiler from sinking the loads to their use
+      __asm__ volatile("" ::: "memory");
     }
     // 4. exclusive prefix over the 256 bins of each occupied bucket
-    for (int h = wv; h < 256; h += NW) {
-      if (bcnt[h] == 0) continue;
+    // (buckets wv + NW i of this wavefront: one count per lane, then the
+    // occupied ones only)
+    constexpr int kWaveBuckets = 256 / NW;
+    static_assert(kWaveBuckets <= 64, "one bucket per lane");
+    const uint64_t occb = __ballot(lane < kWaveBuckets && bcnt[lane < kWaveBuckets ? wv + NW * lane : 0] != 0);
+    for (uint64_t mb = occb; mb; mb &= mb - 1) {
+      const int h = wv + NW * (int)__builtin_ctzll(mb);
       uint2* p = reinterpret_cast<uint2*>(&fine[h * 128 + 2 * lane]);
       const uint2 wd = *p;
       const uint32_t b0 = wd.x & 0xFFFFu, b1 = wd.x >> 16, b2 = wd.y & 0xFFFFu, b3 = wd.y >> 16;
