@@ -597,7 +597,9 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
   }
   for (int o = 32; o > 0; o >>= 1) nf += __shfl_xor(nf, o, 64);
   if (lane == 0 && nf) atomicAdd(&nf_sh, nf);
-  __syncthreads();
+  // orders the LDS count only: the score and flag stores are not waited for,
+  // so the workgroup ends (and the next one starts) while they drain
+  lds_barrier();
   if (tid == 0) {
     a.o.lo_ns[sk] = a.o.lo_ns[sk] < 1 ? 1 : a.o.lo_ns[sk];
     a.o.q1[sk] = a1;
