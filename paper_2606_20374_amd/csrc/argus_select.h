@@ -24,7 +24,10 @@ __device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool acti
     const uint32_t lb = __builtin_amdgcn_readlane(bin, leader);
     const bool mine = active && bin == lb;
     const unsigned long long same = __ballot(mine);
-    if (lane == leader) atomicAdd(&hist[lb], (uint32_t)__popcll(same));
+    // the leader's own bin (equal to lb) as the address: a divergent address
+    // keeps the compiler from wrapping the single-lane atomic in another
+    // wave-wide aggregation of its own
+    if (lane == leader) atomicAdd(&hist[bin], (uint32_t)__popcll(same));
     if (mine) active = false;
   }
   if (active) atomicAdd(&hist[bin], 1u);

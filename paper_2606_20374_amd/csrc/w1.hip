@@ -317,29 +317,47 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
   return v;
 }
 
-// Adds one to the 16-bit counter of bin v (two counters per word) for every
-// active lane and returns the counter's value before the lane's own claim,
-// so lanes with equal v get distinct consecutive values. Lanes sharing the
-// first active lane's value are served by one atomic (at the ends of the
-// grid most ranks share the value 0 or 65535); the rest claim one by one
-// (a second shared round cost more than it saved). Must be reached by every
-// lane of the wavefront.
-__device__ __forceinline__ uint32_t claim_bin(uint32_t* fine, uint32_t v, bool active) {
+// Claims for slots j0 .. j0 + B - 1 of every lane (qt[j] holds the value;
+// bit j of pm: slot j active): the 16-bit counter of bin v (two counters per
+// word) counts one per active lane, and each lane gets the counter's value
+// before its own claim, so lanes with equal v get distinct consecutive
+// values. Per slot one atomic instruction, in which the first active lane
+// adds for every lane sharing its value (at the ends of the grid most ranks
+// share the value 0 or 65535) and the lanes with other values add one each;
+// every slot's atomic is issued before any result is waited for. On return
+// qt[j] = value | claim << 16. Must be reached by every lane of the
+// wavefront.
+template <int VS, int B>
+__device__ __forceinline__ void claim_bins(uint32_t* fine, uint32_t (&qt)[VS], uint32_t pm, int j0) {
   const int lane = threadIdx.x & 63;
-  const unsigned long long act = __ballot(active);
-  if (act == 0) return 0;
-  const int leader = __ffsll((long long)act) - 1;
-  const uint32_t lv = __builtin_amdgcn_readlane(v, leader);
-  const bool mine = active && v == lv;
-  const unsigned long long same = __ballot(mine);
-  const uint32_t sh = (lv & 1u) * 16u;
-  uint32_t old = 0;
-  if (lane == leader) old = atomicAdd(&fine[lv >> 1], (uint32_t)__popcll(same) << sh);
-  old = __builtin_amdgcn_readlane(old, leader);
-  if (mine) return ((old >> sh) & 0xFFFFu) + (uint32_t)__popcll(same & ((1ull << lane) - 1ull));
-  if (!active) return 0;
-  const uint32_t shv = (v & 1u) * 16u;
-  return (atomicAdd(&fine[v >> 1], 1u << shv) >> shv) & 0xFFFFu;
+  const unsigned long long below = (1ull << lane) - 1ull;
+  uint32_t old[B];
+  int leader[B];
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    const int j = j0 + i;
+    const uint32_t v = qt[j] & 0xFFFFu;
+    const bool active = ((pm >> j) & 1u) != 0;
+    const unsigned long long act = __ballot(active);
+    leader[i] = act ? __ffsll((long long)act) - 1 : 0;
+    const uint32_t lv = __builtin_amdgcn_readlane(v, leader[i]);
+    const bool mine = active && v == lv;
+    const unsigned long long same = __ballot(mine);
+    const bool lead = mine && lane == leader[i];
+    const uint32_t add = (lead ? (uint32_t)__popcll(same) : 1u) << ((v & 1u) * 16u);
+    old[i] = 0;
+    if (active && (lead || !mine)) old[i] = atomicAdd(&fine[v >> 1], add);
+    // lanes sharing the leader's value: their place among those lanes
+    qt[j] = v | ((mine ? 0x8000u | (uint32_t)__popcll(same & below) : 0u) << 16);
+  }
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    const int j = j0 + i;
+    const uint32_t v = qt[j] & 0xFFFFu, sh = (v & 1u) * 16u;
+    const uint32_t lo = __builtin_amdgcn_readlane(old[i], leader[i]);
+    const uint32_t c = (qt[j] >> 31) ? ((lo >> sh) & 0xFFFFu) + ((qt[j] >> 16) & 0x7FFFu) : (old[i] >> sh) & 0xFFFFu;
+    qt[j] = v | (c << 16);
+  }
 }
 
 // Rank of slot j of thread tid: slots come in pairs of neighbouring ranks,
@@ -466,11 +484,7 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
       for (int w = 0; w < wv; ++w) base += wtot[w];
       bexcl[tid] = base + binc - bc;
     }
-#pragma unroll
-    for (int j = 0; j < VS; ++j) {
-      const uint32_t v = qt[j] & 0xFFFFu;
-      qt[j] = v | (claim_bin(fine, v, present(j)) << 16);
-    }
+    claim_bins<VS, VS>(fine, qt, pm, 0);
     lds_barrier();
     // the next point's words, one load per pair with no arithmetic on the
     // result: the loads stay in flight until step 8 (the barriers of the
