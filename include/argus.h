@@ -461,8 +461,10 @@ typedef struct argus_w1_out {
 
 void argus_w1_default(argus_w1_params_t* p);
 
-/* Workspace bytes: 2 * n_steps * n_kernels * grid * (n_ranks rounded up to
- * even) (the 16-bit CDF values of every rank at every grid point). */
+/* Workspace bytes: 2 * n_steps * n_kernels * grid * R' rounded up to a
+ * multiple of 256 (the 16-bit CDF values of every rank at every grid point),
+ * plus 9 * n_steps * n_kernels * R' (scores and flags on their way to the
+ * outputs), R' = n_ranks rounded up to even. */
 size_t argus_w1_workspace(int32_t n_ranks, int32_t n_steps, int32_t n_kernels, int32_t grid);
 
 /* clusters: the n_clusters, count, p50_ns and p99_ns outputs of argus_kde

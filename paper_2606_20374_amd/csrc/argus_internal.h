@@ -50,6 +50,17 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Work item of workgroup b of a grid of n, numbered so that the workgroups
+// of one XCD take consecutive items. Workgroups are dispatched to the eight
+// XCDs in turn (b mod 8), each XCD with its own L2; items whose outputs or
+// inputs share cache lines (neighbouring kernel ids of one cell row) then
+// meet in one L2 instead of eight. A bijection on [0, n).
+__device__ __forceinline__ int64_t xcd_item(int64_t b, int64_t n) {
+  constexpr int64_t kXcd = 8;
+  const int64_t x = b % kXcd, i = b / kXcd, q = n / kXcd, r = n % kXcd;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + i;
+}
+
 // 64-lane wavefront reductions (gfx950 runs wave64 only).
 __device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

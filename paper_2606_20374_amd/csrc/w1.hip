@@ -30,7 +30,11 @@
 //               nearest-rank quartiles of the scores come from a radix
 //               selection on their bit patterns (non-negative doubles order
 //               like their bits), then the upper fence of Eq. 4 and the
-//               flags.
+//               flags, written to the workspace contiguously.
+//               Workgroups are numbered so that neighbouring kernel ids run
+//               on one XCD.
+//   w1_out      the scores and flags from the workspace to the
+//               [rank][step][kernel] outputs through 64 x 64 LDS tiles.
 // The pairwise matrix of the paper is never formed: S_a is the row sum of
 // |F_a - F_b| at one grid point, which is all the mean-W1 score needs.
 #include <cmath>
@@ -75,9 +79,29 @@ struct W1Args {
   uint16_t* q;  // workspace [S][K][G][R rounded up to even]
 };
 
-// Workspace row stride: the rank count rounded up to even, so that the
-// values of ranks 2p and 2p + 1 share one aligned 32-bit word.
-__device__ __forceinline__ int64_t row_stride(const W1Args& a) { return (int64_t)(a.R + (a.R & 1)); }
+// Workspace layout: the CDF values, one block per (step, kernel) of G rows
+// of R' 16-bit values, R' (the row stride) the rank count rounded up to
+// even, so that the values of ranks 2p and 2p + 1 share one aligned 32-bit
+// word; then, 256-byte aligned, the scores ([step, kernel][R'] doubles) and
+// the flags ([step, kernel][R'] bytes) on their way to the
+// [rank][step][kernel] outputs.
+__host__ __device__ __forceinline__ int64_t ws_row_stride(int32_t R) { return (int64_t)R + (R & 1); }
+__host__ __device__ __forceinline__ int64_t ws_q_bytes(int32_t R, int32_t S, int32_t K, int32_t G) {
+  return ((int64_t)S * K * G * ws_row_stride(R) * 2 + 255) & ~(int64_t)255;
+}
+__device__ __forceinline__ int64_t row_stride(const W1Args& a) { return ws_row_stride(a.R); }
+__device__ __forceinline__ uint16_t* ws_block(const W1Args& a, int64_t sk) {
+  return a.q + sk * a.G * ws_row_stride(a.R);
+}
+__device__ __forceinline__ double* ws_scores(const W1Args& a, int64_t sk) {
+  return reinterpret_cast<double*>(reinterpret_cast<char*>(a.q) + ws_q_bytes(a.R, a.S, a.K, a.G)) +
+         sk * ws_row_stride(a.R);
+}
+__device__ __forceinline__ uint8_t* ws_flags(const W1Args& a, int64_t sk) {
+  const int64_t SK = (int64_t)a.S * a.K, rs = ws_row_stride(a.R);
+  return reinterpret_cast<uint8_t*>(reinterpret_cast<char*>(a.q) + ws_q_bytes(a.R, a.S, a.K, a.G) + SK * rs * 8) +
+         sk * rs;
+}
 
 __device__ __forceinline__ int64_t cell_of(const W1Args& a, int r, int s, int k) {
   return ((int64_t)r * a.S + s) * a.K + k;
@@ -236,7 +260,7 @@ __global__ __launch_bounds__(256) void w1_cdf(W1Args a) {
       wt[cl] = (double)a.cnt[c * kMaxC + cl] / (double)tot;
     }
     const int64_t rs = row_stride(a);
-    uint16_t* out = a.q + (sk * a.G) * rs + r;
+    uint16_t* out = ws_block(a, sk) + r;
     for (int gb = 0; gb < a.G; gb += 64) {
       const int gn = a.G - gb < 64 ? a.G - gb : 64;
       uint64_t unsure = 0;
@@ -381,18 +405,22 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
   __shared__ unsigned long long mn_sh, mx_sh;
   __shared__ uint32_t nf_sh;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int64_t sk = blockIdx.x;
+  const int64_t sk = xcd_item(blockIdx.x, gridDim.x);
   const int s = (int)(sk / a.K), k = (int)(sk % a.K);
   const uint32_t n = a.o.n_present[sk];
+  // scores and flags go to the workspace, contiguous per (step, kernel);
+  // w1_out moves them to the cell layout
+  const int64_t rs = row_stride(a);
+  double* ws_score = ws_scores(a, sk);
+  uint8_t* ws_flag = ws_flags(a, sk);
 
   if (!evaluated(a, n)) {
 #pragma unroll
     for (int j = 0; j < VS; ++j) {
       const int r = slot_rank<NT>(tid, j);
       if (r >= a.R) break;
-      const int64_t c = cell_of(a, r, s, k);
-      a.o.score[c] = 0.0;
-      a.o.flag[c] = 0;
+      ws_score[r] = 0.0;
+      ws_flag[r] = 0;
     }
     if (tid == 0) {
       a.o.lo_ns[sk] = 0;
@@ -415,12 +443,11 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
   double lnlo, du;
   grid_of(a, sk, lnlo, du);
   const int G = a.G;
-  const int64_t rs = row_stride(a);
   // this kernel's rows as a buffer: the word of pair m in row g is at byte
   // 2 rs g + 4 (tid + m NT); words of pairs past the ranks are never used,
   // and those past the last row read 0 (buffer range check)
   const __amdgpu_buffer_rsrc_t qbuf =
-      __builtin_amdgcn_make_buffer_rsrc(a.q + sk * (int64_t)G * rs, (short)0, (int)(2 * rs * G), 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc(ws_block(a, sk), (short)0, (int)(2 * rs * G), 0x00020000);
   auto pair_word = [&](int g, int m) -> uint32_t {
     return __builtin_amdgcn_raw_buffer_load_b32(qbuf, (int)(2u * (uint32_t)rs * (uint32_t)g + 4u * (uint32_t)(tid + m * NT)), 0, 0);
   };
@@ -605,9 +632,8 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
     const double sc = __longlong_as_double((long long)(kmin + key[j]));
     const bool f = p && sc > fence;
     nf += f ? 1u : 0u;
-    const int64_t c = cell_of(a, r, s, k);
-    a.o.score[c] = p ? sc : 0.0;
-    a.o.flag[c] = f ? 1 : 0;
+    ws_score[r] = p ? sc : 0.0;
+    ws_flag[r] = f ? 1 : 0;
   }
   for (int o = 32; o > 0; o >>= 1) nf += __shfl_xor(nf, o, 64);
   if (lane == 0 && nf) atomicAdd(&nf_sh, nf);
@@ -620,6 +646,41 @@ __global__ __launch_bounds__(NT) void w1_score(W1Args a) {
     a.o.q3[sk] = a3;
     a.o.fence[sk] = fence;
     a.o.n_flag[sk] = nf_sh;
+  }
+}
+
+// ------------------------------------------------------------------ out
+// The scores and flags of the workspace blocks ([step, kernel][rank]) into
+// the [rank][step][kernel] outputs, through 64 x 64 LDS tiles so that both
+// the reads and the writes are contiguous.
+__global__ __launch_bounds__(256) void w1_out(W1Args a) {
+  __shared__ double ts[64][65];
+  __shared__ uint8_t tf[64][68];
+  const int64_t SK = (int64_t)a.S * a.K, sk0 = (int64_t)blockIdx.x * 64;
+  const int r0 = blockIdx.y * 64, t = threadIdx.x;
+  for (int i = t; i < 64 * 64; i += 256) {
+    const int row = i >> 6, col = i & 63;  // row: (step, kernel), col: rank
+    const int64_t sk = sk0 + row;
+    const int r = r0 + col;
+    double v = 0.0;
+    uint8_t f = 0;
+    if (sk < SK && r < a.R) {
+      v = ws_scores(a, sk)[r];
+      f = ws_flags(a, sk)[r];
+    }
+    ts[row][col] = v;
+    tf[row][col] = f;
+  }
+  __syncthreads();
+  for (int i = t; i < 64 * 64; i += 256) {
+    const int row = i >> 6, col = i & 63;  // row: rank, col: (step, kernel)
+    const int r = r0 + row;
+    const int64_t sk = sk0 + col;
+    if (sk < SK && r < a.R) {
+      const int64_t c = (int64_t)r * SK + sk;  // cell (r, s, k)
+      a.o.score[c] = ts[col][row];
+      a.o.flag[c] = tf[col][row];
+    }
   }
 }
 
@@ -659,7 +720,7 @@ hipError_t ensure_phi_table() {
 
 size_t w1_workspace_bytes(int32_t R, int32_t S, int32_t K, int32_t G) {
   if (R < 0 || S < 0 || K < 0 || G < 0) return 0;
-  return (size_t)S * (size_t)K * (size_t)G * (size_t)(R + (R & 1)) * sizeof(uint16_t);
+  return (size_t)ws_q_bytes(R, S, K, G) + (size_t)S * (size_t)K * (size_t)ws_row_stride(R) * 9;
 }
 
 hipError_t launch_w1(const W1Launch& l, hipStream_t st) {
@@ -689,6 +750,9 @@ hipError_t launch_w1(const W1Launch& l, hipStream_t st) {
   else if (R <= 10240) launch_score<1024, 10>(wa, st);
   else if (R <= 12288) launch_score<1024, 12>(wa, st);
   else launch_score<1024, 16>(wa, st);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(w1_out, dim3((unsigned)((SK + 63) / 64), (unsigned)((l.R + 63) / 64)), dim3(256), 0, st, wa);
   return hipGetLastError();
 }
 

@@ -122,9 +122,13 @@ def test_kde_rejects_bad_arguments(mutate):
 
 def test_w1_defaults_and_workspace():
     assert pa.w1_defaults() == dict(grid=64, min_ranks=3, alpha_pm=1500)
-    assert pa.lib().argus_w1_workspace(10240, 1, 2048, 64) == 2 * 10240 * 2048 * 64
-    # rows of an odd rank count are padded to even
-    assert pa.lib().argus_w1_workspace(3, 2, 5, 64) == 2 * 4 * 2 * 5 * 64
+    def al256(x):
+        return (x + 255) // 256 * 256
+    # CDF values (rows of an odd rank count padded to even), then 9 bytes per
+    # (step, kernel, rank) of staged scores and flags
+    assert pa.lib().argus_w1_workspace(10240, 1, 2048, 64) == 2 * 10240 * 2048 * 64 + 9 * 10240 * 2048
+    assert pa.lib().argus_w1_workspace(3, 2, 5, 64) == al256(2 * 4 * 2 * 5 * 64) + 9 * 4 * 2 * 5
+    assert pa.lib().argus_w1_workspace(3, 2, 5, 2) == al256(2 * 4 * 2 * 5 * 2) + 9 * 4 * 2 * 5
 
 
 @pytest.mark.parametrize("mutate", [
