@@ -317,9 +317,11 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
 
   // Persistent workgroups pull segments from a queue, so the output stores
   // of one segment drain while the loads of the next are already in flight.
+  // Threads share only LDS state, so every barrier orders LDS alone: no
+  // barrier waits for the outputs' stores.
   while (true) {
   if (tid == 0) g_next = (int64_t)atomicAdd(a.queue, 1u);
-  __syncthreads();
+  lds_barrier();
   // the segment index is wave-uniform: keep it (and what derives from it:
   // bounds, loop limits) in scalar registers
   const int64_t g = (int64_t)__builtin_amdgcn_readfirstlane((int)g_next);
@@ -378,7 +380,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         sm.nslots = 0;
         sm.stuck = 0;
       }
-      __syncthreads();
+      lds_barrier();
 
       // unaligned head and tail: at most 3 events each, on the first threads
       if (a.vec_ok) {
@@ -453,7 +455,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         }
       }
       first_scan = false;
-      __syncthreads();
+      lds_barrier();
 
       // A claim wait cut short dropped an update: every kernel of this pass is
       // redone (the per-segment aggregates were complete in the first scan).
@@ -513,7 +515,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
         const int64_t c = g * K + kb + (MAPPED ? (int)sm.slot_kid[s] : s);
         *reinterpret_cast<uint4*>(a.hist + c * NB + 4 * q) = make_uint4(v[0], v[1], v[2], v[3]);
       }
-      __syncthreads();
+      lds_barrier();
       const bool again = sm.poison != 0 || redo_pass;
       // mark what was written; kernels that ran out of room start over
       for (int s = tid; s < nslot; s += kThreads) {
@@ -531,7 +533,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
       if (MAPPED)
         for (int i = tid; i < nk; i += kThreads)
           if (sg.map_get(i) == kMapDefer) sg.map_set(i, (uint16_t)kMapEmpty);
-      __syncthreads();
+      lds_barrier();
       if (!again) break;
     }
     if (MAPPED) {
@@ -539,7 +541,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
       // are not written)
       for (int i = tid; i < nk; i += kThreads)
         if (sg.map_get(i) == kMapEmpty) a.count[g * K + kb + i] = 0;
-      __syncthreads();
+      lds_barrier();
     }
   }
 
@@ -555,7 +557,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
     atomicMin(&sm.red_first, wf);
     atomicMax(&sm.red_last, wl);
   }
-  __syncthreads();
+  lds_barrier();
   if (tid == 0) {
     a.n_valid[g] = sm.red_valid;
     a.n_invalid[g] = sm.red_invalid;
@@ -566,7 +568,7 @@ __global__ __launch_bounds__(kThreads) void summarize_kernel(Args a) {
     if (a.wire_bytes) a.wire_bytes[g] = (int64_t)sm.red_wire;
   }
   if (tid < NS) a.stream_busy_ns[g * NS + tid] = (int64_t)sm.stream_busy[tid];
-  __syncthreads();
+  lds_barrier();
   }
 }
 
