@@ -1508,10 +1508,59 @@ constexpr int kBlockDepth = 8;  // duration loads in flight per thread in the st
 constexpr uint32_t kBlockMin = 2048;
 constexpr int kSelRegion = 512;                      // words per target, within the tier-1 grid words
 constexpr int kSelDigit = 9;                         // log2(kSelRegion)
-constexpr int kSelCap = 64;
+constexpr int kSelCap = 64;        // gathered durations per target (8-byte entries)
+constexpr int kSelCap32 = 256;     // gathered offsets per target (4-byte entries, bins narrower than 2^32)
 static_assert(kMaxT % kBlockWaves == 0, "selection targets shared out over the wavefronts");
 static_assert((1 << kSelDigit) == kSelRegion && 2 * kSelCap <= kSelRegion && kMaxT * kSelRegion <= Tier<1>::kWords,
               "selection regions");
+static_assert(kSelCap32 + 256 <= kSelRegion && kSelCap32 == 4 * kWave, "offset list and its digit histogram");
+
+// Element of rank r among the k <= kSelCap32 offsets of list (one wavefront,
+// four entries per lane): MSD radix selection with 8-bit digits over the
+// nb-bit offsets, the digit histogram in hist (256 words). Sets ok = false
+// when r >= k.
+__device__ __forceinline__ uint32_t select_offsets(const uint32_t* list, uint32_t* hist, int k, int nb, uint64_t r,
+                                                   bool& ok) {
+  const int l = lane_id();
+  ok = r < (uint64_t)k;
+  uint32_t e[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) e[j] = l + kWave * j < k ? list[l + kWave * j] : 0u;
+  uint32_t prefix = 0, rr = ok ? (uint32_t)r : 0u;
+  for (int sh = ((nb + 7) / 8 - 1) * 8; sh >= 0; sh -= 8) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) hist[l + kWave * j] = 0;
+    wave_sync();
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (l + kWave * j < k && (sh + 8 >= 32 || (e[j] >> (sh + 8)) == (prefix >> (sh + 8))))
+        atomicAdd(&hist[(e[j] >> sh) & 255u], 1u);
+    wave_sync();
+    const uint4 hv = reinterpret_cast<const uint4*>(hist)[l];  // bins 4l .. 4l + 3
+    const uint32_t sum = hv.x + hv.y + hv.z + hv.w;
+    const uint32_t incl = wave_incl_scan(sum), excl = incl - sum;
+    const uint64_t bm = __ballot(excl <= rr && rr < incl);
+    const int owner = bm ? __builtin_ctzll(bm) : 0;
+    uint32_t d = 0, x = rr - excl;
+    if (x >= hv.x) {
+      x -= hv.x;
+      d = 1;
+      if (x >= hv.y) {
+        x -= hv.y;
+        d = 2;
+        if (x >= hv.z) {
+          x -= hv.z;
+          d = 3;
+        }
+      }
+    }
+    const uint32_t digit = 4u * (uint32_t)owner + __builtin_amdgcn_readlane(d, owner);
+    rr = __builtin_amdgcn_readlane(x, owner);
+    prefix |= digit << sh;
+    wave_sync();
+  }
+  return prefix;
+}
 
 __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) {
   __shared__ CellLds<1> L;
@@ -1590,10 +1639,12 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
     if (tid < kMaxT) L.tdone[tid] = tid < NT && L.tub[tid] - L.tlb[tid] <= 1 ? 1u : 0u;
     __syncthreads();
     while (true) {
-      // per target, uniform: range start, width (0 once resolved), digit shift (-1: gather)
+      // per target, uniform: range start, width (0 once resolved), digit
+      // shift (-1: gather); bit t of narrow: offsets in the range fit 32 bits
+      // (gathered as 4-byte offsets, up to kSelCap32 of them)
       uint64_t tlo[kMaxT], twd[kMaxT];
       int tsh[kMaxT];
-      uint32_t live = 0;
+      uint32_t live = 0, narrow = 0;
 #pragma unroll
       for (int t = 0; t < kMaxT; ++t) {
         tlo[t] = 0;
@@ -1603,12 +1654,16 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
           tlo[t] = readlane64(L.tlb[t], 0);
           twd[t] = readlane64(L.tub[t] - L.tlb[t], 0);
           const int bits = 64 - __builtin_clzll(twd[t] - 1);  // width >= 2
+          const bool nar = bits <= 32;
+          const uint32_t cap = nar ? (uint32_t)kSelCap32 : (uint32_t)kSelCap;
           tsh[t] = (int)__builtin_amdgcn_readfirstlane(
-              L.tpop[t] <= (uint32_t)kSelCap ? -1 : (bits > kSelDigit ? bits - kSelDigit : 0));
+              L.tpop[t] <= cap ? -1 : (bits > kSelDigit ? bits - kSelDigit : 0));
           live |= 1u << t;
+          narrow |= (nar ? 1u : 0u) << t;
         }
       }
       live = __builtin_amdgcn_readfirstlane(live);
+      narrow = __builtin_amdgcn_readfirstlane(narrow);
       if (live == 0) break;
       for (int i = tid; i < kMaxT * kSelRegion; i += kBlockThreads) L.buf[i] = 0;
       if (tid < kMaxT) L.tcnt[tid] = 0;
@@ -1626,8 +1681,11 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
             if (i0 + k * kBlockThreads < n && u < twd[t]) {
               if (tsh[t] < 0) {
                 const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
-                if (slot < (uint32_t)kSelCap)
+                if ((narrow >> t) & 1u) {
+                  if (slot < (uint32_t)kSelCap32) L.buf[t * kSelRegion + (int)slot] = (uint32_t)u;
+                } else if (slot < (uint32_t)kSelCap) {
                   reinterpret_cast<uint64_t*>(L.buf + t * kSelRegion)[slot] = v[k];
+                }
               } else {
                 atomicAdd(&L.buf[t * kSelRegion + (int)(u >> tsh[t])], 1u);
               }
@@ -1641,7 +1699,18 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
         if (!((live >> t) & 1u)) continue;
         const uint64_t r = readlane64(L.trank[t], 0);
         const uint64_t base = readlane64(L.tlb[t], 0);
-        if (tsh[t] < 0) {
+        if (tsh[t] < 0 && ((narrow >> t) & 1u)) {
+          // radix selection among the gathered offsets
+          const uint32_t got = L.tcnt[t];
+          const int k = got < (uint32_t)kSelCap32 ? (int)got : kSelCap32;
+          bool ok;
+          const uint32_t off = select_offsets(L.buf + t * kSelRegion, L.buf + t * kSelRegion + kSelCap32, k,
+                                              64 - __builtin_clzll(twd[t] - 1), r, ok);
+          if (l == 0) {
+            L.tlb[t] = ok ? base + off : base;
+            L.tdone[t] = 1;
+          }
+        } else if (tsh[t] < 0) {
           // counting rank among the gathered durations
           const uint64_t* list = reinterpret_cast<const uint64_t*>(L.buf + t * kSelRegion);
           const uint32_t got = L.tcnt[t];
