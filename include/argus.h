@@ -398,8 +398,13 @@ void argus_kde_default(argus_kde_params_t* p);
 size_t argus_kde_workspace(const argus_events_t* ev);
 
 /* ev: as for argus_summarize, n_kernels <= ARGUS_MAX_KDE_KERNELS.
- * sum: only count, min_ns and max_ns are read. out->count, p50_ns and p99_ns
- * must be 16-byte aligned. The workspace must be 256-byte aligned. */
+ * sum: count, min_ns and max_ns are read, and n_invalid unless it is NULL: a
+ * segment whose n_invalid is 0 holds only valid events, so for id spaces of
+ * up to 2,048 kernel ids its stream array is not read (a sixth of the input
+ * bytes). sum must be the argus_summarize output of these same events; a
+ * summary that does not match them makes the cells concerned report
+ * ARGUS_DEV_KDE_SUMMARY. out->count, p50_ns and p99_ns must be 16-byte
+ * aligned. The workspace must be 256-byte aligned. */
 int argus_kde(const argus_events_t* ev, const argus_summary_t* sum, const argus_kde_params_t* params,
               const argus_kde_out_t* out, void* workspace, size_t workspace_bytes, void* stream);
 

@@ -364,7 +364,8 @@ def kde(ev: dict, summary: dict, n_ranks: int, n_steps: int, n_kernels: int, n_s
     for k, v in params.items():
         setattr(p, k, v)
     e = _events(ev, n_ranks, n_steps, n_kernels, n_streams)
-    s = Summary(*[_ptr(summary.get(f)) if f in ("count", "min_ns", "max_ns") else None for f in SUMMARY_FIELDS])
+    s = Summary(*[_ptr(summary.get(f)) if f in ("count", "min_ns", "max_ns", "n_invalid") else None
+                  for f in SUMMARY_FIELDS])
     o = KdeOut(*[_ptr(out.get(f)) for f in KDE_FIELDS])
     ws = out["_workspace"]
     _check(lib().argus_kde(ctypes.byref(e), ctypes.byref(s), ctypes.byref(p), ctypes.byref(o), _ptr(ws),

@@ -256,7 +256,8 @@ int argus_kde(const argus_events_t* ev, const argus_summary_t* sum, const argus_
   int rc = check_device();
   if (rc != ARGUS_OK) return rc;
   KdeLaunch l{ev->kernel_id, ev->stream, ev->start_ns, ev->end_ns, ev->seg_off, ev->n_events, (int32_t)n_seg,
-              ev->n_kernels, ev->n_streams, sum->count, sum->min_ns, sum->max_ns, p, *out, workspace};
+              ev->n_kernels, ev->n_streams, sum->count, sum->min_ns, sum->max_ns, sum->n_invalid, p, *out,
+              workspace};
   return status_of(launch_kde(l, (hipStream_t)stream));
 }
 

@@ -143,6 +143,7 @@ struct KdeLaunch {
   const uint32_t* count;
   const int64_t* min_ns;
   const int64_t* max_ns;
+  const uint32_t* n_invalid;  // per segment, or null
   argus_kde_params_t p;
   argus_kde_out_t o;
   void* workspace;  // kde_workspace_bytes(n_events, n_seg, n_seg * n_kernels), 256-byte aligned

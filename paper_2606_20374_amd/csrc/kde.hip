@@ -89,6 +89,7 @@ struct KdeArgs {
   const uint32_t* count;
   const int64_t* min_ns;
   const int64_t* max_ns;
+  const uint32_t* n_invalid;  // per segment, or null
   uint8_t* n_clusters;
   uint32_t* cl_count;
   int64_t* p50;
@@ -486,8 +487,11 @@ __device__ __forceinline__ void stage_write(const StageCtx<R>& s, __amdgpu_buffe
 }
 
 // One well-formed segment [lo, hi) of the staged scatter, the cursors set up;
-// returns with every staged position written out.
-template <typename R>
+// returns with every staged position written out. Without STREAMS the stream
+// array is not read and every stream counts as valid: the segment's summary
+// found no invalid event, so every stream is in range (the other validity
+// tests stay, as they use what is read anyway).
+template <typename R, bool STREAMS>
 __device__ void stage_segment(const KdeArgs& a, const StageCtx<R>& s, uint32_t* done, FlushEntry* list,
                               uint32_t* n_list, int64_t lo, int64_t hi, int tid) {
   const v4i* K4 = reinterpret_cast<const v4i*>(a.kernel_id);
@@ -502,9 +506,9 @@ __device__ void stage_segment(const KdeArgs& a, const StageCtx<R>& s, uint32_t* 
   }
   // head [lo, a4) (the whole segment without aligned arrays) and tail [b4, hi)
   for (int64_t i = lo + tid; i < a4; i += kStageThreads)
-    stage_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
+    stage_one(s, a.kernel_id[i], STREAMS ? a.stream[i] : 0, a.start_ns[i], a.end_ns[i]);
   for (int64_t i = b4 + tid; i < hi; i += kStageThreads)
-    stage_one(s, a.kernel_id[i], a.stream[i], a.start_ns[i], a.end_ns[i]);
+    stage_one(s, a.kernel_id[i], STREAMS ? a.stream[i] : 0, a.start_ns[i], a.end_ns[i]);
   const int64_t qa = a4 >> 2, qb = b4 >> 2;
   if (hi - lo <= kBufEvents) {
     // rounds of kStageD groups of four events per thread with the next
@@ -519,7 +523,7 @@ __device__ void stage_segment(const KdeArgs& a, const StageCtx<R>& s, uint32_t* 
     auto load = [&](int d, int64_t rq) {
       const uint32_t o16 = rq < ng ? (uint32_t)rq * 16u : kOob, o32 = rq < ng ? (uint32_t)rq * 32u : kOob;
       bk[d] = __builtin_amdgcn_raw_buffer_load_b128(rk, (int)o16, 0, 0);
-      bs[d] = __builtin_amdgcn_raw_buffer_load_b128(rs, (int)o16, 0, 0);
+      bs[d] = STREAMS ? __builtin_amdgcn_raw_buffer_load_b128(rs, (int)o16, 0, 0) : v4u{0u, 0u, 0u, 0u};
       ba0[d] = __builtin_amdgcn_raw_buffer_load_b128(r0, (int)o32, 0, 0);
       ba1[d] = __builtin_amdgcn_raw_buffer_load_b128(r0, (int)(o32 + 16u), 0, 0);
       bb0[d] = __builtin_amdgcn_raw_buffer_load_b128(r1, (int)o32, 0, 0);
@@ -558,7 +562,7 @@ __device__ void stage_segment(const KdeArgs& a, const StageCtx<R>& s, uint32_t* 
         ba0[d] = ba1[d] = bb0[d] = bb1[d] = 0;
         if (q < qb) {
           bk[d] = __builtin_nontemporal_load(K4 + q);
-          bs[d] = __builtin_nontemporal_load(S4 + q);
+          if (STREAMS) bs[d] = __builtin_nontemporal_load(S4 + q);
           ba0[d] = __builtin_nontemporal_load(T0 + 2 * q);
           ba1[d] = __builtin_nontemporal_load(T0 + 2 * q + 1);
           bb0[d] = __builtin_nontemporal_load(T1 + 2 * q);
@@ -574,7 +578,7 @@ __device__ void stage_segment(const KdeArgs& a, const StageCtx<R>& s, uint32_t* 
           const int64_t qn = q + (int64_t)kStageD * kStageThreads;
           if (qn < qb) {
             bk[d] = __builtin_nontemporal_load(K4 + qn);
-            bs[d] = __builtin_nontemporal_load(S4 + qn);
+            if (STREAMS) bs[d] = __builtin_nontemporal_load(S4 + qn);
             ba0[d] = __builtin_nontemporal_load(T0 + 2 * qn);
             ba1[d] = __builtin_nontemporal_load(T0 + 2 * qn + 1);
             bb0[d] = __builtin_nontemporal_load(T1 + 2 * qn);
@@ -645,16 +649,20 @@ __global__ __launch_bounds__(kStageThreads) void kde_scatter_staged_kernel(KdeAr
     const int64_t lo = a.seg_off[g], hi = a.seg_off[g + 1];
     const bool bad = !(lo >= 0 && lo <= hi && hi <= a.n_events && hi - lo <= (int64_t)UINT32_MAX);
     const bool w4 = !bad && hi - lo <= kBufEvents && !wide;
+    // a segment whose summary counted no invalid event skips the stream array
+    const bool streams = !(a.n_invalid && a.n_invalid[g] == 0);
     if (tid == 0) a.seg_w4[g] = w4 ? 1 : 0;
     lds_barrier();
     if (w4) {
       const StageCtx<uint32_t> s{stage.w4, cur, done, reinterpret_cast<uint32_t*>(a.bucket + lo),
                                  (uint32_t)(hi - lo), (uint32_t)((2 * lo) & 15), K, a.NS};
-      stage_segment(a, s, done, list, &n_list, lo, hi, tid);
+      if (streams) stage_segment<uint32_t, true>(a, s, done, list, &n_list, lo, hi, tid);
+      else stage_segment<uint32_t, false>(a, s, done, list, &n_list, lo, hi, tid);
     } else if (!bad) {
       const StageCtx<uint64_t> s{stage.w8, cur, done, a.bucket + lo, (uint32_t)(hi - lo), (uint32_t)(lo & 7), K,
                                  a.NS};
-      stage_segment(a, s, done, list, &n_list, lo, hi, tid);
+      if (streams) stage_segment<uint64_t, true>(a, s, done, list, &n_list, lo, hi, tid);
+      else stage_segment<uint64_t, false>(a, s, done, list, &n_list, lo, hi, tid);
     }
     lds_barrier();
     uint32_t* ends = a.cell_end + (int64_t)g * K;
@@ -2366,6 +2374,7 @@ hipError_t launch_kde(const KdeLaunch& l, hipStream_t st) {
   a.count = l.count;
   a.min_ns = l.min_ns;
   a.max_ns = l.max_ns;
+  a.n_invalid = l.n_invalid;
   a.n_clusters = l.o.n_clusters;
   a.cl_count = l.o.count;
   a.p50 = l.o.p50_ns;

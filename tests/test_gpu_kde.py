@@ -97,6 +97,31 @@ def test_kde_ragged_corrupt_and_malformed():
     assert int(k["dev_status"].item()) == 0
 
 
+def test_kde_stream_array_skipped_only_for_valid_segments():
+    """Segments whose summary counts no invalid event are scattered without
+    reading the stream array; the clusters equal those of the full read (no
+    n_invalid passed) and the oracle's, with invalid events (bad streams
+    among them) in the other segments of the same call."""
+    _announce("kde stream array skipped for all-valid segments")
+    lens = np.array([0, 5, 40, 3000, 20_000, 7, 1, 12_345] * 4)
+    t = tracegen.make("tiny", invalid_ppm=300, seg_lengths=lens)
+    c = t.cfg
+    ev = t.fill_host()
+    R, S, K, NS = c.n_ranks, c.n_steps, c.n_kernels, c.n_streams
+    ev_d = _dev(ev)
+    s = pa.summarize(ev_d, R, S, K, NS)
+    n_inv = s["n_invalid"].cpu().numpy()
+    assert (n_inv == 0).sum() >= 8 and (n_inv > 0).sum() >= 4, n_inv
+    k_skip = pa.kde(ev_d, s, R, S, K, NS)
+    k_full = pa.kde(ev_d, {f: v for f, v in s.items() if f != "n_invalid"}, R, S, K, NS)
+    torch.cuda.synchronize()
+    for f in ("n_clusters", "count", "p50_ns", "p99_ns", "bw_q8", "dev_status"):
+        assert torch.equal(k_skip[f], k_full[f]), f
+    o = oracle.kde(ev, K, NS, n_events=len(ev["kernel_id"]))
+    P.assert_kde_equal(k_skip, o, "stream skip")
+    assert int(k_skip["dev_status"].item()) == 0
+
+
 def _groups_to_events(groups, K, NS, seed=0):
     """One segment; groups: list of duration arrays, group i -> kernel id i."""
     rng = np.random.default_rng(seed)
