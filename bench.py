@@ -401,11 +401,19 @@ def main():
         # summary record per present cell: kernel id 4 B + cluster count 1 B,
         # then (count 4, p50 8, p99 8) per cluster
         wire = int(5 * np.count_nonzero(ncl) + 20 * ncl.astype(np.int64).sum())
-        # algorithmic bytes: every event read once (24 B), each cell's count /
-        # min / max read (20 B) and its record written (n_clusters 1, count 16,
-        # p50 32, p99 32, bw 4 = 85 B); the bucketed durations the kernels
-        # write and re-read are the design's, not the operation's
-        kde_alg = 24 * trace.n_events + (20 + 85) * G * K
+        # algorithmic bytes: every event's kernel id, start and end read once
+        # (20 B) and its stream (4 B) where validity is not known from the
+        # summary (a rank-step with invalid events, or id spaces beyond 2,048,
+        # whose scatter reads every field); each rank-step's n_invalid (4 B);
+        # each cell's count / min / max read (20 B) and its record written
+        # (n_clusters 1, count 16, p50 32, p99 32, bw 4 = 85 B). The bucketed
+        # durations the kernels write and re-read are the design's, not the
+        # operation's.
+        seg_events = torch.diff(ev["seg_off"]).to(torch.int64)
+        inv = (s["n_invalid"].to(torch.int64) & 0xFFFFFFFF) > 0
+        stream_events = trace.n_events if K > 2048 else int(seg_events[inv].sum().item())
+        ev_bytes = 20 * trace.n_events + 4 * stream_events + 4 * G
+        kde_alg = ev_bytes + (20 + 85) * G * K
         # the scatter writes each valid duration once, in 4 bytes where every
         # present cell of its rank-step has a maximum below 2^31 ns, else 8
         wide = ((s["max_ns"] >= 2**31) & (s["count"] > 0)).view(G, K).any(dim=1)
@@ -416,7 +424,7 @@ def main():
             "roofline": {"bound": "hbm", "achieved": kde_alg / (kde_ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
                          "unit": "GB/s", "frac": kde_alg / (kde_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                          "algorithmic_bytes_per_call": kde_alg},
-            "scatter_algorithmic_bytes": 24 * trace.n_events + rec_bytes + 8 * G * K,
+            "scatter_algorithmic_bytes": ev_bytes + rec_bytes + 8 * G * K,
             "cells": G * K, "present_cells": int(np.count_nonzero(ncl)),
             "mean_clusters_per_present_cell": float(ncl[ncl > 0].mean()) if (ncl > 0).any() else 0.0,
             "cells_with_several_clusters": int((ncl > 1).sum()),
