@@ -121,6 +121,7 @@ struct KdeArgs {
 
 // the grid index of a duration (kde_math.h)
 __device__ __forceinline__ int grid64(uint64_t d, const uint32_t* th) { return kde_grid64(d, th); }
+__device__ __forceinline__ int grid32(uint32_t d, const uint32_t* th) { return kde_grid32(d, th); }
 
 // Smallest duration whose 64-per-octave grid value is >= b.
 __device__ __forceinline__ uint64_t grid64_lb(int b, const uint32_t* th) {
@@ -1190,27 +1191,35 @@ __device__ bool kde_one_cell(const KdeArgs& a, CellLds<TIER>& L, int64_t c, cons
   for (int j = l; j < G; j += kWave) cgrid[j] = 0;
   wave_sync();
   bool out_of_range = false;
+  // 4-byte records (the cell's flag is wavefront-uniform): grid indices
+  // from 32-bit operations
+  auto add = [&](int x) {
+    if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
+    else out_of_range = true;
+  };
   if (in_regs) {
+    if (vals.w4) {
 #pragma unroll
-    for (int r = 0; r < kRegVals; ++r) {
-      const uint32_t i = (uint32_t)(l + r * kWave);
-      if (i < n) {
-        const int x = (grid64(rv[r], L.th) >> sh) - lo;
-        if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
-        else out_of_range = true;
-      }
+      for (int r = 0; r < kRegVals; ++r)
+        if ((uint32_t)(l + r * kWave) < n) add((grid32((uint32_t)rv[r], L.th) >> sh) - lo);
+    } else {
+#pragma unroll
+      for (int r = 0; r < kRegVals; ++r)
+        if ((uint32_t)(l + r * kWave) < n) add((grid64(rv[r], L.th) >> sh) - lo);
     }
   } else {
     // four loads in flight per lane
     for (uint64_t i0 = l; i0 < n; i0 += 4 * kWave) {
       uint64_t v[4];
       vals.get(i0, kWave, n, v, 0ull);
+      if (vals.w4) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (i0 + u * kWave >= n) break;
-        const int x = (grid64(v[u], L.th) >> sh) - lo;
-        if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
-        else out_of_range = true;
+        for (int u = 0; u < 4; ++u)
+          if (i0 + u * kWave < n) add((grid32((uint32_t)v[u], L.th) >> sh) - lo);
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (i0 + u * kWave < n) add((grid64(v[u], L.th) >> sh) - lo);
       }
     }
   }
@@ -1603,15 +1612,36 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
     for (int j = tid; j < G; j += kBlockThreads) cgrid[j] = 0;
     __syncthreads();
     bool out_of_range = false;
-    for (uint64_t i0 = tid; i0 < n; i0 += kBlockDepth * kBlockThreads) {
-      uint64_t v[kBlockDepth];
-      vals.get(i0, kBlockThreads, n, v, 0ull);
+    if (vals.w4) {
+      // 4-byte records: 32-bit loads and grid indices
+      const uint32_t* q = static_cast<const uint32_t*>(vals.p);
+      const uint32_t n32 = (uint32_t)n;
+      for (uint32_t i0 = (uint32_t)tid; i0 < n32; i0 += kBlockDepth * kBlockThreads) {
+        uint32_t v[kBlockDepth];
 #pragma unroll
-      for (int u = 0; u < kBlockDepth; ++u) {
-        if (i0 + u * kBlockThreads >= n) break;
-        const int x = (grid64(v[u], L.th) >> sh) - lo;
-        if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
-        else out_of_range = true;
+        for (int u = 0; u < kBlockDepth; ++u) {
+          const uint32_t i = i0 + (uint32_t)(u * kBlockThreads);
+          v[u] = i < n32 ? q[i] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kBlockDepth; ++u) {
+          if (i0 + (uint32_t)(u * kBlockThreads) >= n32) break;
+          const int x = (grid32(v[u], L.th) >> sh) - lo;
+          if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
+          else out_of_range = true;
+        }
+      }
+    } else {
+      for (uint64_t i0 = tid; i0 < n; i0 += kBlockDepth * kBlockThreads) {
+        uint64_t v[kBlockDepth];
+        vals.get(i0, kBlockThreads, n, v, 0ull);
+#pragma unroll
+        for (int u = 0; u < kBlockDepth; ++u) {
+          if (i0 + u * kBlockThreads >= n) break;
+          const int x = (grid64(v[u], L.th) >> sh) - lo;
+          if (x >= 0 && x < G) atomicAdd(&cgrid[x], 1u);
+          else out_of_range = true;
+        }
       }
     }
     if (out_of_range) s_bad = 1;
@@ -1676,26 +1706,64 @@ __global__ __launch_bounds__(kBlockThreads, 4) void kde_block_kernel(KdeArgs a) 
       for (int i = tid; i < kMaxT * kSelRegion; i += kBlockThreads) L.buf[i] = 0;
       if (tid < kMaxT) L.tcnt[tid] = 0;
       __syncthreads();
-      // live targets outer (a uniform test each), the loaded durations inner
-      for (uint64_t i0 = tid; i0 < n; i0 += kBlockDepth * kBlockThreads) {
-        uint64_t v[kBlockDepth];
-        vals.get(i0, kBlockThreads, n, v, 0ull);
+      // 4-byte records whose live target ranges all end at or below 2^32:
+      // the same tests on 32-bit offsets (every such range is narrow, so its
+      // candidates are gathered as offsets), half the arithmetic per test
+      bool t32 = vals.w4;
 #pragma unroll
-        for (int t = 0; t < kMaxT; ++t) {
-          if (!((live >> t) & 1u)) continue;
+      for (int t = 0; t < kMaxT; ++t)
+        if ((live >> t) & 1u)
+          t32 = t32 && tlo[t] < (1ull << 32) && twd[t] < (1ull << 32) && twd[t] <= (1ull << 32) - tlo[t];
+      if (t32) {
+        const uint32_t* q = static_cast<const uint32_t*>(vals.p);
+        const uint32_t n32 = (uint32_t)n;
+        for (uint32_t i0 = (uint32_t)tid; i0 < n32; i0 += kBlockDepth * kBlockThreads) {
+          uint32_t v[kBlockDepth];
 #pragma unroll
           for (int k = 0; k < kBlockDepth; ++k) {
-            const uint64_t u = v[k] - tlo[t];
-            if (i0 + k * kBlockThreads < n && u < twd[t]) {
-              if (tsh[t] < 0) {
-                const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
-                if ((narrow >> t) & 1u) {
-                  if (slot < (uint32_t)kSelCap32) L.buf[t * kSelRegion + (int)slot] = (uint32_t)u;
-                } else if (slot < (uint32_t)kSelCap) {
-                  reinterpret_cast<uint64_t*>(L.buf + t * kSelRegion)[slot] = v[k];
+            const uint32_t i = i0 + (uint32_t)(k * kBlockThreads);
+            v[k] = i < n32 ? q[i] : 0u;
+          }
+#pragma unroll
+          for (int t = 0; t < kMaxT; ++t) {
+            if (!((live >> t) & 1u)) continue;
+            const uint32_t lo32 = (uint32_t)tlo[t], wd32 = (uint32_t)twd[t];
+#pragma unroll
+            for (int k = 0; k < kBlockDepth; ++k) {
+              const uint32_t u = v[k] - lo32;
+              if (i0 + (uint32_t)(k * kBlockThreads) < n32 && u < wd32) {
+                if (tsh[t] < 0) {
+                  const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
+                  if (slot < (uint32_t)kSelCap32) L.buf[t * kSelRegion + (int)slot] = u;
+                } else {
+                  atomicAdd(&L.buf[t * kSelRegion + (int)(u >> tsh[t])], 1u);
                 }
-              } else {
-                atomicAdd(&L.buf[t * kSelRegion + (int)(u >> tsh[t])], 1u);
+              }
+            }
+          }
+        }
+      } else {
+        // live targets outer (a uniform test each), the loaded durations inner
+        for (uint64_t i0 = tid; i0 < n; i0 += kBlockDepth * kBlockThreads) {
+          uint64_t v[kBlockDepth];
+          vals.get(i0, kBlockThreads, n, v, 0ull);
+#pragma unroll
+          for (int t = 0; t < kMaxT; ++t) {
+            if (!((live >> t) & 1u)) continue;
+#pragma unroll
+            for (int k = 0; k < kBlockDepth; ++k) {
+              const uint64_t u = v[k] - tlo[t];
+              if (i0 + k * kBlockThreads < n && u < twd[t]) {
+                if (tsh[t] < 0) {
+                  const uint32_t slot = atomicAdd(&L.tcnt[t], 1u);
+                  if ((narrow >> t) & 1u) {
+                    if (slot < (uint32_t)kSelCap32) L.buf[t * kSelRegion + (int)slot] = (uint32_t)u;
+                  } else if (slot < (uint32_t)kSelCap) {
+                    reinterpret_cast<uint64_t*>(L.buf + t * kSelRegion)[slot] = v[k];
+                  }
+                } else {
+                  atomicAdd(&L.buf[t * kSelRegion + (int)(u >> tsh[t])], 1u);
+                }
               }
             }
           }
@@ -1881,16 +1949,23 @@ __device__ bool lane_cell(const KdeArgs& a, LaneLds<GC>& L, int64_t c, const Cel
   // return nothing, so no iteration waits on the previous one
   for (int j = 0; j < G; ++j) L.cp[j][l] = 0;
   bool out_of_range = false;
+  // the lane's count byte lives in a word shared with three other lanes
+  auto add = [&](int x) {
+    if (x >= 0 && x < G) atomicAdd(reinterpret_cast<uint32_t*>(&L.cp[x][l & ~3]), 1u << ((l & 3) * 8));
+    else out_of_range = true;
+  };
   for (uint32_t i0 = 0; i0 < n; i0 += 8) {
     uint64_t d[8];
     vals.run8(i0, n, d, 0ull);
+    // 4-byte records: grid indices from 32-bit operations
+    if (vals.w4) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (i0 + u >= n) break;
-      const int x = (grid64(d[u], L.th) >> sh) - lo;
-      // the lane's count byte lives in a word shared with three other lanes
-      if (x >= 0 && x < G) atomicAdd(reinterpret_cast<uint32_t*>(&L.cp[x][l & ~3]), 1u << ((l & 3) * 8));
-      else out_of_range = true;
+      for (int u = 0; u < 8; ++u)
+        if (i0 + u < n) add((grid32((uint32_t)d[u], L.th) >> sh) - lo);
+    } else {
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (i0 + u < n) add((grid64(d[u], L.th) >> sh) - lo);
     }
   }
   uint32_t cnt[kMaxC] = {0, 0, 0, 0};

@@ -62,11 +62,9 @@ inline const uint32_t* kde_thresholds() {
 // estimate's bracket [th[t], th[t + 1]) is read at once, a result equal to
 // the estimate is proved by those two comparisons, and only an estimate off
 // by a step (a mantissa next to a threshold) walks the table to the exact
-// index.
-__device__ __forceinline__ int kde_grid64(uint64_t d, const uint32_t* th) {
-  if (d < 2) return 0;
-  const int e = 63 - __builtin_clzll(d);
-  const uint32_t m = e >= 23 ? (uint32_t)(d >> (e - 23)) : (uint32_t)(d << (23 - e));
+// index. kde_grid_of_mantissa takes d's exponent e = floor(log2 d) and m = d'
+// (in [2^23, 2^24)).
+__device__ __forceinline__ int kde_grid_of_mantissa(int e, uint32_t m, const uint32_t* th) {
   int t0 = (int)((__log2f((float)m) - 23.0f) * 64.0f);
   t0 = t0 < 0 ? 0 : (t0 > 63 ? 63 : t0);
   const uint32_t a0 = th[t0], a1 = th[t0 < 63 ? t0 + 1 : 63];
@@ -77,6 +75,20 @@ __device__ __forceinline__ int kde_grid64(uint64_t d, const uint32_t* th) {
     while (t < 63 && m >= th[t + 1]) ++t;
   }
   return e * 64 + t;
+}
+
+__device__ __forceinline__ int kde_grid64(uint64_t d, const uint32_t* th) {
+  if (d < 2) return 0;
+  const int e = 63 - __builtin_clzll(d);
+  return kde_grid_of_mantissa(e, e >= 23 ? (uint32_t)(d >> (e - 23)) : (uint32_t)(d << (23 - e)), th);
+}
+
+// The same index for a duration held in 32 bits (4-byte records): the same
+// exponent and mantissa from 32-bit operations.
+__device__ __forceinline__ int kde_grid32(uint32_t d, const uint32_t* th) {
+  if (d < 2) return 0;
+  const int e = 31 - __builtin_clz(d);
+  return kde_grid_of_mantissa(e, e >= 23 ? d >> (e - 23) : d << (23 - e), th);
 }
 
 // Sign of c^5 n - 2^e, exactly (c < 2^55, n < 2^33, so the product has at

@@ -46,6 +46,15 @@ __global__ void grid_kernel(const uint64_t* d, int64_t m, Thresholds t, int32_t*
   if (i < m) out[i] = argus::kde_grid64(d[i], th);
 }
 
+// The 32-bit form the kernels use for 4-byte records (durations below 2^32).
+__global__ void grid32_kernel(const uint32_t* d, int64_t m, Thresholds t, int32_t* out) {
+  __shared__ uint32_t th[64];
+  if (threadIdx.x < 64) th[threadIdx.x] = t.th[threadIdx.x];
+  __syncthreads();
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < m) out[i] = argus::kde_grid32(d[i], th);
+}
+
 int status(hipError_t e) { return e == hipSuccess ? 0 : -3; }
 
 }  // namespace
@@ -70,6 +79,16 @@ int probe_kde_grid(const uint64_t* d, int64_t m, int32_t* out, void* stream) {
   const uint32_t* th = argus::kde_thresholds();
   for (int i = 0; i < 64; ++i) t.th[i] = th[i];
   hipLaunchKernelGGL(grid_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, (hipStream_t)stream, d, m, t, out);
+  return status(hipGetLastError());
+}
+
+int probe_kde_grid32(const uint32_t* d, int64_t m, int32_t* out, void* stream) {
+  if (m <= 0) return 0;
+  Thresholds t;
+  const uint32_t* th = argus::kde_thresholds();
+  for (int i = 0; i < 64; ++i) t.th[i] = th[i];
+  hipLaunchKernelGGL(grid32_kernel, dim3((unsigned)((m + 255) / 256)), dim3(256), 0, (hipStream_t)stream, d, m, t,
+                     out);
   return status(hipGetLastError());
 }
 

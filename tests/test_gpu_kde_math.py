@@ -19,7 +19,8 @@ they must equal the oracle's bit for bit:
 The grid index of a duration (an integer result that a hardware log2
 estimate only starts) must equal the oracle's exact one for every duration
 below 2^20, every threshold of every octave and its two neighbours, and 2^22
-log-uniform random durations.
+log-uniform random durations; so must the 32-bit form the kernels use for
+4-byte records, on every one of those durations below 2^32.
 The full-size KDE parity tests compare the bandwidth and clusters of every
 cell of the benchmarked workloads on top of this.
 """
@@ -48,6 +49,7 @@ def _probe():
     L.probe_kde_root5.argtypes = [V, ctypes.c_int64, V, V]
     L.probe_kde_bw_q8.argtypes = [V, V, V, ctypes.c_int64, V, V]
     L.probe_kde_grid.argtypes = [V, ctypes.c_int64, V, V]
+    L.probe_kde_grid32.argtypes = [V, ctypes.c_int64, V, V]
     return L
 
 
@@ -121,7 +123,7 @@ def test_bandwidth_matches_the_host():
 
 
 def test_grid_index_matches_the_oracle():
-    print("\n[gpu-case] kde grid index: d < 2^20, every threshold of every octave +-1, 2^22 random", flush=True)
+    print("\n[gpu-case] kde grid index (64- and 32-bit forms): d < 2^20, every threshold of every octave +-1, 2^22 random", flush=True)
     th = oracle.kde_thresholds().astype(np.uint64)
     parts = [np.arange(1 << 20, dtype=np.uint64)]
     # every threshold of every octave and its neighbours: for octaves below
@@ -145,3 +147,13 @@ def test_grid_index_matches_the_oracle():
     got = out.cpu().numpy()
     bad = np.flatnonzero(got != want)
     assert bad.size == 0, (bad.size, d[bad[:5]], got[bad[:5]], want[bad[:5]])
+    # the 32-bit form (4-byte records) on every sampled duration below 2^32
+    sel = d < np.uint64(1 << 32)
+    d32, want32 = d[sel].astype(np.uint32), want[sel]
+    assert d32.size > (1 << 20) and int(d32.max()) > (1 << 31)
+    out32 = torch.empty(d32.size, dtype=torch.int32, device=DEV)
+    assert _probe().probe_kde_grid32(_dev(d32.view(np.int32)).data_ptr(), d32.size, out32.data_ptr(), _stream()) == 0
+    torch.cuda.synchronize()
+    got32 = out32.cpu().numpy()
+    bad = np.flatnonzero(got32 != want32)
+    assert bad.size == 0, (bad.size, d32[bad[:5]], got32[bad[:5]], want32[bad[:5]])
