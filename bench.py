@@ -200,7 +200,7 @@ def main():
     ap.add_argument("--compact-reps", type=int, default=5, help="timed argus_compact calls (0: skip that leg)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+        print(f"bench.py runs on one GPU only: libargus has no multi-GPU path (asked for --gpus {args.gpus}).",
               file=sys.stderr)
         sys.exit(2)
 
