@@ -7,8 +7,9 @@ variants, ragged / corrupted / malformed segments, hand-built groups that
 exercise every filter rule and both LDS paths (cells whose grid, kernel or
 valley list do not fit the fast path are finished by the large-LDS path),
 summaries that do not match the events, segments of 4-byte and 8-byte
-bucket records in one call, and full-size workloads (sampled segments checked
-against the oracle).
+bucket records in one call, a rank-step longer than 2^26 events (the
+scatter's global-load path), the stream array skipped or read, and full-size
+workloads (sampled segments checked against the oracle).
 """
 import gc
 
@@ -326,6 +327,38 @@ def test_kde_record_widths_mixed():
     assert int(k2["n_clusters"][bad].item()) == 0
     keep = np.setdiff1d(np.arange(R * S * K), [bad])
     P.assert_kde_equal(k2, {f: np.asarray(o[f])[keep] for f in P.KDE_FIELDS}, "understated maximum", rows=keep)
+
+
+def test_kde_long_segment_global_path():
+    """A rank-step of more than 2^26 events is scattered with global loads and
+    8-byte records (the buffer path covers shorter ones); with the stream
+    array skipped (its summary counts no invalid event) and read (no
+    n_invalid passed) its clusters equal the oracle's."""
+    _announce("kde long rank-step (2^26 + 4093 events): global-load scatter path")
+    lens = np.array([2**26 + 4093] + [3000] * 31)
+    t = tracegen.make("tiny", seg_lengths=lens)
+    c = t.cfg
+    R, S, K, NS = c.n_ranks, c.n_steps, c.n_kernels, c.n_streams
+    n = int(lens.sum())
+    ev_d = t.fill_device(device=DEV)
+    s = pa.summarize(ev_d, R, S, K, NS)
+    k_skip = pa.kde(ev_d, s, R, S, K, NS)
+    torch.cuda.synchronize()
+    assert int(k_skip["dev_status"].item()) == 0
+    assert list(_record_widths(k_skip, n, R * S, R * S * K)) == [0] + [1] * (R * S - 1)
+    got = {f: k_skip[f].cpu() for f in P.KDE_FIELDS}
+    del k_skip
+    k_full = pa.kde(ev_d, {f: v for f, v in s.items() if f != "n_invalid"}, R, S, K, NS)
+    torch.cuda.synchronize()
+    for f in P.KDE_FIELDS:
+        assert torch.equal(got[f], k_full[f].cpu()), f
+    del k_full, ev_d, s
+    gc.collect()
+    torch.cuda.empty_cache()
+    ev_h = t.fill_host(0, 1)
+    o = oracle.kde(ev_h, K, NS, n_events=len(ev_h["kernel_id"]))
+    assert (o["n_clusters"] > 1).sum() > 8  # multimodal kernels are present
+    P.assert_kde_equal(got, o, "long rank-step", rows=np.arange(K))
 
 
 @pytest.mark.parametrize("name,n_check", [("production", 96), ("cluster", 48), ("skew", 48)])
