@@ -126,14 +126,25 @@ __device__ __forceinline__ void cluster_ab(const W1Args& a, int64_t c, uint32_t 
   if (y < x) y = x;
 }
 
+// floor(a / b) for a < 2^53, 1 <= b < 2^53: both are exact doubles, and the
+// correctly rounded quotient truncates to the exact floor or one above it
+// (never below: the floor is representable), which one exact product detects.
+__device__ __forceinline__ uint64_t floor_div53(uint64_t a, uint64_t b) {
+  uint64_t q = (uint64_t)((double)a / (double)b);
+  if (q * b > a) --q;
+  return q;
+}
+
 // floor(x^2 / y) and min(ceil(y^2 / x), INT64_MAX), for 1 <= x <= y: the
 // lognormal's mirror of its 99th percentile below the median, and its
 // 99.99th percentile.
 __device__ __forceinline__ uint64_t lo_of(uint64_t x, uint64_t y) {
+  if (x < (1ull << 26) && y < (1ull << 53)) return floor_div53(x * x, y);
   if (x < (1ull << 32)) return (x * x) / y;
   return (uint64_t)(((u128)x * x) / y);
 }
 __device__ __forceinline__ uint64_t hi_of(uint64_t x, uint64_t y) {
+  if (y < (1ull << 26)) return floor_div53(y * y + (x - 1), x);  // x <= y
   u128 q;
   if (y < (1ull << 32))
     q = (y * y + (x - 1)) / x;
